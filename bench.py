@@ -1,0 +1,228 @@
+"""Throughput of the cached mixed-precision EmbeddingBag training step on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--config industrial] [--gpus 1]
+
+One step = forward (tag probe, gather + dequantize, sum-pool) + backward_update
+(sort/de-dup, merged gradients, priority update, replacement, optimizer, write-back,
+evict/fill) over one batch of synthetic Zipf-skewed lookups already resident in
+HBM.  Prints one JSON line: pooled lookups/s (value), algorithmic HBM GB/s, the
+roofline of the dominant kernel, and the CPU oracle timed on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2010_11305_amd import configs, workload  # noqa: E402
+
+METRIC = "pooled lookups/sec + achieved HBM GB/s (fwd+bwd+update), 1 MI355X"
+HBM_PEAK_GBS = 8000.0
+
+
+def describe(cfg):
+    T, N = len(cfg["rows"]), cfg["rows"][0]
+    pool = cfg["pooling"]
+    return (f"{cfg['name']}: {T} tables x {N} rows x d{cfg['dim']} INT{cfg['bits']} + "
+            f"{'FP16' if cfg['sb_fp16'] else 'FP32'} (s,b); FP32 cache {cfg['cache_fraction']:.0%} "
+            f"{cfg['assoc']}-way {cfg['policy'].upper()}; B={cfg['batch']} bags/table, pooling {pool}; "
+            f"Zipf {cfg['zipf']}; {cfg['optimizer']} lr {cfg['lr']}; {cfg['rounding']} rounding")
+
+
+def algorithmic_bytes(cfg, st, B, decay_step=False):
+    """Bytes the method must move for one table and one step (each unique row once).
+
+    Forward:  4L + 4(B+1) indices/offsets, 4*assoc*U tag probes, 4d*U_h cached rows,
+              rho*U_m low-precision rows, 4dB pooled output.
+    Backward: 4L + 4(B+1), 4dB output gradients, row re-read (4d*U_h + rho*U_m),
+              row writes (4d*(U_h - E_h) + rho*(E_h + U_byp) + 4d*U_ins), displaced
+              residents V_o*(4d + rho), tags + stamps of inserts (8 U_ins) and stamps
+              of hits (4 U_h, LRU), Adagrad (8 U), LFU counts (8 U, + 8N on decay steps).
+    """
+    d = cfg["dim"]
+    phi = 4 * d
+    rho = d * cfg["bits"] // 8 + (4 if cfg["sb_fp16"] else 8)
+    L, U, Uh = st["bwd_lookups"], st["unique"], st["unique_hits"]
+    Um = U - Uh
+    Eh, Ubyp, Uins = st["hit_evictions"], st["bypasses"], st["inserts"]
+    Vo = st["evictions"] - Eh
+    A = cfg["assoc"]
+    fwd = 4 * L + 4 * (B + 1) + 4 * A * U + phi * Uh + rho * Um + 4 * d * B
+    bwd = 4 * L + 4 * (B + 1) + 4 * d * B + phi * Uh + rho * Um
+    bwd += phi * (Uh - Eh) + rho * (Eh + Ubyp) + phi * Uins + Vo * (phi + rho) + 8 * Uins
+    if cfg["policy"] == "lru":
+        bwd += 4 * Uh
+    else:
+        bwd += 8 * U
+    if cfg["optimizer"] == "adagrad":
+        bwd += 8 * U
+    return fwd, bwd
+
+
+def cpu_baseline(cfg, steps, budget_s):
+    """The CPU oracle on one table of the workload (table 0), single thread."""
+    import oracle  # test infrastructure: only this leg of the benchmark loads it
+
+    one = configs.get(cfg["name"], rows=[cfg["rows"][0]])
+    o = oracle.Oracle(one["rows"], one["dim"], one["bits"], one["sb_fp16"], one["cache_fraction"], one["assoc"],
+                      one["policy"], one.get("lfu_decay_interval", 0), one["rounding"] == "stochastic",
+                      one["optimizer"] == "adagrad", one["lr"], one["eps"], one["seed"])
+    o.init_uniform(cfg["init_lo"], cfg["init_hi"], cfg["init_seed"])
+    B = cfg["batch"]
+    lookups, elapsed, done = 0, 0.0, 0
+    for k in range(steps):
+        idx, off = workload.make_indices(cfg, k, tables=[0])
+        n0 = int(off[B])
+        g = workload._rng(cfg["grad_seed"], k, 99).standard_normal((B, 1, cfg["dim"]), dtype=np.float32)
+        g *= np.float32(cfg["grad_sigma"])
+        t0 = time.perf_counter()
+        o.forward(idx[:n0], off[:B + 1], B)
+        o.backward_update(idx[:n0], off[:B + 1], B, g)
+        elapsed += time.perf_counter() - t0
+        lookups += n0
+        done += 1
+        if elapsed > budget_s:
+            break
+    return {"value": lookups / elapsed, "unit": "lookups/s", "cores": 1, "kind": "oracle",
+            "sample": f"table 0 of {len(cfg['rows'])} ({cfg['rows'][0]} rows), {done} steps of fwd+bwd+update, "
+                      f"{lookups} lookups in {elapsed:.1f} s, single thread"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="industrial")
+    ap.add_argument("--pool", type=int, default=3, help="distinct input batches cycled through")
+    ap.add_argument("--stats-steps", type=int, default=3)
+    ap.add_argument("--cpu-steps", type=int, default=20)
+    ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the multi-GPU path is not built.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2010_11305_amd.emb_cache import EmbCache
+
+    cfg = configs.get(args.config)
+    T, B, d = len(cfg["rows"]), cfg["batch"], cfg["dim"]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    t0 = time.time()
+    pool = []
+    for k in range(args.pool):
+        idx, off = workload.make_indices(cfg, k)
+        pool.append((torch.from_numpy(idx).to(dev), torch.from_numpy(off).to(dev), idx.size))
+        print(f"[bench] input batch {k}: {idx.size} lookups ({time.time() - t0:.1f} s)", file=sys.stderr, flush=True)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(cfg["grad_seed"])
+    grads = [torch.randn((B, T, d), generator=gen, device=dev, dtype=torch.float32) * cfg["grad_sigma"]
+             for _ in range(2)]
+    max_idx = max(p[2] for p in pool)
+    emb = EmbCache(cfg, max_indices=max_idx)
+    emb.init_uniform(cfg["init_lo"], cfg["init_hi"], cfg["init_seed"])
+    out = torch.empty((B, T, d), dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+    print(f"[bench] state {emb.sizes.state_bytes / 2**30:.2f} GiB, workspace {emb.sizes.workspace_bytes / 2**30:.2f} GiB",
+          file=sys.stderr, flush=True)
+
+    def step(k, ev=None):
+        idx, off, _ = pool[k % len(pool)]
+        if ev is not None:
+            ev[0].record()
+        emb.forward(idx, off, B, out=out)
+        if ev is not None:
+            ev[1].record()
+        emb.backward_update(idx, off, B, grads[k % 2])
+        if ev is not None:
+            ev[2].record()
+
+    for k in range(args.warmup):
+        step(k)
+    torch.cuda.synchronize()
+    print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record()
+    for k in range(args.steps):
+        step(args.warmup + k, evs[k])
+    t_end.record()
+    torch.cuda.synchronize()
+    total_ms = t_start.elapsed_time(t_end)
+    fwd_ms = [e[0].elapsed_time(e[1]) for e in evs]
+    bwd_ms = [e[1].elapsed_time(e[2]) for e in evs]
+    ms_per_step = total_ms / args.steps
+    lookups = sum(pool[(args.warmup + k) % len(pool)][2] for k in range(args.steps))
+    print(f"[bench] timed {args.steps} steps: {ms_per_step:.3f} ms/step", file=sys.stderr, flush=True)
+
+    # algorithmic bytes from the statistics of further steps of the same stream
+    fwd_b, bwd_b, n_st = 0, 0, 0
+    hit_lk, all_lk = 0, 0
+    for k in range(args.stats_steps):
+        step(args.warmup + args.steps + k)
+        for t in range(T):
+            st = emb.stats(t)
+            f, b = algorithmic_bytes(cfg, st, B)
+            fwd_b += f
+            bwd_b += b
+            hit_lk += st["hit_lookups"]
+            all_lk += st["lookups"]
+        n_st += 1
+    fwd_b /= n_st
+    bwd_b /= n_st
+    status = emb.check()
+    step_bytes = fwd_b + bwd_b
+    gbs = step_bytes / (ms_per_step * 1e-3) / 1e9
+    fwd_avg = float(np.mean(fwd_ms))
+    fwd_gbs = fwd_b / (fwd_avg * 1e-3) / 1e9
+
+    result = {
+        "metric": METRIC,
+        "value": lookups / (total_ms * 1e-3),
+        "unit": "lookups/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": describe(cfg), "global_batch": B, "tables": T, "lookups_per_step": lookups / args.steps},
+        "hbm_gbps_algorithmic": gbs,
+        "hbm_frac_of_peak": gbs / HBM_PEAK_GBS,
+        "bytes_per_step_algorithmic": step_bytes,
+        "fwd_ms": fwd_avg,
+        "bwd_ms": float(np.mean(bwd_ms)),
+        "fwd_ms_p90": float(np.percentile(fwd_ms, 90)),
+        "bwd_ms_p90": float(np.percentile(bwd_ms, 90)),
+        "hit_rate_lookups": hit_lk / max(all_lk, 1),
+        "status": status,
+        "roofline": {"bound": "hbm", "kernel": "k_forward (tag probe + gather/dequant + sum-pool)",
+                     "achieved": fwd_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": fwd_gbs / HBM_PEAK_GBS,
+                     "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] CPU oracle baseline ...", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = cpu_baseline(cfg, args.cpu_steps, args.cpu_budget)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,131 @@
+// Internal declarations shared by the runtime and the HIP kernels of libembcache.
+//
+// Data layout in HBM (one caller-owned state buffer, 256-byte aligned pieces):
+//   rec   [total_rows][row_bytes]   low-precision row records: codes, then scale, then bias
+//                                   (INT4: two codes per byte, even column in the low nibble;
+//                                   scale/bias FP32 pair, or FP16 pair packed in one dword)
+//   crow  [total_slots][dim] FP32   cache rows; slot = slot_base[t] + set*assoc + way
+//   tag   [total_slots] int32       resident row id (table-local), -1 = empty way
+//   ts    [total_slots] int32       LRU: step of last access (-1 = empty); absent under LFU
+//   cnt   [total_rows] int32        LFU: access counts; absent under LRU
+//   G     [total_rows] FP32         row-wise Adagrad accumulators; absent under SGD
+//   desc  [T] TableDesc, key_base [T+1], stats [T][kNStat] u64, err flags
+// Rows of all tables are concatenated (global row = row_base[t] + row), and so
+// are cache slots, so one base pointer serves every table.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace embc {
+
+constexpr uint32_t kKeyInvalid = 0xFFFFFFFFu;  // sort key of a skipped lookup (sorts last)
+constexpr int kSumChunk = 64;                  // occurrences per chunk of a merged-gradient sum
+constexpr int kMaxAssoc = 64;
+
+enum : int32_t { kActHitStay = 0, kActHitEvict = 1, kActInsert = 2, kActBypass = 3 };
+
+enum : int {
+  kStLookups = 0, kStHitLookups, kStBwdLookups, kStUnique, kStUniqueHits, kStInserts, kStBypasses,
+  kStEvictions, kStEmptyFills, kStHitEvictions, kStInvalidFwd, kStInvalidBwd, kNStat
+};
+
+enum : int { kErrIndex = 1, kErrOffsets = 2 };
+
+// Per-table geometry.  Sort keys are set-major: key = key_base + set*Q + row/n_sets,
+// with set = row % n_sets and Q = ceil(N/n_sets), so that one sort groups the
+// lookups by row, the rows by set, and the rows of a set in ascending order.
+struct TableDesc {
+  int64_t N;
+  int64_t row_base;
+  int64_t n_sets;     // 0: no cache
+  int64_t slot_base;
+  int64_t Q;          // key stride of a set; N when there is no cache
+  int64_t key_base;
+};
+
+// Device view of the state, passed by value to every kernel.
+struct Dev {
+  uint8_t* rec;
+  float* crow;
+  int32_t* tag;
+  int32_t* ts;
+  int32_t* cnt;
+  float* G;
+  const TableDesc* desc;
+  const int64_t* key_base;       // [T+1], key_base[T] = total key space
+  unsigned long long* stats;     // [T][kNStat]
+  int32_t* err;
+  int32_t T;
+  int32_t dim;
+  int32_t bits;
+  int32_t sb16;
+  int32_t assoc;
+  int32_t rec_bytes;
+  int32_t policy;     // 0 LRU, 1 LFU
+  int32_t rounding;   // 0 nearest, 1 stochastic
+  int32_t optimizer;  // 0 SGD, 1 row-wise Adagrad
+  float lr;
+  float eps;
+  uint64_t seed;
+  int64_t total_rows;
+  int64_t total_slots;
+};
+
+// Per-call temporaries carved from the caller's workspace buffer.
+struct Work {
+  uint32_t* keysA;
+  uint32_t* valsA;
+  uint32_t* keysB;
+  uint32_t* valsB;
+  uint32_t* hist;        // radix histograms [256][nblocks]
+  unsigned long long* part;  // scan partials
+  unsigned long long* flag;  // packed (set-start << 32 | row-start) flags
+  unsigned long long* pre;   // their exclusive prefix sums
+  uint32_t* uniq_key;    // [L]
+  uint32_t* seg;         // [L+1] start of each unique row's occurrences in the sorted stream
+  uint32_t* set_first;   // [L+1] first unique row of each touched set
+  int32_t* urow;         // [L] global row id
+  int32_t* utab;         // [L] table
+  int32_t* uslot;        // [L] global slot before the step, -1 = miss
+  int32_t* uact;         // [L] action
+  int32_t* udest;        // [L] destination slot of an insert
+  uint32_t* nch;         // [L] chunk count (rows with > kSumChunk occurrences), then its prefix
+  uint32_t* chunk_base;  // [L+1]
+  int32_t* vic_slot;     // [L] displaced residents not updated this step
+  int32_t* vic_row;      // [L] their global row
+  int32_t* vic_tab;      // [L]
+  int32_t* ins_list;     // [L] unique rows inserted this step
+  float* partial;        // [L/32 + 2][dim] chunk sums
+  unsigned long long* ctr;  // counters, see kC*
+  int64_t max_indices;
+  int64_t max_partials;
+};
+
+enum : int {
+  kCValid = 0,      // valid (sorted) lookups
+  kCUnique = 1,     // unique rows
+  kCSets = 2,       // touched sets (of cached tables)
+  kCChunks = 3,     // chunk partials
+  kCVictims = 4,
+  kCInserts = 5,
+  kCScanTotal = 6,  // scratch total of the last scan
+  kCBadOffsets = 7, // offsets of this step failed validation
+  kNCounters = 16
+};
+
+// ---- launchers (defined in the .hip sources) -------------------------------------------
+hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int64_t n, hipStream_t s);
+hipError_t launch_reset_state(const Dev& d, hipStream_t s);
+hipError_t launch_init_uniform(const Dev& d, float lo, float hi, uint64_t init_seed, hipStream_t s);
+hipError_t launch_forward(const Dev& d, const int32_t* idx, int64_t L, const int32_t* off, int32_t B,
+                          float* out, hipStream_t s);
+hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int64_t L, const int32_t* off,
+                           int32_t B, const float* grad, uint64_t step, int key_bits, bool decay,
+                           hipStream_t s);
+
+size_t radix_hist_words(int64_t n);
+size_t scan_partial_words(int64_t n);
+
+}  // namespace embc

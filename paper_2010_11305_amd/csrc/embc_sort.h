@@ -1,0 +1,24 @@
+// Sort / scan / de-duplication launchers (k_sort.hip).
+#pragma once
+
+#include "embc_internal.h"
+
+namespace embc {
+
+template <typename T>
+hipError_t scan_exclusive(const T* in, T* out, int64_t n, const unsigned long long* dev_n, T* part, T* total,
+                          hipStream_t s);
+
+// Stable LSD radix sort of n (key, value) pairs over `passes` 8-bit digits,
+// ping-ponging between (kA, vA) and (kB, vB); *in_B tells where the result is.
+hipError_t sort_pairs(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32_t* vB, int64_t n, int passes, uint32_t* hist,
+                      uint32_t* part, int* in_B, hipStream_t s);
+
+hipError_t launch_expand(const Dev& dv, const int32_t* idx, int64_t L, const int32_t* off, int32_t B, uint32_t* keys,
+                         uint32_t* vals, unsigned long long* ctr, hipStream_t s);
+
+hipError_t launch_unique(const Dev& dv, const uint32_t* sk, int64_t n, unsigned long long* flag,
+                         unsigned long long* pre, unsigned long long* part, uint32_t* uk, uint32_t* seg,
+                         uint32_t* set_first, unsigned long long* ctr, hipStream_t s);
+
+}  // namespace embc

@@ -1,0 +1,421 @@
+// Sort and de-duplication of one step's lookups (the paper's Sec. 5.1: sort the
+// row indices of the mini-batch, merge the gradients of each row).
+//
+//   k_expand       lookups -> (set-major row key, gradient-row index), position order
+//   radix passes   stable LSD radix sort, 8-bit digits, wave-ballot ranking
+//   k_row_flags    first occurrence of each row / of each cache set in the sorted stream
+//   scans          3-phase exclusive prefix sums (u32 / u64)
+//   k_compact      unique-row and touched-set lists
+#include "embc_device.h"
+#include "embc_dispatch.h"
+#include "embc_sort.h"
+
+namespace embc {
+
+constexpr int kScanThreads = 256;
+constexpr int kScanItems = 8;
+constexpr int kScanTile = kScanThreads * kScanItems;
+constexpr int kRadixThreads = 256;
+constexpr int kRadixItems = 16;
+constexpr int kRadixTile = kRadixThreads * kRadixItems;
+constexpr int kRadixWaves = kRadixThreads / 64;
+
+size_t radix_hist_words(int64_t n) { return 256 * (size_t)((n + kRadixTile - 1) / kRadixTile + 1); }
+size_t scan_partial_words(int64_t n) { return (size_t)((n + kScanTile - 1) / kScanTile + 64); }
+
+// ---- block-wide exclusive scan of one value per thread (256 threads) -------------------
+template <typename T>
+__device__ __forceinline__ T block_exclusive_scan(T v, T* lds4, T& total) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  T x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const T y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) lds4[wv] = x;
+  __syncthreads();
+  T pre = 0;
+  total = 0;
+#pragma unroll
+  for (int w = 0; w < kScanThreads / 64; ++w) {
+    const T s = lds4[w];
+    if (w < wv) pre += s;
+    total += s;
+  }
+  __syncthreads();
+  return pre + x - v;
+}
+
+// ---- 3-phase exclusive scan ---------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(kScanThreads) void k_scan_reduce(const T* __restrict__ in, int64_t n,
+                                                              const unsigned long long* dev_n, T* part) {
+  __shared__ T lds4[4];
+  if (dev_n) n = min(n, (int64_t)*dev_n);
+  const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
+  T s = 0;
+#pragma unroll
+  for (int i = 0; i < kScanItems; ++i)
+    if (base + i < n) s += in[base + i];
+  T tot;
+  block_exclusive_scan<T>(s, lds4, tot);
+  if (threadIdx.x == 0) part[blockIdx.x] = tot;
+}
+
+template <typename T>
+__global__ __launch_bounds__(kScanThreads) void k_scan_top(T* part, int64_t nb, T* total_out) {
+  __shared__ T lds4[4];
+  T carry = 0;
+  for (int64_t b0 = 0; b0 < nb; b0 += kScanThreads) {
+    const int64_t i = b0 + threadIdx.x;
+    const T v = i < nb ? part[i] : (T)0;
+    T tot;
+    const T ex = block_exclusive_scan<T>(v, lds4, tot);
+    if (i < nb) part[i] = carry + ex;
+    carry += tot;
+  }
+  if (threadIdx.x == 0 && total_out) *total_out = carry;
+}
+
+template <typename T>
+__global__ __launch_bounds__(kScanThreads) void k_scan_down(const T* __restrict__ in, T* __restrict__ out, int64_t n,
+                                                            const unsigned long long* dev_n, const T* part) {
+  __shared__ T lds4[4];
+  if (dev_n) n = min(n, (int64_t)*dev_n);
+  const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
+  T v[kScanItems];
+  T s = 0;
+#pragma unroll
+  for (int i = 0; i < kScanItems; ++i) {
+    v[i] = base + i < n ? in[base + i] : (T)0;
+    s += v[i];
+  }
+  T tot;
+  T run = block_exclusive_scan<T>(s, lds4, tot) + part[blockIdx.x];
+#pragma unroll
+  for (int i = 0; i < kScanItems; ++i) {
+    if (base + i < n) out[base + i] = run;
+    run += v[i];
+  }
+}
+
+template <typename T>
+hipError_t scan_exclusive(const T* in, T* out, int64_t n, const unsigned long long* dev_n, T* part, T* total,
+                          hipStream_t s) {
+  if (n <= 0) {
+    if (total) k_scan_top<T><<<1, kScanThreads, 0, s>>>(part, 0, total);
+    return hipGetLastError();
+  }
+  const int64_t nb = (n + kScanTile - 1) / kScanTile;
+  k_scan_reduce<T><<<(unsigned)nb, kScanThreads, 0, s>>>(in, n, dev_n, part);
+  k_scan_top<T><<<1, kScanThreads, 0, s>>>(part, nb, total);
+  k_scan_down<T><<<(unsigned)nb, kScanThreads, 0, s>>>(in, out, n, dev_n, part);
+  return hipGetLastError();
+}
+
+template hipError_t scan_exclusive<uint32_t>(const uint32_t*, uint32_t*, int64_t, const unsigned long long*,
+                                             uint32_t*, uint32_t*, hipStream_t);
+template hipError_t scan_exclusive<unsigned long long>(const unsigned long long*, unsigned long long*, int64_t,
+                                                       const unsigned long long*, unsigned long long*,
+                                                       unsigned long long*, hipStream_t);
+
+// ---- LSD radix sort of (key, value) pairs -----------------------------------------------
+// Lanes whose 8-bit digits are equal, among the `valid` lanes of the wave.
+__device__ __forceinline__ uint64_t match_digit(uint32_t d, bool valid) {
+  uint64_t m = __ballot(valid);
+#pragma unroll
+  for (int b = 0; b < 8; ++b) {
+    const bool bit = (d >> b) & 1u;
+    const uint64_t bb = __ballot(bit);
+    m &= bit ? bb : ~bb;
+  }
+  return m;
+}
+
+// Per-tile digit histogram, written digit-major: hist[digit * nblocks + block].
+__global__ __launch_bounds__(kRadixThreads) void k_radix_hist(const uint32_t* __restrict__ keys, int64_t n, int shift,
+                                                              uint32_t* __restrict__ hist, int64_t nblocks) {
+  __shared__ uint32_t h[256];
+  h[threadIdx.x] = 0;
+  __syncthreads();
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int64_t base = (int64_t)blockIdx.x * kRadixTile + (int64_t)wv * 64 * kRadixItems;
+  for (int i = 0; i < kRadixItems; ++i) {
+    const int64_t p = base + i * 64 + lane;
+    const bool valid = p < n;
+    const uint32_t d = valid ? (keys[p] >> shift) & 255u : 0u;
+    const uint64_t peers = match_digit(d, valid);
+    if (valid && (peers & lanemask_lt()) == 0) atomicAdd(&h[d], (uint32_t)__popcll(peers));
+  }
+  __syncthreads();
+  hist[(int64_t)threadIdx.x * nblocks + blockIdx.x] = h[threadIdx.x];
+}
+
+// Stable scatter: rank inside the tile by (digit, position), stage in LDS in
+// digit order, then write runs to the digit's global offset.
+__global__ __launch_bounds__(kRadixThreads) void k_radix_scatter(const uint32_t* __restrict__ kin,
+                                                                 const uint32_t* __restrict__ vin,
+                                                                 uint32_t* __restrict__ kout,
+                                                                 uint32_t* __restrict__ vout, int64_t n, int shift,
+                                                                 const uint32_t* __restrict__ hist_scanned,
+                                                                 int64_t nblocks) {
+  __shared__ uint32_t wcnt[kRadixWaves][256];
+  __shared__ uint32_t dpre[256];
+  __shared__ uint32_t goff[256];
+  __shared__ uint32_t skey[kRadixTile];
+  __shared__ uint32_t sval[kRadixTile];
+  __shared__ uint32_t lds4[4];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  for (int i = threadIdx.x; i < kRadixWaves * 256; i += kRadixThreads) (&wcnt[0][0])[i] = 0;
+  __syncthreads();
+  const int64_t tile0 = (int64_t)blockIdx.x * kRadixTile;
+  const int64_t base = tile0 + (int64_t)wv * 64 * kRadixItems;
+  uint32_t k[kRadixItems], v[kRadixItems], rank[kRadixItems];
+#pragma unroll
+  for (int i = 0; i < kRadixItems; ++i) {
+    const int64_t p = base + i * 64 + lane;
+    const bool valid = p < n;
+    k[i] = valid ? kin[p] : 0xFFFFFFFFu;
+    v[i] = valid ? vin[p] : 0u;
+    const uint32_t d = (k[i] >> shift) & 255u;
+    const uint64_t peers = match_digit(d, valid);
+    const uint32_t before = (uint32_t)__popcll(peers & lanemask_lt());
+    uint32_t old = 0;
+    if (valid) old = wcnt[wv][d];
+    __builtin_amdgcn_wave_barrier();
+    if (valid && before == 0) wcnt[wv][d] = old + (uint32_t)__popcll(peers);
+    __builtin_amdgcn_wave_barrier();
+    rank[i] = old + before;
+  }
+  __syncthreads();
+  {
+    const int d = threadIdx.x;
+    uint32_t run = 0;
+#pragma unroll
+    for (int w = 0; w < kRadixWaves; ++w) {
+      const uint32_t c = wcnt[w][d];
+      wcnt[w][d] = run;
+      run += c;
+    }
+    uint32_t tot;
+    dpre[d] = block_exclusive_scan<uint32_t>(run, lds4, tot);
+    goff[d] = hist_scanned[(int64_t)d * nblocks + blockIdx.x];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < kRadixItems; ++i) {
+    const int64_t p = base + i * 64 + lane;
+    if (p < n) {
+      const uint32_t d = (k[i] >> shift) & 255u;
+      const uint32_t pos = dpre[d] + wcnt[wv][d] + rank[i];
+      skey[pos] = k[i];
+      sval[pos] = v[i];
+    }
+  }
+  __syncthreads();
+  const int cnt = (int)min((int64_t)kRadixTile, n - tile0);
+  for (int j = threadIdx.x; j < cnt; j += kRadixThreads) {
+    const uint32_t key = skey[j];
+    const uint32_t d = (key >> shift) & 255u;
+    const uint32_t g = goff[d] + (uint32_t)j - dpre[d];
+    kout[g] = key;
+    vout[g] = sval[j];
+  }
+}
+
+hipError_t sort_pairs(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32_t* vB, int64_t n, int passes, uint32_t* hist,
+                      uint32_t* part, int* in_B, hipStream_t s) {
+  *in_B = 0;
+  if (n <= 0) return hipSuccess;
+  const int64_t nb = (n + kRadixTile - 1) / kRadixTile;
+  for (int pass = 0; pass < passes; ++pass) {
+    const int shift = 8 * pass;
+    const uint32_t* ki = *in_B ? kB : kA;
+    const uint32_t* vi = *in_B ? vB : vA;
+    uint32_t* ko = *in_B ? kA : kB;
+    uint32_t* vo = *in_B ? vA : vB;
+    k_radix_hist<<<(unsigned)nb, kRadixThreads, 0, s>>>(ki, n, shift, hist, nb);
+    hipError_t e = scan_exclusive<uint32_t>(hist, hist, 256 * nb, nullptr, part, nullptr, s);
+    if (e != hipSuccess) return e;
+    k_radix_scatter<<<(unsigned)nb, kRadixThreads, 0, s>>>(ki, vi, ko, vo, n, shift, hist, nb);
+    *in_B = !*in_B;
+  }
+  return hipGetLastError();
+}
+
+// ---- lookups -> sort pairs ----------------------------------------------------------------
+// One wave per 64 consecutive bags (global bag = t*B + b); each position of those
+// bags finds its bag by a binary search over the 64 lane-held bag starts.
+// key: set-major row key (kKeyInvalid for an out-of-range row); value: index of
+// the bag's gradient row in grad_out [B][T][d], i.e. b*T + t.
+__global__ __launch_bounds__(256) void k_expand(Dev dv, const int32_t* __restrict__ idx, int64_t L,
+                                                const int32_t* __restrict__ off, int32_t B,
+                                                uint32_t* __restrict__ keys, uint32_t* __restrict__ vals,
+                                                int64_t nbag_waves, const unsigned long long* __restrict__ ctr) {
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int64_t nbags = (int64_t)dv.T * B;
+  if (ctr[kCBadOffsets]) {
+    // offsets failed validation: every lookup of the step is skipped
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < L; p += stride)
+      keys[p] = kKeyInvalid, vals[p] = 0;
+    return;
+  }
+  if (wave >= nbag_waves) {
+    // positions outside every bag: [0, off[0]) and [off[nbags], L)
+    const int64_t head = min<int64_t>(max<int64_t>(off[0], 0), L);
+    const int64_t tail = min<int64_t>(max<int64_t>(off[nbags], head), L);
+    const int64_t tid = ((wave - nbag_waves) << 6) + lane;
+    const int64_t stride = 64 * (int64_t)(gridDim.x * (blockDim.x >> 6) - nbag_waves);
+    for (int64_t p = tid; p < head; p += stride) keys[p] = kKeyInvalid, vals[p] = 0;
+    for (int64_t p = tail + tid; p < L; p += stride) keys[p] = kKeyInvalid, vals[p] = 0;
+    return;
+  }
+  const int64_t bag0 = wave * 64;
+  const int64_t mybag = bag0 + lane;
+  const int64_t lastbag = min<int64_t>(bag0 + 64, nbags);
+  int64_t st = L;
+  if (mybag < nbags) st = min<int64_t>(max<int64_t>(off[mybag], 0), L);
+  const int64_t P0 = min<int64_t>(max<int64_t>(off[bag0], 0), L);
+  const int64_t P1 = min<int64_t>(max<int64_t>(off[lastbag], P0), L);
+  uint32_t n_ok = 0, n_bad = 0;
+  int t_run = (int)(bag0 / B);
+  for (int64_t pc = P0; pc < P1; pc += 64) {
+    const int64_t p = pc + lane;
+    const bool in = p < P1;
+    // largest lane j with start_j <= p
+    int j = 0;
+#pragma unroll
+    for (int step = 32; step >= 1; step >>= 1) {
+      const int64_t s2 = __shfl(st, j + step);
+      if (j + step < 64 && s2 <= p) j += step;
+    }
+    if (in) {
+      const int64_t bag = bag0 + j;
+      const int t = (int)(bag / B);
+      const int b = (int)(bag - (int64_t)t * B);
+      const TableDesc td = dv.desc[t];
+      const int32_t r = idx[p];
+      uint32_t key = kKeyInvalid;
+      if (r >= 0 && (int64_t)r < td.N) {
+        if (td.n_sets > 0) {
+          const uint32_t set = (uint32_t)r % (uint32_t)td.n_sets;
+          const uint32_t q = (uint32_t)r / (uint32_t)td.n_sets;
+          key = (uint32_t)(td.key_base + (int64_t)set * td.Q + q);
+        } else {
+          key = (uint32_t)(td.key_base + r);
+        }
+        if (t == t_run) ++n_ok; else atomicAdd(&dv.stats[(int64_t)t * kNStat + kStBwdLookups], 1ull);
+      } else {
+        if (t == t_run) ++n_bad; else atomicAdd(&dv.stats[(int64_t)t * kNStat + kStInvalidBwd], 1ull);
+        atomicOr(dv.err, kErrIndex);
+      }
+      keys[p] = key;
+      vals[p] = (uint32_t)((int64_t)b * dv.T + t);
+    }
+  }
+  // lookups of the wave's first table: one atomic per wave
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    n_ok += __shfl_xor(n_ok, o);
+    n_bad += __shfl_xor(n_bad, o);
+  }
+  if (lane == 0 && n_ok) atomicAdd(&dv.stats[(int64_t)t_run * kNStat + kStBwdLookups], (unsigned long long)n_ok);
+  if (lane == 0 && n_bad) atomicAdd(&dv.stats[(int64_t)t_run * kNStat + kStInvalidBwd], (unsigned long long)n_bad);
+}
+
+// Offsets must be non-decreasing and inside [0, L]; otherwise flag the step.
+__global__ __launch_bounds__(256) void k_check_offsets(Dev dv, const int32_t* __restrict__ off, int64_t nbags,
+                                                       int64_t L, unsigned long long* __restrict__ ctr) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nbags; i += stride) {
+    const int64_t a = off[i], b = off[i + 1];
+    if (a < 0 || b < a || b > L) {
+      ctr[kCBadOffsets] = 1;
+      atomicOr(dv.err, kErrOffsets);
+    }
+  }
+}
+
+hipError_t launch_expand(const Dev& dv, const int32_t* idx, int64_t L, const int32_t* off, int32_t B, uint32_t* keys,
+                         uint32_t* vals, unsigned long long* ctr, hipStream_t s) {
+  const int64_t nbags = (int64_t)dv.T * B;
+  const unsigned cgrid = grid_for(nbags, 2048);
+  k_check_offsets<<<cgrid, 256, 0, s>>>(dv, off, nbags, L, ctr);
+  const int64_t nbag_waves = (nbags + 63) / 64;
+  const int64_t tail_waves = 64;
+  const int64_t waves = nbag_waves + tail_waves;
+  k_expand<<<(unsigned)((waves + 3) / 4), 256, 0, s>>>(dv, idx, L, off, B, keys, vals, nbag_waves, ctr);
+  return hipGetLastError();
+}
+
+// ---- unique rows and touched sets ---------------------------------------------------------
+// flag[i] = (first of its cache set) << 32 | (first of its row); invalid keys get 0.
+__global__ __launch_bounds__(256) void k_row_flags(Dev dv, const uint32_t* __restrict__ sk, int64_t n,
+                                                   unsigned long long* __restrict__ flag,
+                                                   unsigned long long* __restrict__ ctr) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+    const uint32_t k = sk[i];
+    const uint32_t prev = i ? sk[i - 1] : kKeyInvalid;
+    unsigned long long f = 0;
+    if (k == kKeyInvalid) {
+      if (i == 0 || prev != kKeyInvalid) ctr[kCValid] = (unsigned long long)i;
+    } else if (i == 0 || prev != k) {
+      f = 1;
+      const int t = table_of_key(dv.key_base, dv.T, k);
+      const TableDesc td = dv.desc[t];
+      if (td.n_sets > 0) {
+        bool new_set = (i == 0);
+        if (!new_set) {
+          const int tp = table_of_key(dv.key_base, dv.T, prev);
+          new_set = tp != t || ((int64_t)prev - td.key_base) / td.Q != ((int64_t)k - td.key_base) / td.Q;
+        }
+        if (new_set) f |= 1ull << 32;
+      }
+    }
+    flag[i] = f;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_compact(const uint32_t* __restrict__ sk, int64_t n,
+                                                 const unsigned long long* __restrict__ flag,
+                                                 const unsigned long long* __restrict__ pre, uint32_t* __restrict__ uk,
+                                                 uint32_t* __restrict__ seg, uint32_t* __restrict__ set_first,
+                                                 unsigned long long* __restrict__ ctr) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (tid == 0) {
+    const unsigned long long tot = ctr[kCScanTotal];
+    const uint32_t nu = (uint32_t)(tot & 0xFFFFFFFFull), ns = (uint32_t)(tot >> 32);
+    ctr[kCUnique] = nu;
+    ctr[kCSets] = ns;
+    seg[nu] = (uint32_t)ctr[kCValid];
+    set_first[ns] = nu;
+  }
+  for (int64_t i = tid; i < n; i += stride) {
+    const unsigned long long f = flag[i];
+    if (f & 1ull) {
+      const unsigned long long p = pre[i];
+      const uint32_t u = (uint32_t)(p & 0xFFFFFFFFull);
+      uk[u] = sk[i];
+      seg[u] = (uint32_t)i;
+      if (f >> 32) set_first[(uint32_t)(p >> 32)] = u;
+    }
+  }
+}
+
+hipError_t launch_unique(const Dev& dv, const uint32_t* sk, int64_t n, unsigned long long* flag,
+                         unsigned long long* pre, unsigned long long* part, uint32_t* uk, uint32_t* seg,
+                         uint32_t* set_first, unsigned long long* ctr, hipStream_t s) {
+  const unsigned grid = grid_for(n, 4096);
+  k_row_flags<<<grid, 256, 0, s>>>(dv, sk, n, flag, ctr);
+  hipError_t e = scan_exclusive<unsigned long long>(flag, pre, n, nullptr, part, ctr + kCScanTotal, s);
+  if (e != hipSuccess) return e;
+  k_compact<<<grid, 256, 0, s>>>(sk, n, flag, pre, uk, seg, set_first, ctr);
+  return hipGetLastError();
+}
+
+}  // namespace embc

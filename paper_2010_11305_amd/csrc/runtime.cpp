@@ -1,0 +1,526 @@
+// Host side of libembcache: the C ABI of include/emb_cache.h.
+//
+// Validates configurations, plans the layout of the caller's state and
+// workspace buffers, keeps the step counter and launches the kernels.  The
+// library never allocates device memory.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "emb_cache.h"
+#include "embc_internal.h"
+
+using embc::TableDesc;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+int bit_length(uint64_t v) {
+  int b = 0;
+  while (v) {
+    ++b;
+    v >>= 1;
+  }
+  return b;
+}
+
+struct Plan {
+  int64_t total_rows = 0, total_slots = 0, total_keys = 0;
+  int rec_bytes = 0;
+  std::vector<TableDesc> desc;
+  std::vector<int64_t> key_base;
+  // state offsets
+  size_t o_rec, o_crow, o_tag, o_ts, o_cnt, o_G, o_desc, o_keyb, o_stats, o_err, state_bytes;
+  // workspace offsets
+  size_t o_kA, o_vA, o_kB, o_vB, o_hist, o_part, o_flag, o_pre, o_uk, o_seg, o_setf, o_urow, o_utab, o_uslot,
+      o_uact, o_udest, o_nch, o_cbase, o_vslot, o_vrow, o_vtab, o_ins, o_partial, o_ctr, ws_bytes;
+  int64_t max_partials = 0;
+};
+
+bool is_pow2(int64_t v) { return v > 0 && (v & (v - 1)) == 0; }
+
+int plan_config(const emb_cache_config* c, Plan* p) {
+  if (!c || !p) return EMB_EINVAL;
+  if (c->num_tables < 1 || c->num_tables > 65535 || !c->rows) return EMB_EINVAL;
+  if (c->dim != 16 && c->dim != 32 && c->dim != 64 && c->dim != 128 && c->dim != 256) return EMB_EINVAL;
+  if (c->precision != EMB_INT8 && c->precision != EMB_INT4) return EMB_EINVAL;
+  if (c->sb_dtype != EMB_SB_FP32 && c->sb_dtype != EMB_SB_FP16) return EMB_EINVAL;
+  if (!(c->cache_fraction >= 0.0) || !std::isfinite(c->cache_fraction)) return EMB_EINVAL;
+  if (!is_pow2(c->assoc) || c->assoc > embc::kMaxAssoc) return EMB_EINVAL;
+  if (c->policy != EMB_LRU && c->policy != EMB_LFU) return EMB_EINVAL;
+  if (c->lfu_decay_interval < 0) return EMB_EINVAL;
+  if (c->rounding != EMB_ROUND_NEAREST && c->rounding != EMB_ROUND_STOCHASTIC) return EMB_EINVAL;
+  if (c->optimizer != EMB_OPT_SGD && c->optimizer != EMB_OPT_ROWWISE_ADAGRAD) return EMB_EINVAL;
+  if (!std::isfinite(c->lr) || !std::isfinite(c->eps) || c->eps < 0.0f) return EMB_EINVAL;
+  if (c->max_batch < 1 || c->max_indices < 1 || c->max_indices >= (int64_t)INT32_MAX) return EMB_EINVAL;
+  if ((int64_t)c->max_batch * c->num_tables >= (int64_t)UINT32_MAX) return EMB_EINVAL;
+
+  const int T = c->num_tables;
+  p->desc.assign(T, TableDesc{});
+  p->key_base.assign(T + 1, 0);
+  int64_t rows = 0, slots = 0, keys = 0;
+  for (int t = 0; t < T; ++t) {
+    const int64_t N = c->rows[t];
+    if (N < 1 || N >= (int64_t)INT32_MAX) return EMB_EINVAL;
+    int64_t n_sets = 0;
+    if (c->cache_fraction > 0.0) {
+      const double cr = std::floor(c->cache_fraction * (double)N);
+      if (!(cr < 4.0e18)) return EMB_EINVAL;
+      n_sets = (int64_t)cr / c->assoc;
+      if (n_sets < 1) n_sets = 1;
+    }
+    TableDesc& d = p->desc[t];
+    d.N = N;
+    d.row_base = rows;
+    d.n_sets = n_sets;
+    d.slot_base = slots;
+    d.Q = n_sets ? (N + n_sets - 1) / n_sets : N;
+    d.key_base = keys;
+    p->key_base[t] = keys;
+    rows += N;
+    slots += n_sets * c->assoc;
+    keys += n_sets ? n_sets * d.Q : N;
+    if (rows >= (int64_t)INT32_MAX || slots >= (int64_t)INT32_MAX || keys >= (int64_t)UINT32_MAX - 1)
+      return EMB_EINVAL;
+  }
+  p->key_base[T] = keys;
+  p->total_rows = rows;
+  p->total_slots = slots;
+  p->total_keys = keys;
+  p->rec_bytes = c->dim * c->precision / 8 + (c->sb_dtype == EMB_SB_FP16 ? 4 : 8);
+
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = o;
+    o = align_up(o + bytes);
+    return at;
+  };
+  const bool lru = c->policy == EMB_LRU, lfu = c->policy == EMB_LFU;
+  p->o_rec = take((size_t)rows * p->rec_bytes);
+  p->o_crow = take((size_t)slots * c->dim * 4);
+  p->o_tag = take((size_t)slots * 4);
+  p->o_ts = take(lru ? (size_t)slots * 4 : 0);
+  p->o_cnt = take(lfu ? (size_t)rows * 4 : 0);
+  p->o_G = take(c->optimizer == EMB_OPT_ROWWISE_ADAGRAD ? (size_t)rows * 4 : 0);
+  p->o_desc = take(sizeof(TableDesc) * T);
+  p->o_keyb = take(sizeof(int64_t) * (T + 1));
+  p->o_stats = take(sizeof(unsigned long long) * T * embc::kNStat);
+  p->o_err = take(kAlign);
+  p->state_bytes = o;
+
+  const size_t L = (size_t)c->max_indices;
+  o = 0;
+  p->o_kA = take(4 * L);
+  p->o_vA = take(4 * L);
+  p->o_kB = take(4 * L);
+  p->o_vB = take(4 * L);
+  p->o_hist = take(4 * embc::radix_hist_words((int64_t)L));
+  p->o_part = take(8 * embc::scan_partial_words((int64_t)L + 256 * 64));
+  p->o_flag = take(8 * L);
+  p->o_pre = take(8 * L);
+  p->o_uk = take(4 * L);
+  p->o_seg = take(4 * (L + 1));
+  p->o_setf = take(4 * (L + 1));
+  p->o_urow = take(4 * L);
+  p->o_utab = take(4 * L);
+  p->o_uslot = take(4 * L);
+  p->o_uact = take(4 * L);
+  p->o_udest = take(4 * L);
+  p->o_nch = take(4 * L);
+  p->o_cbase = take(4 * (L + 1));
+  p->o_vslot = take(4 * L);
+  p->o_vrow = take(4 * L);
+  p->o_vtab = take(4 * L);
+  p->o_ins = take(4 * L);
+  p->max_partials = (int64_t)(L / (embc::kSumChunk / 2) + 2);
+  p->o_partial = take((size_t)p->max_partials * c->dim * 4);
+  p->o_ctr = take(8 * embc::kNCounters);
+  p->ws_bytes = o;
+  return EMB_OK;
+}
+
+}  // namespace
+
+struct emb_cache {
+  emb_cache_config cfg;
+  std::vector<int64_t> rows;
+  Plan plan;
+  embc::Dev dev;
+  embc::Work work;
+  uint64_t step = 0;
+  int key_bits = 1;
+};
+
+namespace {
+
+hipStream_t S(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+int hip_status(hipError_t e) { return e == hipSuccess ? EMB_OK : EMB_EHIP; }
+
+// IEEE binary16 <-> binary32 on the host (exact widening; RNE narrowing).
+float half_bits_to_float(uint16_t h) { return (float)*reinterpret_cast<const _Float16*>(&h); }
+uint16_t float_to_half_bits(float f) {
+  const _Float16 h = (_Float16)f;
+  uint16_t b;
+  std::memcpy(&b, &h, 2);
+  return b;
+}
+
+}  // namespace
+
+extern "C" {
+
+int emb_cache_query_sizes(const emb_cache_config* cfg, emb_cache_sizes* out) {
+  if (!out) return EMB_EINVAL;
+  Plan p;
+  const int st = plan_config(cfg, &p);
+  if (st != EMB_OK) return st;
+  out->state_bytes = p.state_bytes;
+  out->workspace_bytes = p.ws_bytes;
+  out->total_rows = p.total_rows;
+  out->total_slots = p.total_slots;
+  out->row_bytes = p.rec_bytes;
+  out->pad = 0;
+  return EMB_OK;
+}
+
+int emb_cache_table_geometry(const emb_cache_config* cfg, int32_t table, int64_t* n_sets, int64_t* slots) {
+  Plan p;
+  const int st = plan_config(cfg, &p);
+  if (st != EMB_OK) return st;
+  if (table < 0 || table >= cfg->num_tables || !n_sets || !slots) return EMB_EINVAL;
+  *n_sets = p.desc[table].n_sets;
+  *slots = p.desc[table].n_sets * cfg->assoc;
+  return EMB_OK;
+}
+
+int emb_cache_create(const emb_cache_config* cfg, void* state, size_t state_bytes, void* workspace,
+                     size_t workspace_bytes, void* stream, emb_cache_t* out) {
+  if (!out) return EMB_EINVAL;
+  *out = nullptr;
+  emb_cache* h = new (std::nothrow) emb_cache();
+  if (!h) return EMB_EINVAL;
+  int st = plan_config(cfg, &h->plan);
+  if (st != EMB_OK) {
+    delete h;
+    return st;
+  }
+  const Plan& p = h->plan;
+  if (!state || !workspace || (reinterpret_cast<uintptr_t>(state) % kAlign) ||
+      (reinterpret_cast<uintptr_t>(workspace) % kAlign)) {
+    delete h;
+    return EMB_EINVAL;
+  }
+  if (state_bytes < p.state_bytes || workspace_bytes < p.ws_bytes) {
+    delete h;
+    return EMB_ENOMEM;
+  }
+  h->cfg = *cfg;
+  h->rows.assign(cfg->rows, cfg->rows + cfg->num_tables);
+  h->cfg.rows = h->rows.data();
+  h->key_bits = bit_length((uint64_t)(p.total_keys > 0 ? p.total_keys - 1 : 0));
+  if (h->key_bits < 1) h->key_bits = 1;
+
+  uint8_t* sb = static_cast<uint8_t*>(state);
+  embc::Dev& d = h->dev;
+  d.rec = sb + p.o_rec;
+  d.crow = reinterpret_cast<float*>(sb + p.o_crow);
+  d.tag = reinterpret_cast<int32_t*>(sb + p.o_tag);
+  d.ts = cfg->policy == EMB_LRU ? reinterpret_cast<int32_t*>(sb + p.o_ts) : nullptr;
+  d.cnt = cfg->policy == EMB_LFU ? reinterpret_cast<int32_t*>(sb + p.o_cnt) : nullptr;
+  d.G = cfg->optimizer == EMB_OPT_ROWWISE_ADAGRAD ? reinterpret_cast<float*>(sb + p.o_G) : nullptr;
+  d.desc = reinterpret_cast<const TableDesc*>(sb + p.o_desc);
+  d.key_base = reinterpret_cast<const int64_t*>(sb + p.o_keyb);
+  d.stats = reinterpret_cast<unsigned long long*>(sb + p.o_stats);
+  d.err = reinterpret_cast<int32_t*>(sb + p.o_err);
+  d.T = cfg->num_tables;
+  d.dim = cfg->dim;
+  d.bits = cfg->precision;
+  d.sb16 = cfg->sb_dtype == EMB_SB_FP16;
+  d.assoc = cfg->assoc;
+  d.rec_bytes = p.rec_bytes;
+  d.policy = cfg->policy;
+  d.rounding = cfg->rounding;
+  d.optimizer = cfg->optimizer;
+  d.lr = cfg->lr;
+  d.eps = cfg->eps;
+  d.seed = cfg->seed;
+  d.total_rows = p.total_rows;
+  d.total_slots = p.total_slots;
+
+  uint8_t* wb = static_cast<uint8_t*>(workspace);
+  embc::Work& w = h->work;
+  w.keysA = reinterpret_cast<uint32_t*>(wb + p.o_kA);
+  w.valsA = reinterpret_cast<uint32_t*>(wb + p.o_vA);
+  w.keysB = reinterpret_cast<uint32_t*>(wb + p.o_kB);
+  w.valsB = reinterpret_cast<uint32_t*>(wb + p.o_vB);
+  w.hist = reinterpret_cast<uint32_t*>(wb + p.o_hist);
+  w.part = reinterpret_cast<unsigned long long*>(wb + p.o_part);
+  w.flag = reinterpret_cast<unsigned long long*>(wb + p.o_flag);
+  w.pre = reinterpret_cast<unsigned long long*>(wb + p.o_pre);
+  w.uniq_key = reinterpret_cast<uint32_t*>(wb + p.o_uk);
+  w.seg = reinterpret_cast<uint32_t*>(wb + p.o_seg);
+  w.set_first = reinterpret_cast<uint32_t*>(wb + p.o_setf);
+  w.urow = reinterpret_cast<int32_t*>(wb + p.o_urow);
+  w.utab = reinterpret_cast<int32_t*>(wb + p.o_utab);
+  w.uslot = reinterpret_cast<int32_t*>(wb + p.o_uslot);
+  w.uact = reinterpret_cast<int32_t*>(wb + p.o_uact);
+  w.udest = reinterpret_cast<int32_t*>(wb + p.o_udest);
+  w.nch = reinterpret_cast<uint32_t*>(wb + p.o_nch);
+  w.chunk_base = reinterpret_cast<uint32_t*>(wb + p.o_cbase);
+  w.vic_slot = reinterpret_cast<int32_t*>(wb + p.o_vslot);
+  w.vic_row = reinterpret_cast<int32_t*>(wb + p.o_vrow);
+  w.vic_tab = reinterpret_cast<int32_t*>(wb + p.o_vtab);
+  w.ins_list = reinterpret_cast<int32_t*>(wb + p.o_ins);
+  w.partial = reinterpret_cast<float*>(wb + p.o_partial);
+  w.ctr = reinterpret_cast<unsigned long long*>(wb + p.o_ctr);
+  w.max_indices = cfg->max_indices;
+  w.max_partials = p.max_partials;
+
+  hipStream_t s = S(stream);
+  hipError_t e = hipMemcpyAsync(sb + p.o_desc, p.desc.data(), sizeof(TableDesc) * p.desc.size(),
+                                hipMemcpyHostToDevice, s);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(sb + p.o_keyb, p.key_base.data(), sizeof(int64_t) * p.key_base.size(), hipMemcpyHostToDevice,
+                       s);
+  if (e == hipSuccess) e = embc::launch_reset_state(d, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) {
+    delete h;
+    return EMB_EHIP;
+  }
+  h->step = 0;
+  *out = h;
+  return EMB_OK;
+}
+
+int emb_cache_destroy(emb_cache_t h) {
+  delete h;
+  return EMB_OK;
+}
+
+int emb_cache_init_uniform(emb_cache_t h, float lo, float hi, uint64_t init_seed, void* stream) {
+  if (!h || !std::isfinite(lo) || !std::isfinite(hi)) return EMB_EINVAL;
+  return hip_status(embc::launch_init_uniform(h->dev, lo, hi, init_seed, S(stream)));
+}
+
+int emb_cache_forward(emb_cache_t h, const int32_t* indices, int64_t num_indices, const int32_t* offsets,
+                      int32_t batch, float* out, void* stream) {
+  if (!h || batch < 0 || batch > h->cfg.max_batch || num_indices < 0 || num_indices > h->cfg.max_indices)
+    return EMB_EINVAL;
+  if ((num_indices > 0 && !indices) || !offsets || (batch > 0 && !out)) return EMB_EINVAL;
+  return hip_status(embc::launch_forward(h->dev, indices, num_indices, offsets, batch, out, S(stream)));
+}
+
+int emb_cache_backward_update(emb_cache_t h, const int32_t* indices, int64_t num_indices, const int32_t* offsets,
+                              int32_t batch, const float* grad_out, void* stream) {
+  if (!h || batch < 0 || batch > h->cfg.max_batch || num_indices < 0 || num_indices > h->cfg.max_indices)
+    return EMB_EINVAL;
+  if ((num_indices > 0 && !indices) || !offsets || (batch > 0 && !grad_out)) return EMB_EINVAL;
+  const int K = h->cfg.lfu_decay_interval;
+  const bool decay = h->cfg.policy == EMB_LFU && K > 0 && h->step > 0 && h->step % (uint64_t)K == 0;
+  const hipError_t e = embc::launch_backward(h->dev, h->work, indices, num_indices, offsets, batch, grad_out,
+                                             h->step, h->key_bits, decay, S(stream));
+  if (e != hipSuccess) return EMB_EHIP;
+  h->step += 1;
+  return EMB_OK;
+}
+
+int emb_cache_get_stats(emb_cache_t h, int32_t table, int64_t* out, void* stream) {
+  if (!h || !out || table < 0 || table >= h->cfg.num_tables) return EMB_EINVAL;
+  hipStream_t s = S(stream);
+  unsigned long long tmp[embc::kNStat];
+  hipError_t e = hipMemcpyAsync(tmp, h->dev.stats + (int64_t)table * embc::kNStat, sizeof(tmp), hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return EMB_EHIP;
+  for (int i = 0; i < embc::kNStat; ++i) out[i] = (int64_t)tmp[i];
+  return EMB_OK;
+}
+
+int emb_cache_check(emb_cache_t h, void* stream) {
+  if (!h) return EMB_EINVAL;
+  hipStream_t s = S(stream);
+  int32_t flag = 0;
+  hipError_t e = hipMemcpyAsync(&flag, h->dev.err, sizeof(flag), hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return EMB_EHIP;
+  if (flag) {
+    const int32_t zero = 0;
+    e = hipMemcpyAsync(h->dev.err, &zero, sizeof(zero), hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return EMB_EHIP;
+    return EMB_EINDEX;
+  }
+  return EMB_OK;
+}
+
+int emb_cache_export_rows(emb_cache_t h, int32_t table, int64_t row0, int64_t n, uint8_t* codes, float* scale,
+                          float* bias, int32_t* lfu_count, float* adagrad, void* stream) {
+  if (!h || table < 0 || table >= h->cfg.num_tables || row0 < 0 || n < 0) return EMB_EINVAL;
+  const TableDesc& td = h->plan.desc[table];
+  if (row0 + n > td.N) return EMB_EINVAL;
+  if (n == 0) return EMB_OK;
+  hipStream_t s = S(stream);
+  const int d = h->cfg.dim, RB = h->plan.rec_bytes, bits = h->cfg.precision;
+  const int64_t g0 = td.row_base + row0;
+  hipError_t e = hipSuccess;
+  if (codes || scale || bias) {
+    std::vector<uint8_t> buf((size_t)n * RB);
+    e = hipMemcpyAsync(buf.data(), h->dev.rec + g0 * RB, buf.size(), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return EMB_EHIP;
+    const int cb = d * bits / 8;
+    for (int64_t i = 0; i < n; ++i) {
+      const uint8_t* r = buf.data() + i * RB;
+      if (codes) {
+        for (int j = 0; j < d; ++j)
+          codes[i * d + j] = bits == 8 ? r[j] : (uint8_t)((r[j >> 1] >> ((j & 1) * 4)) & 15);
+      }
+      float sv, bv;
+      if (h->cfg.sb_dtype == EMB_SB_FP16) {
+        uint16_t hs, hb;
+        std::memcpy(&hs, r + cb, 2);
+        std::memcpy(&hb, r + cb + 2, 2);
+        sv = half_bits_to_float(hs);
+        bv = half_bits_to_float(hb);
+      } else {
+        std::memcpy(&sv, r + cb, 4);
+        std::memcpy(&bv, r + cb + 4, 4);
+      }
+      if (scale) scale[i] = sv;
+      if (bias) bias[i] = bv;
+    }
+  }
+  if (lfu_count) {
+    if (h->dev.cnt) e = hipMemcpyAsync(lfu_count, h->dev.cnt + g0, 4 * (size_t)n, hipMemcpyDeviceToHost, s);
+    else std::memset(lfu_count, 0, 4 * (size_t)n);
+  }
+  if (e == hipSuccess && adagrad) {
+    if (h->dev.G) e = hipMemcpyAsync(adagrad, h->dev.G + g0, 4 * (size_t)n, hipMemcpyDeviceToHost, s);
+    else std::memset(adagrad, 0, 4 * (size_t)n);
+  }
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  return hip_status(e);
+}
+
+int emb_cache_import_rows(emb_cache_t h, int32_t table, int64_t row0, int64_t n, const uint8_t* codes,
+                          const float* scale, const float* bias, const int32_t* lfu_count, const float* adagrad,
+                          void* stream) {
+  if (!h || table < 0 || table >= h->cfg.num_tables || row0 < 0 || n < 0) return EMB_EINVAL;
+  const TableDesc& td = h->plan.desc[table];
+  if (row0 + n > td.N) return EMB_EINVAL;
+  if (n == 0) return EMB_OK;
+  hipStream_t s = S(stream);
+  const int d = h->cfg.dim, RB = h->plan.rec_bytes, bits = h->cfg.precision;
+  const int64_t g0 = td.row_base + row0;
+  hipError_t e = hipSuccess;
+  std::vector<uint8_t> buf;
+  if (codes || scale || bias) {
+    if (!codes || !scale || !bias) return EMB_EINVAL;  // a record is written whole
+    const int K = (1 << bits) - 1;
+    const int cb = d * bits / 8;
+    buf.assign((size_t)n * RB, 0);
+    for (int64_t i = 0; i < n; ++i) {
+      uint8_t* r = buf.data() + i * RB;
+      for (int j = 0; j < d; ++j) {
+        const uint8_t q = codes[i * d + j];
+        if (q > K) return EMB_EINVAL;
+        if (bits == 8) r[j] = q;
+        else r[j >> 1] |= (uint8_t)(q << ((j & 1) * 4));
+      }
+      if (h->cfg.sb_dtype == EMB_SB_FP16) {
+        const uint16_t hs = float_to_half_bits(scale[i]), hb = float_to_half_bits(bias[i]);
+        if (half_bits_to_float(hs) != scale[i] || half_bits_to_float(hb) != bias[i]) return EMB_EINVAL;
+        std::memcpy(r + cb, &hs, 2);
+        std::memcpy(r + cb + 2, &hb, 2);
+      } else {
+        std::memcpy(r + cb, &scale[i], 4);
+        std::memcpy(r + cb + 4, &bias[i], 4);
+      }
+    }
+    e = hipMemcpyAsync(h->dev.rec + g0 * RB, buf.data(), buf.size(), hipMemcpyHostToDevice, s);
+  }
+  if (e == hipSuccess && lfu_count && h->dev.cnt)
+    e = hipMemcpyAsync(h->dev.cnt + g0, lfu_count, 4 * (size_t)n, hipMemcpyHostToDevice, s);
+  if (e == hipSuccess && adagrad && h->dev.G)
+    e = hipMemcpyAsync(h->dev.G + g0, adagrad, 4 * (size_t)n, hipMemcpyHostToDevice, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  return hip_status(e);
+}
+
+int emb_cache_export_cache(emb_cache_t h, int32_t table, float* rows, int32_t* tags, int32_t* lru_stamp,
+                           void* stream) {
+  if (!h || table < 0 || table >= h->cfg.num_tables) return EMB_EINVAL;
+  const TableDesc& td = h->plan.desc[table];
+  const int64_t slots = td.n_sets * h->cfg.assoc;
+  if (slots == 0) return EMB_OK;
+  hipStream_t s = S(stream);
+  const int d = h->cfg.dim;
+  hipError_t e = hipSuccess;
+  if (rows) e = hipMemcpyAsync(rows, h->dev.crow + td.slot_base * d, 4 * (size_t)(slots * d), hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess && tags)
+    e = hipMemcpyAsync(tags, h->dev.tag + td.slot_base, 4 * (size_t)slots, hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess && lru_stamp) {
+    if (h->dev.ts) e = hipMemcpyAsync(lru_stamp, h->dev.ts + td.slot_base, 4 * (size_t)slots, hipMemcpyDeviceToHost, s);
+    else
+      for (int64_t i = 0; i < slots; ++i) lru_stamp[i] = -1;
+  }
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  return hip_status(e);
+}
+
+int emb_cache_import_cache(emb_cache_t h, int32_t table, const float* rows, const int32_t* tags,
+                           const int32_t* lru_stamp, void* stream) {
+  if (!h || table < 0 || table >= h->cfg.num_tables) return EMB_EINVAL;
+  const TableDesc& td = h->plan.desc[table];
+  const int64_t slots = td.n_sets * h->cfg.assoc;
+  if (slots == 0) return EMB_OK;
+  if (tags) {
+    for (int64_t i = 0; i < slots; ++i) {
+      const int32_t tg = tags[i];
+      if (tg < -1 || tg >= td.N) return EMB_EINVAL;
+      if (tg >= 0 && (tg % td.n_sets) != (i / h->cfg.assoc)) return EMB_EINVAL;  // row must map to its set
+    }
+  }
+  hipStream_t s = S(stream);
+  const int d = h->cfg.dim;
+  hipError_t e = hipSuccess;
+  if (rows) e = hipMemcpyAsync(h->dev.crow + td.slot_base * d, rows, 4 * (size_t)(slots * d), hipMemcpyHostToDevice, s);
+  if (e == hipSuccess && tags)
+    e = hipMemcpyAsync(h->dev.tag + td.slot_base, tags, 4 * (size_t)slots, hipMemcpyHostToDevice, s);
+  if (e == hipSuccess && lru_stamp && h->dev.ts)
+    e = hipMemcpyAsync(h->dev.ts + td.slot_base, lru_stamp, 4 * (size_t)slots, hipMemcpyHostToDevice, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  return hip_status(e);
+}
+
+int emb_cache_get_step(emb_cache_t h, uint64_t* step) {
+  if (!h || !step) return EMB_EINVAL;
+  *step = h->step;
+  return EMB_OK;
+}
+
+int emb_cache_set_step(emb_cache_t h, uint64_t step) {
+  if (!h) return EMB_EINVAL;
+  h->step = step;
+  return EMB_OK;
+}
+
+const char* emb_cache_status_string(int status) {
+  switch (status) {
+    case EMB_OK: return "ok";
+    case EMB_EINVAL: return "invalid argument or configuration";
+    case EMB_ENOMEM: return "buffer smaller than required";
+    case EMB_EINDEX: return "index outside the table, or malformed offsets";
+    case EMB_EHIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+}  // extern "C"

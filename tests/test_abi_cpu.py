@@ -1,0 +1,130 @@
+"""Host-side checks of the C-ABI library (no GPU call): it loads, exports every
+function include/emb_cache.h declares, validates configurations, and plans the
+same cache geometry as the oracle (computed independently there)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import oracle
+from common import custom_cfg, oracle_from_cfg
+from paper_2010_11305_amd import configs
+from paper_2010_11305_amd import emb_cache as ec
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "emb_cache.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(ec.LIB_PATH):
+        from paper_2010_11305_amd import build
+        build.build()
+    return ec.load()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(emb_cache_\w+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_functions()
+    assert len(names) >= 16
+    for n in names:
+        assert hasattr(lib, n), n
+        assert ctypes.cast(getattr(lib, n), ctypes.c_void_p).value
+
+
+def test_status_strings(lib):
+    for st in range(5):
+        assert ec.status_string(st)
+    assert ec.status_string(99) == "unknown status"
+
+
+@pytest.mark.parametrize("name", configs.ORDER)
+def test_query_sizes_named_configs(lib, name):
+    cfg = configs.get(name)
+    L = 1 << 20
+    s = ec.query_sizes(cfg, L)
+    N = sum(cfg["rows"])
+    rec = cfg["dim"] * cfg["bits"] // 8 + (4 if cfg["sb_fp16"] else 8)
+    assert s["row_bytes"] == rec and s["total_rows"] == N
+    assert s["state_bytes"] >= N * rec + s["total_slots"] * (4 * cfg["dim"] + 4)
+    assert s["workspace_bytes"] >= 16 * L
+
+
+@pytest.mark.parametrize("name,over", [
+    ("tiny", {}), ("tiny", {"assoc": 1}), ("tiny", {"cache_fraction": 0.0}), ("tiny", {"cache_fraction": 1.024, "assoc": 32}),
+    ("kaggle_int8", {}), ("kaggle_int4", {}), ("industrial", {}), ("stress", {}),
+])
+def test_geometry_matches_oracle(lib, name, over):
+    cfg = configs.get(name, **over)
+    c, keep = ec.make_config(cfg, 1024)
+    for t in range(len(cfg["rows"])):
+        ns, sl = ctypes.c_int64(), ctypes.c_int64()
+        assert lib.emb_cache_table_geometry(ctypes.byref(c), t, ctypes.byref(ns), ctypes.byref(sl)) == 0
+        # the oracle computes its own geometry; build only tiny tables there
+        if cfg["rows"][t] <= 100_000:
+            o = oracle_from_cfg(dict(cfg, rows=[cfg["rows"][t]]))
+            assert (ns.value, sl.value) == (o.n_sets[0], o.slots[0])
+    if name == "industrial":
+        assert (ns.value, sl.value) == (3125, 50000)
+    if name == "stress":
+        assert (ns.value, sl.value) == (62500, 2_000_000)
+
+
+@pytest.mark.parametrize("bad", [
+    {"dim": 24}, {"dim": 512}, {"bits": 2}, {"assoc": 3}, {"assoc": 128}, {"assoc": 0}, {"cache_fraction": -0.1},
+    {"cache_fraction": float("nan")}, {"rows": [0]}, {"rows": [2**31]}, {"rows": []}, {"policy": "fifo"},
+    {"lfu_decay_interval": -1}, {"eps": -1.0}, {"lr": float("inf")},
+])
+def test_invalid_configs_rejected(lib, bad):
+    cfg = custom_cfg()
+    if "policy" in bad and bad["policy"] == "fifo":
+        c, keep = ec.make_config(cfg, 1024)
+        c.policy = 7
+    else:
+        cfg.update(bad)
+        if cfg["rows"] == []:
+            c, keep = ec.make_config(dict(cfg, rows=[1]), 1024)
+            c.num_tables = 0
+        else:
+            c, keep = ec.make_config(cfg, 1024)
+    s = ec.Sizes()
+    assert lib.emb_cache_query_sizes(ctypes.byref(c), ctypes.byref(s)) == ec.EMB_EINVAL
+
+
+def test_workspace_bounds_rejected(lib):
+    cfg = custom_cfg()
+    for mi, mb in [(0, 128), (1024, 0), (2**31, 128)]:
+        c, keep = ec.make_config(cfg, mi, mb)
+        s = ec.Sizes()
+        assert lib.emb_cache_query_sizes(ctypes.byref(c), ctypes.byref(s)) == ec.EMB_EINVAL
+
+
+def test_create_rejects_small_or_null_buffers(lib):
+    cfg = custom_cfg()
+    c, keep = ec.make_config(cfg, 1024)
+    s = ec.Sizes()
+    assert lib.emb_cache_query_sizes(ctypes.byref(c), ctypes.byref(s)) == 0
+    h = ctypes.c_void_p()
+    assert lib.emb_cache_create(ctypes.byref(c), None, s.state_bytes, None, s.workspace_bytes, None,
+                                ctypes.byref(h)) == ec.EMB_EINVAL
+    fake = ctypes.c_void_p(1 << 20)  # never dereferenced: sizes are checked first
+    assert lib.emb_cache_create(ctypes.byref(c), fake, s.state_bytes - 1, fake, s.workspace_bytes, None,
+                                ctypes.byref(h)) == ec.EMB_ENOMEM
+    assert lib.emb_cache_create(ctypes.byref(c), fake, s.state_bytes, fake, s.workspace_bytes - 1, None,
+                                ctypes.byref(h)) == ec.EMB_ENOMEM
+    assert lib.emb_cache_create(ctypes.byref(c), ctypes.c_void_p((1 << 20) + 4), s.state_bytes, fake,
+                                s.workspace_bytes, None, ctypes.byref(h)) == ec.EMB_EINVAL
+    assert not h.value
+
+
+def test_null_handle_rejected(lib):
+    assert lib.emb_cache_forward(None, None, 0, None, 0, None, None) == ec.EMB_EINVAL
+    assert lib.emb_cache_backward_update(None, None, 0, None, 0, None, None) == ec.EMB_EINVAL
+    assert lib.emb_cache_check(None, None) == ec.EMB_EINVAL
+    assert lib.emb_cache_destroy(None) == 0

@@ -1,0 +1,164 @@
+"""GPU parity: the HIP library (through the C ABI) against the CPU oracle, same
+seeded inputs, every state array compared after every step (see parity.py)."""
+import numpy as np
+import pytest
+
+from common import custom_cfg, oracle_from_cfg
+from parity import assert_f32, assert_same, compare_state, log, make_pair, step_both, to_dev
+from paper_2010_11305_amd import configs, workload
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+    if not t.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2010_11305_amd import emb_cache
+    emb_cache.load()
+    return t
+
+
+INIT_CASES = [(d, b, sb) for d in (16, 32, 64, 128, 256) for b in (8, 4) for sb in (False, True)]
+
+
+@pytest.mark.parametrize("dim,bits,sb16", INIT_CASES)
+def test_init_uniform_parity(torch, dim, bits, sb16):
+    cfg = custom_cfg(rows=[1000, 37, 2049], dim=dim, bits=bits, sb_fp16=sb16)
+    log(f"init parity dim={dim} bits={bits} sb16={sb16}")
+    o, g = make_pair(cfg)
+    compare_state(o, g, cfg)
+
+
+def test_forward_from_imported_state(torch):
+    """Oracle trains 4 steps; its state is imported into the GPU; pooled outputs match."""
+    cfg = configs.get("tiny")
+    log("forward from imported oracle state")
+    o, g = make_pair(cfg)
+    for k in range(4):
+        st = workload.make_step(cfg, k)
+        o.forward(st["indices"], st["offsets"], st["batch"])
+        o.backward_update(st["indices"], st["offsets"], st["batch"], st["grad"])
+    r, c = o.export_rows(0), o.export_cache(0)
+    g.import_rows(0, 0, r["codes"], r["scale"], r["bias"], r["cnt"], r["G"])
+    g.import_cache(0, c["crow"], c["tag"], c["ts"])
+    g.step = o.step
+    compare_state(o, g, cfg)
+    st = workload.make_step(cfg, 4)
+    idx, off, _ = to_dev(st, torch)
+    out_g = g.forward(idx, off, st["batch"]).cpu().numpy()
+    out_o = o.forward(st["indices"], st["offsets"], st["batch"])
+    assert_f32(out_g, out_o, "pooled")
+    assert g.stats(0)["hit_lookups"] == o.stats(0)["hit_lookups"] > 0
+
+
+STEP_CASES = {
+    "tiny": {},
+    "tiny_sr": {"rounding": "stochastic"},
+    "tiny_int4_fp16_lfu_adagrad": {"bits": 4, "sb_fp16": True, "policy": "lfu", "lfu_decay_interval": 3,
+                                   "rounding": "stochastic", "optimizer": "adagrad"},
+    "tiny_assoc1_lru": {"assoc": 1, "cache_fraction": 0.05},
+    "tiny_assoc1_lfu": {"assoc": 1, "policy": "lfu"},
+    "tiny_assoc2_lfu_sgd": {"assoc": 2, "policy": "lfu", "cache_fraction": 0.1},
+    "tiny_assoc32_bigcache": {"assoc": 32, "cache_fraction": 0.3, "batch": 300, "pooling": ("uniform", 1, 12)},
+    "tiny_nocache": {"cache_fraction": 0.0},
+    "tiny_fullcover": {"cache_fraction": 1.024, "assoc": 32},
+    "d32_int4": {"dim": 32, "bits": 4, "rounding": "stochastic"},
+    "d64_int8_adagrad": {"dim": 64, "optimizer": "adagrad"},
+    "d128_int4_fp16_lru16": {"dim": 128, "bits": 4, "sb_fp16": True, "assoc": 16, "cache_fraction": 0.05,
+                             "rounding": "stochastic", "optimizer": "adagrad", "pooling": ("poisson", 30), "zipf": 1.2},
+    "d256_int8_sr": {"dim": 256, "rounding": "stochastic", "assoc": 32, "cache_fraction": 0.1, "lr": 0.05},
+    "hot_row": {"rows": [300], "zipf": 2.0, "batch": 600, "pooling": ("uniform", 1, 8), "assoc": 8},
+    "multi_table": {"rows": [1000, 5, 64, 3000], "batch": 96, "assoc": 4, "cache_fraction": 0.05},
+}
+
+
+@pytest.mark.parametrize("case", list(STEP_CASES))
+def test_step_parity(torch, case):
+    cfg = custom_cfg(**STEP_CASES[case])
+    log(f"step parity {case}: rows={cfg['rows'][:4]} dim={cfg['dim']} bits={cfg['bits']} assoc={cfg['assoc']}")
+    o, g = make_pair(cfg)
+    for k in range(8):
+        st = workload.make_step(cfg, k)
+        step_both(o, g, cfg, st, torch)
+        compare_state(o, g, cfg)
+    s = o.stats(0)
+    if cfg["cache_fraction"] > 0:
+        assert s["inserts"] + s["unique_hits"] > 0
+
+
+def test_kaggle_int8_full_size(torch):
+    """26 Table-1 tables at full size: 12 steps, outputs every step, whole state at the end."""
+    cfg = configs.get("kaggle_int8")
+    log("kaggle_int8 full size: oracle init (33.7M rows) ...")
+    o, g = make_pair(cfg)
+    for k in range(12):
+        step_both(o, g, cfg, workload.make_step(cfg, k), torch)
+    log("kaggle_int8: comparing state")
+    compare_state(o, g, cfg)
+
+
+def test_kaggle_int4_full_size(torch):
+    cfg = configs.get("kaggle_int4")
+    log("kaggle_int4 full size: oracle init (33.7M rows) ...")
+    o, g = make_pair(cfg)
+    for k in range(12):   # crosses the LFU decay at step 10
+        step_both(o, g, cfg, workload.make_step(cfg, k), torch)
+    log("kaggle_int4: comparing state")
+    compare_state(o, g, cfg)
+
+
+def test_invalid_indices_and_empty_bags(torch):
+    from paper_2010_11305_amd.emb_cache import EMB_EINDEX, EMB_OK
+    cfg = custom_cfg(batch=4)
+    log("invalid indices / empty bags")
+    o, g = make_pair(cfg, max_indices=64)
+    st = {"indices": np.array([5, -1, 7, 1000, 3], dtype=np.int32), "offsets": np.array([0, 0, 2, 4, 5], dtype=np.int32),
+          "batch": 4, "grad": np.ones((4, 1, 16), dtype=np.float32)}
+    step_both(o, g, cfg, st, torch)
+    compare_state(o, g, cfg)
+    assert g.check() == EMB_EINDEX
+    assert g.check() == EMB_OK
+
+
+def test_malformed_offsets_skip_the_step(torch):
+    from paper_2010_11305_amd.emb_cache import EMB_EINDEX
+    cfg = custom_cfg(batch=4)
+    log("malformed offsets")
+    o, g = make_pair(cfg, max_indices=64)
+    before = g.export_rows(0)
+    idx = torch.tensor([1, 2, 3, 4, 5], dtype=torch.int32, device="cuda")
+    off = torch.tensor([0, 3, 2, 5, 5], dtype=torch.int32, device="cuda")   # decreasing
+    grad = torch.ones((4, 1, 16), dtype=torch.float32, device="cuda")
+    g.backward_update(idx, off, 4, grad)
+    assert g.check() == EMB_EINDEX
+    after = g.export_rows(0)
+    assert np.array_equal(before["codes"], after["codes"]) and g.stats(0)["unique"] == 0
+
+
+def test_determinism_and_resume(torch):
+    cfg = custom_cfg(bits=4, sb_fp16=True, rounding="stochastic", policy="lfu", lfu_decay_interval=2,
+                     optimizer="adagrad", assoc=4)
+    log("determinism / resume")
+    _, g1 = make_pair(cfg)
+    _, g2 = make_pair(cfg)
+    for k in range(3):
+        for g in (g1, g2):
+            st = workload.make_step(cfg, k)
+            idx, off, grad = to_dev(st, torch)
+            g.backward_update(idx, off, st["batch"], grad)
+    r, c = g2.export_rows(0), g2.export_cache(0)
+    _, g3 = make_pair(cfg)
+    g3.import_rows(0, 0, r["codes"], r["scale"], r["bias"], r["cnt"], r["G"])
+    g3.import_cache(0, c["crow"], c["tag"], c["ts"])
+    g3.step = g2.step
+    for k in range(3, 6):
+        for g in (g1, g3):
+            st = workload.make_step(cfg, k)
+            idx, off, grad = to_dev(st, torch)
+            g.backward_update(idx, off, st["batch"], grad)
+    a, b = g1.export_rows(0), g3.export_rows(0)
+    for key in a:
+        assert np.array_equal(a[key], b[key]), key
+    assert np.array_equal(g1.export_cache(0)["crow"], g3.export_cache(0)["crow"])
