@@ -1,11 +1,12 @@
 // Device-side building blocks of libembcache (gfx950, wave64).
 //
 // Lane layout of one embedding row of width D: a row is handled by a group of
-// LPR = min(D, 64) consecutive lanes; lane g of the group holds the CPL = D/LPR
-// columns g, g + LPR, g + 2*LPR, ...  Column pairs (j, j + D/2) of the
-// halving-tree sum therefore sit in the same lane while D > 64 and in lanes
-// g, g ^ (D/2) below, and consecutive columns (2m, 2m+1) of an INT4 byte sit
-// in neighbouring lanes.
+// LPR = D/8 consecutive lanes (2..32), and lane g of the group holds the 8
+// contiguous columns [8g, 8g+8).  So an FP32 row is two 16-byte loads per lane,
+// the INT4 codes of a lane are one dword (INT8: two), the 8 stochastic-rounding
+// uniforms of a lane are the 8 words of two Philox blocks, and a wave works on
+// 64/LPR rows at once.  The halving-tree sum pairs columns (j, j + h): lanes
+// g and g ^ (h/8) while h >= 8, then inside a lane.
 #pragma once
 
 #include <hip/hip_fp16.h>
@@ -18,9 +19,9 @@ namespace embc {
 
 template <int D>
 struct Geo {
-  static constexpr int LPR = D < 64 ? D : 64;  // lanes per row
-  static constexpr int CPL = D / LPR;          // columns per lane
-  static constexpr int GPW = 64 / LPR;         // row groups per wave
+  static constexpr int CPL = 8;        // contiguous columns per lane
+  static constexpr int LPR = D / CPL;  // lanes per row
+  static constexpr int GPW = 64 / LPR; // rows per wave
 };
 
 template <int D, int BITS, bool SB16>
@@ -43,14 +44,17 @@ __device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1
   return c;
 }
 
-// Uniform in [0,1) with 24 bits for element (table, row, col) at `step`:
-// counter (col/4, row, table, step), key (seed lo, seed hi), word col%4.
-__device__ __forceinline__ float sr_uniform(uint64_t seed, uint32_t step, uint32_t table, uint32_t row,
-                                            uint32_t col) {
-  const uint4 o = philox4x32_10(make_uint4(col >> 2, row, table, step), (uint32_t)seed, (uint32_t)(seed >> 32));
-  const uint32_t q = col & 3u;
-  const uint32_t w = q == 0 ? o.x : (q == 1 ? o.y : (q == 2 ? o.z : o.w));
-  return (float)(w >> 8) * 5.9604644775390625e-08f;  // 2^-24
+__device__ __forceinline__ float u24(uint32_t w) { return (float)(w >> 8) * 5.9604644775390625e-08f; }  // 2^-24
+
+// The 8 uniforms of columns [8g, 8g+8) of (table, row) at `step`: column j uses
+// word j%4 of the block with counter (j/4, row, table, step) and key (seed lo, seed hi).
+__device__ __forceinline__ void uniforms8(uint64_t seed, uint32_t step, uint32_t table, uint32_t row, int g,
+                                          float (&u)[8]) {
+  const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+  const uint4 a = philox4x32_10(make_uint4(2u * g, row, table, step), k0, k1);
+  const uint4 b = philox4x32_10(make_uint4(2u * g + 1u, row, table, step), k0, k1);
+  u[0] = u24(a.x); u[1] = u24(a.y); u[2] = u24(a.z); u[3] = u24(a.w);
+  u[4] = u24(b.x); u[5] = u24(b.y); u[6] = u24(b.z); u[7] = u24(b.w);
 }
 
 __device__ __forceinline__ float f16_round(float x) { return __half2float(__float2half(x)); }
@@ -63,42 +67,60 @@ __device__ __forceinline__ void load_sb(const uint8_t* rec, float& s, float& b) 
     s = __half2float(__ushort_as_half((unsigned short)(w & 0xFFFFu)));
     b = __half2float(__ushort_as_half((unsigned short)(w >> 16)));
   } else {
-    const float2 v = *reinterpret_cast<const float2*>(rec + CB);
-    s = v.x;
-    b = v.y;
+    const float* p = reinterpret_cast<const float*>(rec + CB);
+    s = p[0];
+    b = p[1];
   }
 }
 
+// Raw code words of lane g: INT4 one dword (8 nibbles, column 8g+i in nibble i),
+// INT8 two dwords (column 8g+i in byte i).
 template <int BITS>
-__device__ __forceinline__ uint32_t load_code(const uint8_t* rec, int col) {
-  if constexpr (BITS == 8) {
-    return rec[col];
-  } else {
-    const uint32_t byte = rec[col >> 1];
-    return (byte >> ((col & 1) * 4)) & 15u;
-  }
+struct CodeWords {
+  uint32_t w[BITS == 8 ? 2 : 1];
+};
+
+template <int BITS>
+__device__ __forceinline__ CodeWords<BITS> load_code_words(const uint8_t* rec, int g) {
+  CodeWords<BITS> c;
+  const uint32_t* p = reinterpret_cast<const uint32_t*>(rec) + g * (BITS == 8 ? 2 : 1);
+  c.w[0] = p[0];
+  if constexpr (BITS == 8) c.w[1] = p[1];
+  return c;
+}
+
+template <int BITS>
+__device__ __forceinline__ uint32_t code_of(const CodeWords<BITS>& c, int i) {
+  if constexpr (BITS == 8) return (c.w[i >> 2] >> (8 * (i & 3))) & 0xFFu;
+  else return (c.w[0] >> (4 * i)) & 0xFu;
+}
+
+template <int BITS>
+__device__ __forceinline__ void dequant8(const CodeWords<BITS>& c, float s, float b, float (&x)[8]) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) x[i] = __builtin_fmaf((float)code_of<BITS>(c, i), s, b);
 }
 
 // fetch() of a non-resident row: q*s + b with one rounding (Alg. 1 dequantization).
 template <int D, int BITS, bool SB16>
-__device__ __forceinline__ void dequant_row(const uint8_t* rec, int g, float (&x)[Geo<D>::CPL]) {
+__device__ __forceinline__ void dequant_row(const uint8_t* rec, int g, float (&x)[8]) {
   float s, b;
+  const CodeWords<BITS> c = load_code_words<BITS>(rec, g);
   load_sb<D, BITS, SB16>(rec, s, b);
-#pragma unroll
-  for (int k = 0; k < Geo<D>::CPL; ++k)
-    x[k] = __builtin_fmaf((float)load_code<BITS>(rec, g + Geo<D>::LPR * k), s, b);
+  dequant8<BITS>(c, s, b, x);
 }
 
-template <int D>
-__device__ __forceinline__ void load_frow(const float* row, int g, float (&x)[Geo<D>::CPL]) {
-#pragma unroll
-  for (int k = 0; k < Geo<D>::CPL; ++k) x[k] = row[g + Geo<D>::LPR * k];
+__device__ __forceinline__ void load_frow8(const float* row, int g, float (&x)[8]) {
+  const float4* p = reinterpret_cast<const float4*>(row) + 2 * g;
+  const float4 a = p[0], b = p[1];
+  x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+  x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
 }
 
-template <int D>
-__device__ __forceinline__ void store_frow(float* row, int g, const float (&x)[Geo<D>::CPL]) {
-#pragma unroll
-  for (int k = 0; k < Geo<D>::CPL; ++k) row[g + Geo<D>::LPR * k] = x[k];
+__device__ __forceinline__ void store_frow8(float* row, int g, const float (&x)[8]) {
+  float4* p = reinterpret_cast<float4*>(row) + 2 * g;
+  p[0] = make_float4(x[0], x[1], x[2], x[3]);
+  p[1] = make_float4(x[4], x[5], x[6], x[7]);
 }
 
 // Down-conversion of one FP32 row into its low-precision record (Alg. 1 with the
@@ -106,16 +128,16 @@ __device__ __forceinline__ void store_frow(float* row, int g, const float (&x)[G
 // rounded; then rounded to FP16 when SB16); codes q = round((x - b)/s) clamped to
 // [0, 2^BITS - 1], all zero when s == 0.  A -0 extreme is taken as +0.
 template <int D, int BITS, bool SB16>
-__device__ __forceinline__ void quantize_store(const float (&x)[Geo<D>::CPL], int g, uint8_t* rec, bool sr,
-                                               uint64_t seed, uint32_t step, uint32_t table, uint32_t row) {
-  constexpr int LPR = Geo<D>::LPR, CPL = Geo<D>::CPL;
+__device__ __forceinline__ void quantize_store(const float (&x)[8], int g, uint8_t* rec, bool sr, uint64_t seed,
+                                               uint32_t step, uint32_t table, uint32_t row) {
+  constexpr int LPR = Geo<D>::LPR;
   constexpr int CB = Rec<D, BITS, SB16>::CODE_BYTES;
   constexpr float K = (float)((1 << BITS) - 1);
   float mn = x[0], mx = x[0];
 #pragma unroll
-  for (int k = 1; k < CPL; ++k) {
-    mn = fminf(mn, x[k]);
-    mx = fmaxf(mx, x[k]);
+  for (int i = 1; i < 8; ++i) {
+    mn = fminf(mn, x[i]);
+    mx = fmaxf(mx, x[i]);
   }
 #pragma unroll
   for (int o = LPR / 2; o >= 1; o >>= 1) {
@@ -130,16 +152,17 @@ __device__ __forceinline__ void quantize_store(const float (&x)[Geo<D>::CPL], in
     s = f16_round(s);
     b = f16_round(b);
   }
+  float u[8];
+  if (sr && s != 0.0f) uniforms8(seed, step, table, row, g, u);
+  uint32_t w0 = 0, w1 = 0;
 #pragma unroll
-  for (int k = 0; k < CPL; ++k) {
-    const int col = g + LPR * k;
+  for (int i = 0; i < 8; ++i) {
     float qf = 0.0f;
     if (s != 0.0f) {
-      const float v = (x[k] - b) / s;
+      const float v = (x[i] - b) / s;
       if (sr) {
         const float f = floorf(v);
-        const float u = sr_uniform(seed, step, table, row, (uint32_t)col);
-        qf = (u < v - f) ? f + 1.0f : f;
+        qf = (u[i] < v - f) ? f + 1.0f : f;
       } else {
         qf = rintf(v);
       }
@@ -148,18 +171,22 @@ __device__ __forceinline__ void quantize_store(const float (&x)[Geo<D>::CPL], in
     }
     const uint32_t q = (uint32_t)qf;
     if constexpr (BITS == 8) {
-      rec[col] = (uint8_t)q;
+      if (i < 4) w0 |= q << (8 * i);
+      else w1 |= q << (8 * (i - 4));
     } else {
-      const uint32_t hi = (uint32_t)__shfl_xor((int)q, 1, LPR);
-      if ((g & 1) == 0) rec[col >> 1] = (uint8_t)(q | (hi << 4));
+      w0 |= q << (4 * i);
     }
   }
+  uint32_t* p = reinterpret_cast<uint32_t*>(rec) + g * (BITS == 8 ? 2 : 1);
+  p[0] = w0;
+  if constexpr (BITS == 8) p[1] = w1;
   if (g == 0) {
+    uint32_t* ps = reinterpret_cast<uint32_t*>(rec + CB);
     if constexpr (SB16) {
-      const uint32_t w = (uint32_t)__half_as_ushort(__float2half(s)) | ((uint32_t)__half_as_ushort(__float2half(b)) << 16);
-      *reinterpret_cast<uint32_t*>(rec + CB) = w;
+      ps[0] = (uint32_t)__half_as_ushort(__float2half(s)) | ((uint32_t)__half_as_ushort(__float2half(b)) << 16);
     } else {
-      *reinterpret_cast<float2*>(rec + CB) = make_float2(s, b);
+      ps[0] = __float_as_uint(s);
+      ps[1] = __float_as_uint(b);
     }
   }
 }
@@ -194,6 +221,35 @@ __device__ __forceinline__ int32_t probe_slot(const Dev& dv, const TableDesc& td
       if (tg[w] == r) return (int32_t)(base + w);
   }
   return -1;
+}
+
+// XCD-aware work split.  Workgroups are dispatched round-robin over the 8 XCDs
+// (workgroup i on XCD i % 8), each with its own L2.  Work is cut into T*P segments
+// (table t, part p; P parts per table so that there are at least 8 segments) and
+// XCD x takes segments x, x+8, ...; inside an XCD, its workgroups share a segment.
+// Every segment sees the same L2, so a table's hot cache rows, tags and gradient
+// rows are fetched into one L2 instead of eight.
+constexpr int kXcds = 8;
+
+struct XcdSplit {
+  int xcd;          // this workgroup's XCD
+  int64_t unit;     // this workgroup's index among the XCD's workgroups
+  int64_t units;    // workgroups per XCD
+  int parts;        // parts per table
+  __device__ XcdSplit(int T) {
+    xcd = blockIdx.x % kXcds;
+    unit = blockIdx.x / kXcds;
+    units = gridDim.x / kXcds;
+    parts = T >= kXcds ? 1 : (kXcds + T - 1) / T;
+  }
+  __device__ int segments(int T) const { return T * parts; }
+};
+
+// [lo, hi) of `part` out of `parts` equal slices of [a, b).
+__device__ __forceinline__ void part_range(int64_t a, int64_t b, int part, int parts, int64_t& lo, int64_t& hi) {
+  const int64_t n = b - a;
+  lo = a + n * part / parts;
+  hi = a + n * (part + 1) / parts;
 }
 
 __device__ __forceinline__ uint64_t lanemask_lt() {

@@ -93,10 +93,8 @@ struct Work {
   int32_t* udest;        // [L] destination slot of an insert
   uint32_t* nch;         // [L] chunk count (rows with > kSumChunk occurrences), then its prefix
   uint32_t* chunk_base;  // [L+1]
-  int32_t* vic_slot;     // [L] displaced residents not updated this step
-  int32_t* vic_row;      // [L] their global row
-  int32_t* vic_tab;      // [L]
-  int32_t* ins_list;     // [L] unique rows inserted this step
+  int32_t* uvic_row;     // [L] insert: table-local row displaced from its way, -1 = empty way
+  int32_t* uvic_u;       // [L] insert: unique index of that row if it was updated this step, else -1
   float* partial;        // [L/32 + 2][dim] chunk sums
   unsigned long long* ctr;  // counters, see kC*
   int64_t max_indices;

@@ -42,7 +42,7 @@ __device__ __forceinline__ int table_of_row(const Dev& dv, int64_t grow) {
 // then nearest-even quantization of the row.
 template <int D, int BITS, bool SB16>
 __global__ __launch_bounds__(256) void k_init_uniform(Dev dv, float lo, float hi, uint64_t init_seed) {
-  constexpr int LPR = Geo<D>::LPR, CPL = Geo<D>::CPL;
+  constexpr int LPR = Geo<D>::LPR;
   constexpr int RB = Rec<D, BITS, SB16>::BYTES;
   const int g = threadIdx.x & (LPR - 1);
   const int64_t ngroups = (int64_t)gridDim.x * blockDim.x / LPR;
@@ -51,10 +51,10 @@ __global__ __launch_bounds__(256) void k_init_uniform(Dev dv, float lo, float hi
        grow += ngroups) {
     const int t = table_of_row(dv, grow);
     const uint32_t r = (uint32_t)(grow - dv.desc[t].row_base);
-    float x[CPL];
+    float u[8], x[8];
+    uniforms8(init_seed, 0xFFFFFFFFu, (uint32_t)t, r, g, u);
 #pragma unroll
-    for (int k = 0; k < CPL; ++k)
-      x[k] = __builtin_fmaf(sr_uniform(init_seed, 0xFFFFFFFFu, (uint32_t)t, r, (uint32_t)(g + LPR * k)), width, lo);
+    for (int i = 0; i < 8; ++i) x[i] = __builtin_fmaf(u[i], width, lo);
     quantize_store<D, BITS, SB16>(x, g, dv.rec + grow * RB, false, 0, 0, 0, 0);
   }
 }
@@ -74,21 +74,23 @@ hipError_t launch_init_uniform(const Dev& d, float lo, float hi, uint64_t init_s
 }
 
 // ---- forward --------------------------------------------------------------------------
-// One group of LPR lanes per bag, `bpg` consecutive bags per group.  For each
-// chunk of up to LPR positions, lane j loads index j and probes its set; then
-// the rows are gathered one after the other (each lane its columns) and summed
-// left to right.  A bag with no valid lookup gives +0.
+// One group of LPR lanes per bag (64/LPR bags per wave at once); tables are split
+// over the XCDs (XcdSplit), and the groups of an XCD share the bags of its current
+// table.  For each chunk of up to LPR positions, lane j loads index j and probes its
+// set.  The rows are then fetched FU at a time -- all FU loads (FP32 cache row, or
+// codes and scale/bias) issued before any is used -- and summed left to right.  A
+// bag with no valid lookup gives +0.
+constexpr int kFwdUnroll = 4;
+
 template <int D, int BITS, bool SB16>
 __global__ __launch_bounds__(256) void k_forward(Dev dv, const int32_t* __restrict__ idx, int64_t L,
-                                                 const int32_t* __restrict__ off, int32_t B, float* __restrict__ out,
-                                                 int bpg) {
-  constexpr int LPR = Geo<D>::LPR, CPL = Geo<D>::CPL;
+                                                 const int32_t* __restrict__ off, int32_t B, float* __restrict__ out) {
+  constexpr int LPR = Geo<D>::LPR, FU = kFwdUnroll;
+  constexpr int GPB = 256 / LPR;
   constexpr int RB = Rec<D, BITS, SB16>::BYTES;
   const int g = threadIdx.x & (LPR - 1);
-  const int64_t grp = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / LPR;
-  const int64_t nbags = (int64_t)dv.T * B;
-  int64_t bag = grp * bpg;
-  const int64_t bag_end = min<int64_t>(bag + bpg, nbags);
+  const XcdSplit xs(dv.T);
+  const int64_t gx = xs.unit * GPB + threadIdx.x / LPR, gstride = xs.units * GPB;
   int cur_t = -1;
   uint32_t c_valid = 0, c_hit = 0, c_bad = 0;
   auto flush = [&]() {
@@ -109,20 +111,24 @@ __global__ __launch_bounds__(256) void k_forward(Dev dv, const int32_t* __restri
     }
     c_valid = c_hit = c_bad = 0;
   };
-  for (; bag < bag_end; ++bag) {
-    const int t = (int)(bag / B);
-    if (t != cur_t) {
-      flush();
-      cur_t = t;
-    }
-    const int b = (int)(bag - (int64_t)t * B);
-    const TableDesc td = dv.desc[t];
+  for (int seg = xs.xcd; seg < xs.segments(dv.T); seg += kXcds) {
+   const int t = seg / xs.parts;
+   int64_t blo, bhi;
+   part_range(0, B, seg % xs.parts, xs.parts, blo, bhi);
+   if (t != cur_t) {
+     flush();
+     cur_t = t;
+   }
+   const TableDesc td = dv.desc[t];
+   for (int64_t b = blo + gx; b < bhi; b += gstride) {
+    const int64_t bag = (int64_t)t * B + b;
+    const uint8_t* rec0 = dv.rec + td.row_base * RB;
     int64_t p0 = off[bag], p1 = off[bag + 1];
     p0 = p0 < 0 ? 0 : p0;
     p1 = p1 > L ? L : p1;
-    float acc[CPL];
+    float acc[8];
 #pragma unroll
-    for (int k = 0; k < CPL; ++k) acc[k] = 0.0f;
+    for (int i = 0; i < 8; ++i) acc[i] = 0.0f;
     bool first = true;
     for (int64_t pc = p0; pc < p1; pc += LPR) {
       const int n = (int)min<int64_t>(LPR, p1 - pc);
@@ -138,36 +144,44 @@ __global__ __launch_bounds__(256) void k_forward(Dev dv, const int32_t* __restri
           ++c_bad;
         }
       }
-      for (int j = 0; j < n; ++j) {
-        if (!__shfl(ok, j, LPR)) continue;
-        const int32_t rj = __shfl(r, j, LPR);
-        const int32_t sj = __shfl(slot, j, LPR);
-        float v[CPL];
-        if (sj >= 0) {
-          load_frow<D>(dv.crow + (int64_t)sj * D, g, v);
-        } else {
-          dequant_row<D, BITS, SB16>(dv.rec + (td.row_base + rj) * RB, g, v);
+      for (int j = 0; j < n; j += FU) {
+        float raw[FU][8];
+        CodeWords<BITS> cw[FU];
+        float sq[FU], bq[FU];
+        int kind[FU];  // 0 skip, 1 cache row, 2 low-precision row
+#pragma unroll
+        for (int q = 0; q < FU; ++q) {
+          const int okq = __shfl(ok, j + q, LPR);
+          const int32_t rq = __shfl(r, j + q, LPR);
+          const int32_t sl = __shfl(slot, j + q, LPR);
+          kind[q] = (j + q < n && okq) ? (sl >= 0 ? 1 : 2) : 0;
+          if (kind[q] == 1) {
+            load_frow8(dv.crow + (int64_t)sl * D, g, raw[q]);
+          } else if (kind[q] == 2) {
+            const uint8_t* rec = rec0 + (int64_t)rq * RB;
+            cw[q] = load_code_words<BITS>(rec, g);
+            load_sb<D, BITS, SB16>(rec, sq[q], bq[q]);
+          }
         }
-        if (first) {
 #pragma unroll
-          for (int k = 0; k < CPL; ++k) acc[k] = v[k];
-          first = false;
-        } else {
+        for (int q = 0; q < FU; ++q) {
+          if (kind[q] == 0) continue;
+          if (kind[q] == 2) dequant8<BITS>(cw[q], sq[q], bq[q], raw[q]);
+          if (first) {
 #pragma unroll
-          for (int k = 0; k < CPL; ++k) acc[k] = acc[k] + v[k];
+            for (int i = 0; i < 8; ++i) acc[i] = raw[q][i];
+            first = false;
+          } else {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) acc[i] = acc[i] + raw[q][i];
+          }
         }
       }
     }
-    store_frow<D>(out + ((int64_t)b * dv.T + t) * D, g, acc);
+    store_frow8(out + ((int64_t)b * dv.T + t) * D, g, acc);
+   }
   }
   flush();
-}
-
-__global__ void k_zero_stats(Dev dv, int first, int last) {
-  for (int i = threadIdx.x; i < dv.T * kNStat; i += blockDim.x) {
-    const int f = i % kNStat;
-    if (f >= first && f <= last) dv.stats[i] = 0;
-  }
 }
 
 __global__ void k_zero_fwd_stats(Dev dv) {
@@ -184,10 +198,12 @@ hipError_t launch_forward(const Dev& d, const int32_t* idx, int64_t L, const int
   const int64_t nbags = (int64_t)d.T * B;
   if (nbags == 0) return hipGetLastError();
   return dispatch_row(d.dim, d.bits, d.sb16, [&]<int D, int BITS, bool SB16>() -> hipError_t {
-    const int bpg = 4;
-    const int64_t groups = (nbags + bpg - 1) / bpg;
-    const int64_t threads = groups * Geo<D>::LPR;
-    k_forward<D, BITS, SB16><<<(unsigned)((threads + 255) / 256), 256, 0, s>>>(d, idx, L, off, B, out, bpg);
+    // whole multiples of 8 workgroups (one per XCD), at most 8 per CU
+    const int64_t wgs = (nbags * Geo<D>::LPR + 255) / 256;
+    int64_t blocks = (wgs + 7) / 8 * 8;
+    blocks = blocks < 8 ? 8 : (blocks > 2048 ? 2048 : blocks);
+    const unsigned grid = (unsigned)blocks;
+    k_forward<D, BITS, SB16><<<grid, 256, 0, s>>>(d, idx, L, off, B, out);
     return hipGetLastError();
   });
 }

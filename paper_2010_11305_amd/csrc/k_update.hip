@@ -1,24 +1,28 @@
 // Backward + sparse update of one step (Sec. 3 update operator, Alg. 2, Sec. 5.1 de-dup).
 //
 // After the sort (k_sort.hip) the lookups are grouped by row, the rows by set:
-//   k_probe        per unique row: residency (slot or miss), LRU stamp / LFU count update
-//   k_policy       per touched set (one wave, one lane per way): which missed rows
-//                  enter the cache, which residents leave
-//   k_partials     chunk sums of the merged gradient of rows with > 64 lookups
-//   k_update_main  per unique row not inserted, and per displaced resident: merged
-//                  gradient, fetch, optimizer, write to the cache way or quantize into T
-//   k_update_ins   per inserted row: same, written into its new way (after every
-//                  displaced resident has been read)
+//   k_probe     per unique row: residency (slot or miss), LRU stamp / LFU count update
+//   k_partials  chunk sums (64 lookups each) of the merged gradient of rows with > 64 lookups
+//   k_policy    per touched set, one wave (one lane per way): which missed rows enter the
+//               cache and which resident each of them displaces (decisions only)
+//   k_update    per unique row: merged gradient, fetch, optimizer, then the cache way (hit)
+//               or quantization into T (bypass); an inserted row first quantizes the
+//               resident it displaces into T -- updating it first if it was itself
+//               updated this step (LFU) -- then writes itself into the way
+// The row kernels split tables over the XCDs (XcdSplit) so that each L2 serves one table.
 #include "embc_device.h"
 #include "embc_dispatch.h"
 #include "embc_sort.h"
 
 namespace embc {
 
-constexpr int kGrid = 2048;  // blocks of the grid-stride kernels (8 per CU)
+constexpr int kGrid = 2048;      // blocks of the grid-stride kernels (8 per CU)
+constexpr int32_t kActDone = 4;  // row fully handled by k_policy
 
-// Sum `v` over the active lanes of the wave, per table: one atomic for the lanes
-// that share the first active lane's table, one per lane for the others.
+constexpr int kUnroll = 4;  // independent row loads in flight per row group
+
+// Per-table counts of the active lanes (tables may differ across lanes): one atomic
+// for the lanes sharing the first active lane's table, one per lane for the others.
 // Must be called by all 64 lanes.
 __device__ __forceinline__ void wave_stat_add(unsigned long long* stats, int t, int field, uint32_t v, bool active) {
   const uint64_t act = __ballot(active && v != 0);
@@ -32,18 +36,6 @@ __device__ __forceinline__ void wave_stat_add(unsigned long long* stats, int t, 
   const int lane = threadIdx.x & 63;
   if (lane == leader && s) atomicAdd(&stats[(int64_t)t0 * kNStat + field], (unsigned long long)s);
   if (active && !same && v) atomicAdd(&stats[(int64_t)t * kNStat + field], (unsigned long long)v);
-}
-
-// Wave-aggregated append to a list: returns this lane's position (valid where `want`).
-__device__ __forceinline__ uint32_t wave_append(unsigned long long* counter, bool want) {
-  const uint64_t m = __ballot(want);
-  if (!m) return 0;
-  const int leader = __ffsll((unsigned long long)m) - 1;
-  const int lane = threadIdx.x & 63;
-  unsigned long long base = 0;
-  if (lane == leader) base = atomicAdd(counter, (unsigned long long)__popcll(m));
-  base = __shfl(base, leader);
-  return (uint32_t)(base + __popcll(m & lanemask_lt()));
 }
 
 __global__ void k_chunks_total(unsigned long long* ctr) { ctr[kCChunks] = ctr[kCScanTotal] & 0xFFFFFFFFull; }
@@ -90,7 +82,6 @@ __global__ __launch_bounds__(256) void k_probe(Dev dv, Work w, uint32_t step) {
       w.utab[u] = t;
       w.uslot[u] = slot;
       w.uact[u] = slot >= 0 ? kActHitStay : kActBypass;
-      w.udest[u] = slot;
       w.nch[u] = count > (uint32_t)kSumChunk ? (count + kSumChunk - 1) / kSumChunk : 0u;
       if (dv.policy == 0) {
         if (slot >= 0) dv.ts[slot] = (int32_t)step;
@@ -105,6 +96,160 @@ __global__ __launch_bounds__(256) void k_probe(Dev dv, Work w, uint32_t step) {
   }
 }
 
+// ---- merged gradient ----------------------------------------------------------------------
+// Left-to-right FP32 sum of the gradient rows of occurrences [i0, i1) of the sorted
+// stream (i0 < i1), seeded with the first.  Lane j of the group preloads the row
+// index of occurrence j of each chunk of LPR occurrences; U rows are loaded before
+// they are added in order.
+template <int D>
+__device__ __forceinline__ void sum_occ(const uint32_t* __restrict__ sval, int64_t i0, int64_t i1,
+                                        const float* __restrict__ grad, int g, float (&acc)[8]) {
+  constexpr int LPR = Geo<D>::LPR, CPL = 8, U = kUnroll;
+  bool first = true;
+  for (int64_t ic = i0; ic < i1; ic += LPR) {
+    const int n = (int)min<int64_t>(LPR, i1 - ic);
+    const uint32_t myv = g < n ? sval[ic + g] : 0u;
+    int j = 0;
+    if (first) {
+      load_frow8(grad + (int64_t)__shfl(myv, 0, LPR) * D, g, acc);
+      first = false;
+      j = 1;
+    }
+    for (; j + U <= n; j += U) {
+      float x[U][8];
+#pragma unroll
+      for (int q = 0; q < U; ++q) load_frow8(grad + (int64_t)__shfl(myv, j + q, LPR) * D, g, x[q]);
+#pragma unroll
+      for (int q = 0; q < U; ++q)
+#pragma unroll
+        for (int k = 0; k < CPL; ++k) acc[k] = acc[k] + x[q][k];
+    }
+    for (; j < n; ++j) {
+      float x[8];
+      load_frow8(grad + (int64_t)__shfl(myv, j, LPR) * D, g, x);
+#pragma unroll
+      for (int k = 0; k < CPL; ++k) acc[k] = acc[k] + x[k];
+    }
+  }
+}
+
+// Merged gradient of unique row u: its lookups directly (<= 64), else its chunk sums.
+template <int D>
+__device__ __forceinline__ void merged_grad(const Work& w, const uint32_t* __restrict__ sval,
+                                            const float* __restrict__ grad, int64_t u, int g,
+                                            float (&acc)[8]) {
+  constexpr int CPL = 8, U = kUnroll;
+  const uint32_t nch = w.nch[u];
+  if (nch == 0) {
+    sum_occ<D>(sval, w.seg[u], w.seg[u + 1], grad, g, acc);
+    return;
+  }
+  const float* p = w.partial + (int64_t)w.chunk_base[u] * D;
+  load_frow8(p, g, acc);
+  uint32_t c = 1;
+  for (; c + U <= nch; c += U) {
+    float x[U][8];
+#pragma unroll
+    for (int q = 0; q < U; ++q) load_frow8(p + (int64_t)(c + q) * D, g, x[q]);
+#pragma unroll
+    for (int q = 0; q < U; ++q)
+#pragma unroll
+      for (int k = 0; k < CPL; ++k) acc[k] = acc[k] + x[q][k];
+  }
+  for (; c < nch; ++c) {
+    float x[8];
+    load_frow8(p + (int64_t)c * D, g, x);
+#pragma unroll
+    for (int k = 0; k < CPL; ++k) acc[k] = acc[k] + x[k];
+  }
+}
+
+// [lo, hi) of the unique rows of table t (rows are sorted table-major).
+__device__ __forceinline__ void table_rows(const Work& w, int64_t nU, int t, int64_t& lo, int64_t& hi) {
+  int64_t a = 0, b = nU;
+  while (a < b) {  // first u with utab[u] >= t
+    const int64_t m = (a + b) >> 1;
+    if (w.utab[m] < t) a = m + 1; else b = m;
+  }
+  lo = a;
+  b = nU;
+  while (a < b) {  // first u with utab[u] > t
+    const int64_t m = (a + b) >> 1;
+    if (w.utab[m] <= t) a = m + 1; else b = m;
+  }
+  hi = a;
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void k_partials(Dev dv, Work w, const uint32_t* __restrict__ sval,
+                                                  const float* __restrict__ grad) {
+  constexpr int LPR = Geo<D>::LPR;
+  constexpr int GPB = 256 / LPR;
+  const int g = threadIdx.x & (LPR - 1);
+  const int64_t nC = (int64_t)w.ctr[kCChunks];
+  const int64_t nU = (int64_t)w.ctr[kCUnique];
+  if (nC == 0) return;
+  const XcdSplit xs(dv.T);
+  const int64_t gx = xs.unit * GPB + threadIdx.x / LPR, gstride = xs.units * GPB;
+  for (int seg = xs.xcd; seg < xs.segments(dv.T); seg += kXcds) {
+    const int t = seg / xs.parts;
+    int64_t ulo, uhi;
+    table_rows(w, nU, t, ulo, uhi);
+    const int64_t clo_t = ulo < nU ? (int64_t)w.chunk_base[ulo] : nC;
+    const int64_t chi_t = uhi < nU ? (int64_t)w.chunk_base[uhi] : nC;
+    int64_t clo, chi;
+    part_range(clo_t, chi_t, seg % xs.parts, xs.parts, clo, chi);
+    for (int64_t c = clo + gx; c < chi; c += gstride) {
+      // unique row owning chunk c: the largest u in [ulo, uhi) with chunk_base[u] <= c
+      int64_t lo = ulo, hi = uhi;
+      while (hi - lo > 1) {
+        const int64_t mid = (lo + hi) >> 1;
+        if ((int64_t)w.chunk_base[mid] <= c) lo = mid; else hi = mid;
+      }
+      const int64_t u = lo;
+      const int64_t j = c - (int64_t)w.chunk_base[u];
+      const int64_t i0 = (int64_t)w.seg[u] + j * kSumChunk;
+      const int64_t i1 = min<int64_t>(i0 + kSumChunk, (int64_t)w.seg[u + 1]);
+      float acc[8];
+      sum_occ<D>(sval, i0, i1, grad, g, acc);
+      store_frow8(w.partial + c * D, g, acc);
+    }
+  }
+}
+
+// ---- optimizer (FP32) -----------------------------------------------------------------------
+// SGD: x = fma(-lr, g, x).  Row-wise Adagrad: S = halving-tree sum of g_j^2
+// (a[j] += a[j + h] for h = D/2, ..., 1: across lanes g ^ (h/8) while h >= 8, then
+// inside the lane), G += S * (1/D), r = lr / (sqrt(G) + eps), x = fma(-r, g, x).
+template <int D>
+__device__ __forceinline__ void apply_optimizer(const Dev& dv, float (&x)[8], const float (&gr)[8], int64_t grow,
+                                                int g, float G_old) {
+  constexpr int LPR = Geo<D>::LPR;
+  if (dv.optimizer == 0) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] = __builtin_fmaf(-dv.lr, gr[i], x[i]);
+    return;
+  }
+  float a[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) a[i] = gr[i] * gr[i];
+#pragma unroll
+  for (int o = LPR / 2; o >= 1; o >>= 1)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) a[i] = a[i] + __shfl_xor(a[i], o, LPR);
+#pragma unroll
+  for (int h = 4; h >= 1; h >>= 1)
+#pragma unroll
+    for (int i = 0; i < h; ++i) a[i] = a[i] + a[i + h];
+  const float Gn = G_old + a[0] * (1.0f / (float)D);
+  if (g == 0) dv.G[grow] = Gn;
+  const float rate = dv.lr / (__builtin_sqrtf(Gn) + dv.eps);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) x[i] = __builtin_fmaf(-rate, gr[i], x[i]);
+}
+
+__device__ __forceinline__ float load_G(const Dev& dv, int64_t grow) { return dv.optimizer ? dv.G[grow] : 0.0f; }
+
 // ---- replacement decision, one wave per touched set ------------------------------------------
 struct PolicyLds {
   int32_t hitu[64];       // unique row that hit way w this step, or -1
@@ -112,6 +257,22 @@ struct PolicyLds {
   long long cand_pv[64];
   int32_t vic_way[64];    // victims by rank
   long long vic_pv[64];
+};
+
+// Statistics of the sets a wave handles, accumulated while the table does not change.
+struct PolicyStats {
+  int t = -1;
+  uint32_t ins = 0, byp = 0, ev = 0, em = 0, he = 0;
+  __device__ void flush(unsigned long long* stats) {
+    if (t < 0) return;
+    unsigned long long* s = stats + (int64_t)t * kNStat;
+    if (ins) atomicAdd(s + kStInserts, (unsigned long long)ins);
+    if (byp) atomicAdd(s + kStBypasses, (unsigned long long)byp);
+    if (ev) atomicAdd(s + kStEvictions, (unsigned long long)ev);
+    if (em) atomicAdd(s + kStEmptyFills, (unsigned long long)em);
+    if (he) atomicAdd(s + kStHitEvictions, (unsigned long long)he);
+    ins = byp = ev = em = he = 0;
+  }
 };
 
 __global__ __launch_bounds__(256) void k_policy(Dev dv, Work w, uint32_t step) {
@@ -123,13 +284,16 @@ __global__ __launch_bounds__(256) void k_policy(Dev dv, Work w, uint32_t step) {
   const int64_t nS = (int64_t)w.ctr[kCSets];
   const int64_t wave0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
-  for (int64_t k = wave0; k < nS; k += nwaves) {
+  // contiguous runs of sets per wave, so that the table (and its statistics) rarely changes
+  const int64_t per = (nS + nwaves - 1) / nwaves;
+  const int64_t k0 = wave0 * per, k1 = min<int64_t>(k0 + per, nS);
+  PolicyStats ps;  // meaningful in lane 0
+  for (int64_t k = k0; k < k1; ++k) {
     const int64_t u0 = w.set_first[k], u1 = w.set_first[k + 1];
     const int t = w.utab[u0];
     const TableDesc td = dv.desc[t];
     const int64_t r0 = (int64_t)w.urow[u0] - td.row_base;
-    const int64_t set = r0 % td.n_sets;
-    const int64_t sbase = td.slot_base + set * A;
+    const int64_t sbase = td.slot_base + (r0 % td.n_sets) * A;
 
     // residents that hit this step, and the number of missed rows
     L.hitu[lane] = -1;
@@ -147,6 +311,10 @@ __global__ __launch_bounds__(256) void k_policy(Dev dv, Work w, uint32_t step) {
     }
     __builtin_amdgcn_wave_barrier();
     if (M == 0) continue;
+    if (t != ps.t) {
+      if (lane == 0) ps.flush(dv.stats);
+      ps.t = t;
+    }
 
     // ways, their tags and priorities (empty = lowest)
     int32_t tg = -1;
@@ -155,8 +323,11 @@ __global__ __launch_bounds__(256) void k_policy(Dev dv, Work w, uint32_t step) {
       tg = dv.tag[sbase + lane];
       vpv = tg < 0 ? LLONG_MIN : (lru ? (long long)dv.ts[sbase + lane] : (long long)dv.cnt[td.row_base + tg]);
     }
-    // per-lane contributions to the statistics
-    uint32_t s_ins = 0, s_byp = 0, s_ev = 0, s_em = 0, s_he = 0;
+    // lane k < n_ins: the k-th insert (unique row my_u) takes way my_way, displacing my_old
+    // (-1 if the way was empty); my_hu is my_old's unique row if it was updated this step
+    int my_way = 0;
+    int32_t my_u = -1, my_old = -1, my_hu = -1;
+    int n_ins = 0;
 
     if (A == 1 && lru) {
       // direct-mapped LRU: no priority test; the largest missed row ends in the way
@@ -167,29 +338,10 @@ __global__ __launch_bounds__(256) void k_policy(Dev dv, Work w, uint32_t step) {
         const uint64_t m = __ballot(miss);
         if (m) win = c + 63 - __clzll((unsigned long long)m);
       }
-      const int32_t old = __shfl(tg, 0);
-      const int32_t hu = L.hitu[0];
-      const bool push_victim = lane == 0 && old >= 0 && hu < 0;
-      if (lane == 0) {
-        w.uact[win] = kActInsert;
-        w.udest[win] = (int32_t)sbase;
-        if (old >= 0 && hu >= 0) w.uact[hu] = kActHitEvict;
-      }
-      const uint32_t ip = wave_append(w.ctr + kCInserts, lane == 0);
-      if (lane == 0) w.ins_list[ip] = (int32_t)win;
-      const uint32_t vp = wave_append(w.ctr + kCVictims, push_victim);
-      if (push_victim) {
-        w.vic_slot[vp] = (int32_t)sbase;
-        w.vic_row[vp] = (int32_t)(td.row_base + old);
-        w.vic_tab[vp] = t;
-      }
-      if (lane == 0) {
-        s_ins = 1;
-        s_byp = (uint32_t)(M - 1);
-        s_ev = old >= 0;
-        s_em = old < 0;
-        s_he = old >= 0 && hu >= 0;
-      }
+      n_ins = 1;
+      my_u = (int32_t)win;
+      my_old = __shfl(tg, 0);
+      my_hu = my_old >= 0 ? L.hitu[0] : -1;
     } else {
       // victims ranked by (priority asc, way asc); every lane runs the shuffles
       int vr = 0;
@@ -245,218 +397,98 @@ __global__ __launch_bounds__(256) void k_policy(Dev dv, Work w, uint32_t step) {
       // the k-th candidate takes the k-th victim while strictly higher; stop at the first failure
       const bool ok = lane < K && L.cand_pv[lane] > L.vic_pv[lane];
       const uint64_t fail = __ballot(lane < K && !ok);
-      const int m = fail ? __ffsll((unsigned long long)fail) - 1 : (int)K;
-      bool push_victim = false;
-      int32_t vslot = 0, vrow = 0, cu = -1;
-      const int way = lane < m ? L.vic_way[lane] : 0;
-      const int32_t old = __shfl(tg, way);  // tag of the way this lane's candidate takes
-      if (lane < m) {
-        cu = L.cand_u[lane];
-        const int32_t slot = (int32_t)(sbase + way);
-        w.uact[cu] = kActInsert;
-        w.udest[cu] = slot;
-        s_ins = 1;
-        if (old < 0) {
-          s_em = 1;
-        } else {
-          s_ev = 1;
-          const int32_t hu = L.hitu[way];
-          if (hu >= 0) {
-            w.uact[hu] = kActHitEvict;
-            s_he = 1;
-          } else {
-            push_victim = true;
-            vslot = slot;
-            vrow = (int32_t)(td.row_base + old);
-          }
-        }
-      }
-      const uint32_t ip = wave_append(w.ctr + kCInserts, lane < m);
-      if (lane < m) w.ins_list[ip] = cu;
-      const uint32_t vp = wave_append(w.ctr + kCVictims, push_victim);
-      if (push_victim) {
-        w.vic_slot[vp] = vslot;
-        w.vic_row[vp] = vrow;
-        w.vic_tab[vp] = t;
-      }
-      if (lane == 0) s_byp = (uint32_t)(M - m);
+      n_ins = fail ? __ffsll((unsigned long long)fail) - 1 : (int)K;
+      my_way = lane < n_ins ? L.vic_way[lane] : 0;
+      my_old = __shfl(tg, my_way);
+      my_u = lane < n_ins ? L.cand_u[lane] : -1;
+      my_hu = (lane < n_ins && my_old >= 0) ? L.hitu[my_way] : -1;
       __builtin_amdgcn_wave_barrier();
     }
-    wave_stat_add(dv.stats, t, kStInserts, s_ins, true);
-    wave_stat_add(dv.stats, t, kStBypasses, s_byp, true);
-    wave_stat_add(dv.stats, t, kStEvictions, s_ev, true);
-    wave_stat_add(dv.stats, t, kStEmptyFills, s_em, true);
-    wave_stat_add(dv.stats, t, kStHitEvictions, s_he, true);
-  }
-}
-
-// ---- merged gradient ----------------------------------------------------------------------
-// Left-to-right FP32 sum of the gradient rows of occurrences [i0, i1) of the sorted
-// stream, starting from the first term.  Lane j of the group preloads the row
-// index of occurrence j of each chunk of LPR occurrences.
-template <int D>
-__device__ __forceinline__ void sum_occ(const uint32_t* __restrict__ sval, int64_t i0, int64_t i1,
-                                        const float* __restrict__ grad, int g, float (&acc)[Geo<D>::CPL]) {
-  constexpr int LPR = Geo<D>::LPR, CPL = Geo<D>::CPL;
-  bool first = true;
-  for (int64_t ic = i0; ic < i1; ic += LPR) {
-    const int n = (int)min<int64_t>(LPR, i1 - ic);
-    const uint32_t myv = g < n ? sval[ic + g] : 0u;
-    for (int j = 0; j < n; ++j) {
-      const uint32_t gv = __shfl(myv, j, LPR);
-      float x[CPL];
-      load_frow<D>(grad + (int64_t)gv * D, g, x);
-      if (first) {
-#pragma unroll
-        for (int k = 0; k < CPL; ++k) acc[k] = x[k];
-        first = false;
-      } else {
-#pragma unroll
-        for (int k = 0; k < CPL; ++k) acc[k] = acc[k] + x[k];
-      }
+    if (lane < n_ins) {
+      w.uact[my_u] = kActInsert;
+      w.udest[my_u] = (int32_t)(sbase + my_way);
+      w.uvic_row[my_u] = my_old;
+      w.uvic_u[my_u] = my_hu;
+      if (my_hu >= 0) w.uact[my_hu] = kActDone;  // handled by the row that displaces it
+    }
+    const uint32_t n_valid = (uint32_t)__popcll(__ballot(lane < n_ins && my_old >= 0));
+    const uint32_t n_hitev = (uint32_t)__popcll(__ballot(lane < n_ins && my_hu >= 0));
+    if (lane == 0) {
+      ps.ins += (uint32_t)n_ins;
+      ps.byp += (uint32_t)(M - n_ins);
+      ps.ev += n_valid;
+      ps.em += (uint32_t)n_ins - n_valid;
+      ps.he += n_hitev;
     }
   }
+  if (lane == 0) ps.flush(dv.stats);
 }
 
-template <int D>
-__device__ __forceinline__ void merged_grad(const Work& w, const uint32_t* __restrict__ sval,
-                                            const float* __restrict__ grad, int64_t u, int g,
-                                            float (&acc)[Geo<D>::CPL]) {
-  const uint32_t nch = w.nch[u];
-  if (nch == 0) {
-    sum_occ<D>(sval, w.seg[u], w.seg[u + 1], grad, g, acc);
-  } else {
-    const int64_t c0 = w.chunk_base[u];
-    load_frow<D>(w.partial + c0 * D, g, acc);
-    for (uint32_t c = 1; c < nch; ++c) {
-      float x[Geo<D>::CPL];
-      load_frow<D>(w.partial + (c0 + c) * D, g, x);
-#pragma unroll
-      for (int k = 0; k < Geo<D>::CPL; ++k) acc[k] = acc[k] + x[k];
-    }
-  }
-}
-
-template <int D>
-__global__ __launch_bounds__(256) void k_partials(Work w, const uint32_t* __restrict__ sval,
-                                                  const float* __restrict__ grad) {
-  constexpr int LPR = Geo<D>::LPR, CPL = Geo<D>::CPL;
-  const int g = threadIdx.x & (LPR - 1);
-  const int64_t nC = (int64_t)w.ctr[kCChunks];
-  const int64_t nU = (int64_t)w.ctr[kCUnique];
-  const int64_t ngroups = (int64_t)gridDim.x * blockDim.x / LPR;
-  for (int64_t c = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / LPR; c < nC; c += ngroups) {
-    // unique row owning chunk c: the largest u with chunk_base[u] <= c
-    int64_t lo = 0, hi = nU;
-    while (hi - lo > 1) {
-      const int64_t mid = (lo + hi) >> 1;
-      if ((int64_t)w.chunk_base[mid] <= c) lo = mid; else hi = mid;
-    }
-    const int64_t u = lo;
-    const int64_t j = c - (int64_t)w.chunk_base[u];
-    const int64_t i0 = (int64_t)w.seg[u] + j * kSumChunk;
-    const int64_t i1 = min<int64_t>(i0 + kSumChunk, (int64_t)w.seg[u + 1]);
-    float acc[CPL];
-    sum_occ<D>(sval, i0, i1, grad, g, acc);
-    store_frow<D>(w.partial + c * D, g, acc);
-  }
-}
-
-// ---- optimizer (FP32) -----------------------------------------------------------------------
-// SGD: x = fma(-lr, g, x).  Row-wise Adagrad: S = halving-tree sum of g_j^2
-// (a[j] += a[j + h] for h = D/2, ..., 1), G += S * (1/D), r = lr / (sqrt(G) + eps),
-// x = fma(-r, g, x).
-template <int D>
-__device__ __forceinline__ void apply_optimizer(const Dev& dv, float (&x)[Geo<D>::CPL], const float (&gr)[Geo<D>::CPL],
-                                                int64_t grow, int g) {
-  constexpr int LPR = Geo<D>::LPR, CPL = Geo<D>::CPL;
-  if (dv.optimizer == 0) {
-#pragma unroll
-    for (int k = 0; k < CPL; ++k) x[k] = __builtin_fmaf(-dv.lr, gr[k], x[k]);
-    return;
-  }
-  float a[CPL];
-#pragma unroll
-  for (int k = 0; k < CPL; ++k) a[k] = gr[k] * gr[k];
-#pragma unroll
-  for (int h = CPL / 2; h >= 1; h >>= 1)
-#pragma unroll
-    for (int k = 0; k < h; ++k) a[k] = a[k] + a[k + h];
-  float S = a[0];
-#pragma unroll
-  for (int o = LPR / 2; o >= 1; o >>= 1) S = S + __shfl_xor(S, o, LPR);
-  const float Gn = dv.G[grow] + S * (1.0f / (float)D);
-  if (g == 0) dv.G[grow] = Gn;
-  const float rate = dv.lr / (__builtin_sqrtf(Gn) + dv.eps);
-#pragma unroll
-  for (int k = 0; k < CPL; ++k) x[k] = __builtin_fmaf(-rate, gr[k], x[k]);
-}
-
-// ---- write-back of updated rows and displaced residents -------------------------------------
+// ---- per unique row: optimizer and write-back ------------------------------------------------
 template <int D, int BITS, bool SB16>
-__global__ __launch_bounds__(256) void k_update_main(Dev dv, Work w, const uint32_t* __restrict__ sval,
-                                                     const float* __restrict__ grad, uint32_t step) {
-  constexpr int LPR = Geo<D>::LPR, CPL = Geo<D>::CPL;
+__global__ __launch_bounds__(256) void k_update(Dev dv, Work w, const uint32_t* __restrict__ sval,
+                                                const float* __restrict__ grad, uint32_t step) {
+  constexpr int LPR = Geo<D>::LPR;
+  constexpr int GPB = 256 / LPR;
   constexpr int RB = Rec<D, BITS, SB16>::BYTES;
   const int g = threadIdx.x & (LPR - 1);
   const int64_t nU = (int64_t)w.ctr[kCUnique];
-  const int64_t nV = (int64_t)w.ctr[kCVictims];
-  const int64_t ngroups = (int64_t)gridDim.x * blockDim.x / LPR;
   const bool sr = dv.rounding != 0;
-  for (int64_t it = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / LPR; it < nU + nV; it += ngroups) {
-    float x[CPL];
-    if (it < nU) {
-      const int64_t u = it;
+  const XcdSplit xs(dv.T);
+  const int64_t gx = xs.unit * GPB + threadIdx.x / LPR, gstride = xs.units * GPB;
+  for (int seg = xs.xcd; seg < xs.segments(dv.T); seg += kXcds) {
+    const int t = seg / xs.parts;
+    int64_t tlo, thi, lo, hi;
+    table_rows(w, nU, t, tlo, thi);
+    part_range(tlo, thi, seg % xs.parts, xs.parts, lo, hi);
+    const TableDesc td = dv.desc[t];
+    for (int64_t u = lo + gx; u < hi; u += gstride) {
       const int32_t act = w.uact[u];
-      if (act == kActInsert) continue;
+      if (act == kActDone) continue;
       const int64_t grow = w.urow[u];
-      const int t = w.utab[u];
-      float gr[CPL];
-      merged_grad<D>(w, sval, grad, u, g, gr);
       uint8_t* rec = dv.rec + grow * RB;
       const int32_t slot = w.uslot[u];
-      if (act == kActBypass) dequant_row<D, BITS, SB16>(rec, g, x);
-      else load_frow<D>(dv.crow + (int64_t)slot * D, g, x);
-      apply_optimizer<D>(dv, x, gr, grow, g);
-      if (act == kActHitStay) {
-        store_frow<D>(dv.crow + (int64_t)slot * D, g, x);
-      } else {
-        const uint32_t r = (uint32_t)(grow - dv.desc[t].row_base);
-        quantize_store<D, BITS, SB16>(x, g, rec, sr, dv.seed, step, (uint32_t)t, r);
+      float gr[8], x[8];
+      if (act == kActInsert) {
+        const int32_t dst = w.udest[u];
+        const int32_t vrow = w.uvic_row[u];
+        if (vrow >= 0) {
+          // the displaced resident leaves the cache: its FP32 row goes to T (after its
+          // own update when it was also updated this step)
+          const int64_t vgrow = td.row_base + vrow;
+          float xv[8];
+          load_frow8(dv.crow + (int64_t)dst * D, g, xv);
+          const int32_t vu = w.uvic_u[u];
+          if (vu >= 0) {
+            const float Gv = load_G(dv, vgrow);
+            float gv[8];
+            merged_grad<D>(w, sval, grad, vu, g, gv);
+            apply_optimizer<D>(dv, xv, gv, vgrow, g, Gv);
+          }
+          quantize_store<D, BITS, SB16>(xv, g, dv.rec + vgrow * RB, sr, dv.seed, step, (uint32_t)t, (uint32_t)vrow);
+        }
+        dequant_row<D, BITS, SB16>(rec, g, x);
+        const float G_old = load_G(dv, grow);
+        merged_grad<D>(w, sval, grad, u, g, gr);
+        apply_optimizer<D>(dv, x, gr, grow, g, G_old);
+        store_frow8(dv.crow + (int64_t)dst * D, g, x);
+        if (g == 0) {
+          dv.tag[dst] = (int32_t)(grow - td.row_base);
+          if (dv.policy == 0) dv.ts[dst] = (int32_t)step;
+        }
+        continue;
       }
-    } else {
-      const int64_t v = it - nU;
-      const int32_t slot = w.vic_slot[v];
-      const int64_t grow = w.vic_row[v];
-      const int t = w.vic_tab[v];
-      load_frow<D>(dv.crow + (int64_t)slot * D, g, x);
-      const uint32_t r = (uint32_t)(grow - dv.desc[t].row_base);
-      quantize_store<D, BITS, SB16>(x, g, dv.rec + grow * RB, sr, dv.seed, step, (uint32_t)t, r);
-    }
-  }
-}
-
-template <int D, int BITS, bool SB16>
-__global__ __launch_bounds__(256) void k_update_ins(Dev dv, Work w, const uint32_t* __restrict__ sval,
-                                                    const float* __restrict__ grad, uint32_t step) {
-  constexpr int LPR = Geo<D>::LPR, CPL = Geo<D>::CPL;
-  constexpr int RB = Rec<D, BITS, SB16>::BYTES;
-  const int g = threadIdx.x & (LPR - 1);
-  const int64_t nI = (int64_t)w.ctr[kCInserts];
-  const int64_t ngroups = (int64_t)gridDim.x * blockDim.x / LPR;
-  for (int64_t it = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / LPR; it < nI; it += ngroups) {
-    const int64_t u = w.ins_list[it];
-    const int64_t grow = w.urow[u];
-    const int t = w.utab[u];
-    const int32_t dst = w.udest[u];
-    float gr[CPL], x[CPL];
-    merged_grad<D>(w, sval, grad, u, g, gr);
-    dequant_row<D, BITS, SB16>(dv.rec + grow * RB, g, x);
-    apply_optimizer<D>(dv, x, gr, grow, g);
-    store_frow<D>(dv.crow + (int64_t)dst * D, g, x);
-    if (g == 0) {
-      dv.tag[dst] = (int32_t)(grow - dv.desc[t].row_base);
-      if (dv.policy == 0) dv.ts[dst] = (int32_t)step;
+      // issue the row fetch and the Adagrad state before the gradient gather
+      if (act == kActHitStay) load_frow8(dv.crow + (int64_t)slot * D, g, x);
+      else dequant_row<D, BITS, SB16>(rec, g, x);
+      const float G_old = load_G(dv, grow);
+      merged_grad<D>(w, sval, grad, u, g, gr);
+      apply_optimizer<D>(dv, x, gr, grow, g, G_old);
+      if (act == kActHitStay) {
+        store_frow8(dv.crow + (int64_t)slot * D, g, x);
+      } else {
+        quantize_store<D, BITS, SB16>(x, g, rec, sr, dv.seed, step, (uint32_t)t, (uint32_t)(grow - td.row_base));
+      }
     }
   }
 }
@@ -482,11 +514,10 @@ hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int6
                                reinterpret_cast<uint32_t*>(w.ctr + kCScanTotal), s);
   if (e != hipSuccess) return e;
   k_chunks_total<<<1, 1, 0, s>>>(w.ctr);
-  if (d.total_slots > 0) k_policy<<<kGrid, 256, 0, s>>>(d, w, step);
   return dispatch_row(d.dim, d.bits, d.sb16, [&]<int D, int BITS, bool SB16>() -> hipError_t {
-    k_partials<D><<<kGrid, 256, 0, s>>>(w, sv, grad);
-    k_update_main<D, BITS, SB16><<<kGrid, 256, 0, s>>>(d, w, sv, grad, step);
-    k_update_ins<D, BITS, SB16><<<kGrid, 256, 0, s>>>(d, w, sv, grad, step);
+    k_partials<D><<<kGrid, 256, 0, s>>>(d, w, sv, grad);
+    if (d.total_slots > 0) k_policy<<<kGrid, 256, 0, s>>>(d, w, step);
+    k_update<D, BITS, SB16><<<kGrid, 256, 0, s>>>(d, w, sv, grad, step);
     return hipGetLastError();
   });
 }

@@ -39,7 +39,7 @@ struct Plan {
   size_t o_rec, o_crow, o_tag, o_ts, o_cnt, o_G, o_desc, o_keyb, o_stats, o_err, state_bytes;
   // workspace offsets
   size_t o_kA, o_vA, o_kB, o_vB, o_hist, o_part, o_flag, o_pre, o_uk, o_seg, o_setf, o_urow, o_utab, o_uslot,
-      o_uact, o_udest, o_nch, o_cbase, o_vslot, o_vrow, o_vtab, o_ins, o_partial, o_ctr, ws_bytes;
+      o_uact, o_udest, o_nch, o_cbase, o_uvrow, o_uvu, o_partial, o_ctr, ws_bytes;
   int64_t max_partials = 0;
 };
 
@@ -134,10 +134,8 @@ int plan_config(const emb_cache_config* c, Plan* p) {
   p->o_udest = take(4 * L);
   p->o_nch = take(4 * L);
   p->o_cbase = take(4 * (L + 1));
-  p->o_vslot = take(4 * L);
-  p->o_vrow = take(4 * L);
-  p->o_vtab = take(4 * L);
-  p->o_ins = take(4 * L);
+  p->o_uvrow = take(4 * L);
+  p->o_uvu = take(4 * L);
   p->max_partials = (int64_t)(L / (embc::kSumChunk / 2) + 2);
   p->o_partial = take((size_t)p->max_partials * c->dim * 4);
   p->o_ctr = take(8 * embc::kNCounters);
@@ -274,10 +272,8 @@ int emb_cache_create(const emb_cache_config* cfg, void* state, size_t state_byte
   w.udest = reinterpret_cast<int32_t*>(wb + p.o_udest);
   w.nch = reinterpret_cast<uint32_t*>(wb + p.o_nch);
   w.chunk_base = reinterpret_cast<uint32_t*>(wb + p.o_cbase);
-  w.vic_slot = reinterpret_cast<int32_t*>(wb + p.o_vslot);
-  w.vic_row = reinterpret_cast<int32_t*>(wb + p.o_vrow);
-  w.vic_tab = reinterpret_cast<int32_t*>(wb + p.o_vtab);
-  w.ins_list = reinterpret_cast<int32_t*>(wb + p.o_ins);
+  w.uvic_row = reinterpret_cast<int32_t*>(wb + p.o_uvrow);
+  w.uvic_u = reinterpret_cast<int32_t*>(wb + p.o_uvu);
   w.partial = reinterpret_cast<float*>(wb + p.o_partial);
   w.ctr = reinterpret_cast<unsigned long long*>(wb + p.o_ctr);
   w.max_indices = cfg->max_indices;
