@@ -5,10 +5,13 @@
 //   k_partials  chunk sums (64 lookups each) of the merged gradient of rows with > 64 lookups
 //   k_policy    per touched set, one wave (one lane per way): which missed rows enter the
 //               cache and which resident each of them displaces (decisions only)
-//   k_update    per unique row: merged gradient, fetch, optimizer, then the cache way (hit)
-//               or quantization into T (bypass); an inserted row first quantizes the
-//               resident it displaces into T -- updating it first if it was itself
-//               updated this step (LFU) -- then writes itself into the way
+//   k_hot_fold  per row with > 64 lookups, one workgroup: its chunk sums folded left to
+//               right through LDS; the result replaces the row's first chunk sum
+//   k_evict     per insert that displaces a resident: the resident's FP32 row (updated
+//               first if it was itself updated this step, LFU) is quantized into T
+//   k_update    per unique row: merged gradient, fetch, optimizer, then the cache way
+//               (hit or insert) or quantization into T (bypass); it runs after k_evict,
+//               so every displaced row has been read before an insert overwrites its way
 // The row kernels split tables over the XCDs (XcdSplit) so that each L2 serves one table.
 #include "embc_device.h"
 #include "embc_dispatch.h"
@@ -133,34 +136,58 @@ __device__ __forceinline__ void sum_occ(const uint32_t* __restrict__ sval, int64
   }
 }
 
-// Merged gradient of unique row u: its lookups directly (<= 64), else its chunk sums.
+// Merged gradient of unique row u: its lookups directly (<= 64), else the fold of its
+// chunk sums left by k_hot_fold in its first chunk slot.
 template <int D>
 __device__ __forceinline__ void merged_grad(const Work& w, const uint32_t* __restrict__ sval,
-                                            const float* __restrict__ grad, int64_t u, int g,
-                                            float (&acc)[8]) {
-  constexpr int CPL = 8, U = kUnroll;
-  const uint32_t nch = w.nch[u];
-  if (nch == 0) {
-    sum_occ<D>(sval, w.seg[u], w.seg[u + 1], grad, g, acc);
-    return;
-  }
-  const float* p = w.partial + (int64_t)w.chunk_base[u] * D;
-  load_frow8(p, g, acc);
-  uint32_t c = 1;
-  for (; c + U <= nch; c += U) {
-    float x[U][8];
-#pragma unroll
-    for (int q = 0; q < U; ++q) load_frow8(p + (int64_t)(c + q) * D, g, x[q]);
-#pragma unroll
-    for (int q = 0; q < U; ++q)
-#pragma unroll
-      for (int k = 0; k < CPL; ++k) acc[k] = acc[k] + x[q][k];
-  }
-  for (; c < nch; ++c) {
-    float x[8];
-    load_frow8(p + (int64_t)c * D, g, x);
-#pragma unroll
-    for (int k = 0; k < CPL; ++k) acc[k] = acc[k] + x[k];
+                                            const float* __restrict__ grad, int64_t u, int g, float (&acc)[8]) {
+  if (w.nch[u] == 0) sum_occ<D>(sval, w.seg[u], w.seg[u + 1], grad, g, acc);
+  else load_frow8(w.partial + (int64_t)w.chunk_base[u] * D, g, acc);
+}
+
+// Fold of the chunk sums of each row with > 64 lookups: acc = p0 + p1 + ... left to right,
+// per column.  A workgroup takes the hot rows among 256 consecutive unique rows and, for
+// each, stages up to R chunk sums at a time in LDS (all threads load), then one thread
+// per column folds them in order.
+template <int D>
+__global__ __launch_bounds__(256) void k_hot_fold(Work w) {
+  constexpr int R = 8192 / D < 256 ? 8192 / D : 256;  // chunk rows per LDS round (32 KiB)
+  __shared__ float4 stage[R * D / 4];
+  __shared__ int32_t hot[256];
+  __shared__ int n_hot;
+  const int64_t nU = (int64_t)w.ctr[kCUnique];
+  const int tid = threadIdx.x;
+  for (int64_t base = (int64_t)blockIdx.x * 256; base < nU; base += (int64_t)gridDim.x * 256) {
+    if (tid == 0) n_hot = 0;
+    __syncthreads();
+    const int64_t u = base + tid;
+    if (u < nU && w.nch[u] > 0) hot[atomicAdd(&n_hot, 1)] = (int32_t)u;
+    __syncthreads();
+    const int nh = n_hot;
+    for (int h = 0; h < nh; ++h) {
+      const int64_t hu = hot[h];
+      const int64_t c0 = w.chunk_base[hu];
+      const int64_t nch = w.nch[hu];
+      const float4* src = reinterpret_cast<const float4*>(w.partial + c0 * D);
+      float acc = 0.0f;
+      for (int64_t r0 = 0; r0 < nch; r0 += R) {
+        const int rn = (int)min<int64_t>(R, nch - r0);
+        for (int i = tid; i < rn * D / 4; i += 256) stage[i] = src[r0 * D / 4 + i];
+        __syncthreads();
+        if (tid < D) {
+          const float* st = reinterpret_cast<const float*>(stage);
+          int r = 0;
+          if (r0 == 0) {
+            acc = st[tid];
+            r = 1;
+          }
+          for (; r < rn; ++r) acc = acc + st[r * D + tid];
+        }
+        __syncthreads();
+      }
+      if (tid < D) w.partial[c0 * D + tid] = acc;
+    }
+    __syncthreads();
   }
 }
 
@@ -424,6 +451,45 @@ __global__ __launch_bounds__(256) void k_policy(Dev dv, Work w, uint32_t step) {
   if (lane == 0) ps.flush(dv.stats);
 }
 
+// ---- displaced residents -> T -----------------------------------------------------------------
+template <int D, int BITS, bool SB16>
+__global__ __launch_bounds__(256) void k_evict(Dev dv, Work w, const uint32_t* __restrict__ sval,
+                                               const float* __restrict__ grad, uint32_t step) {
+  constexpr int LPR = Geo<D>::LPR;
+  constexpr int GPB = 256 / LPR;
+  constexpr int RB = Rec<D, BITS, SB16>::BYTES;
+  const int g = threadIdx.x & (LPR - 1);
+  const int64_t nU = (int64_t)w.ctr[kCUnique];
+  const bool sr = dv.rounding != 0;
+  const XcdSplit xs(dv.T);
+  const int64_t gx = xs.unit * GPB + threadIdx.x / LPR, gstride = xs.units * GPB;
+  for (int seg = xs.xcd; seg < xs.segments(dv.T); seg += kXcds) {
+    const int t = seg / xs.parts;
+    int64_t tlo, thi, lo, hi;
+    table_rows(w, nU, t, tlo, thi);
+    part_range(tlo, thi, seg % xs.parts, xs.parts, lo, hi);
+    const TableDesc td = dv.desc[t];
+    for (int64_t u = lo + gx; u < hi; u += gstride) {
+      const int32_t act = w.uact[u];
+      const int32_t dst = w.udest[u];
+      const int32_t vrow = w.uvic_row[u];
+      const int32_t vu = w.uvic_u[u];
+      if (act != kActInsert || vrow < 0) continue;
+      const int64_t vgrow = td.row_base + vrow;
+      float xv[8];
+      load_frow8(dv.crow + (int64_t)dst * D, g, xv);
+      if (vu >= 0) {
+        // the displaced resident was updated this step (LFU): its new value goes to T
+        const float Gv = load_G(dv, vgrow);
+        float gv[8];
+        merged_grad<D>(w, sval, grad, vu, g, gv);
+        apply_optimizer<D>(dv, xv, gv, vgrow, g, Gv);
+      }
+      quantize_store<D, BITS, SB16>(xv, g, dv.rec + vgrow * RB, sr, dv.seed, step, (uint32_t)t, (uint32_t)vrow);
+    }
+  }
+}
+
 // ---- per unique row: optimizer and write-back ------------------------------------------------
 template <int D, int BITS, bool SB16>
 __global__ __launch_bounds__(256) void k_update(Dev dv, Work w, const uint32_t* __restrict__ sval,
@@ -443,49 +509,39 @@ __global__ __launch_bounds__(256) void k_update(Dev dv, Work w, const uint32_t* 
     part_range(tlo, thi, seg % xs.parts, xs.parts, lo, hi);
     const TableDesc td = dv.desc[t];
     for (int64_t u = lo + gx; u < hi; u += gstride) {
+      // every load that does not depend on another is issued before the first use
       const int32_t act = w.uact[u];
-      if (act == kActDone) continue;
       const int64_t grow = w.urow[u];
-      uint8_t* rec = dv.rec + grow * RB;
       const int32_t slot = w.uslot[u];
-      float gr[8], x[8];
-      if (act == kActInsert) {
-        const int32_t dst = w.udest[u];
-        const int32_t vrow = w.uvic_row[u];
-        if (vrow >= 0) {
-          // the displaced resident leaves the cache: its FP32 row goes to T (after its
-          // own update when it was also updated this step)
-          const int64_t vgrow = td.row_base + vrow;
-          float xv[8];
-          load_frow8(dv.crow + (int64_t)dst * D, g, xv);
-          const int32_t vu = w.uvic_u[u];
-          if (vu >= 0) {
-            const float Gv = load_G(dv, vgrow);
-            float gv[8];
-            merged_grad<D>(w, sval, grad, vu, g, gv);
-            apply_optimizer<D>(dv, xv, gv, vgrow, g, Gv);
-          }
-          quantize_store<D, BITS, SB16>(xv, g, dv.rec + vgrow * RB, sr, dv.seed, step, (uint32_t)t, (uint32_t)vrow);
-        }
-        dequant_row<D, BITS, SB16>(rec, g, x);
-        const float G_old = load_G(dv, grow);
-        merged_grad<D>(w, sval, grad, u, g, gr);
-        apply_optimizer<D>(dv, x, gr, grow, g, G_old);
+      const int32_t dst = w.udest[u];
+      const uint32_t nch = w.nch[u];
+      const uint32_t s0 = w.seg[u], s1 = w.seg[u + 1];
+      const uint32_t cb = w.chunk_base[u];
+      if (act == kActDone) continue;
+      uint8_t* rec = dv.rec + grow * RB;
+      float x[8], gr[8];
+      CodeWords<BITS> cw;
+      float sc = 0.0f, bi = 0.0f;
+      const bool hit = act == kActHitStay;
+      if (hit) {
+        load_frow8(dv.crow + (int64_t)slot * D, g, x);
+      } else {
+        cw = load_code_words<BITS>(rec, g);
+        load_sb<D, BITS, SB16>(rec, sc, bi);
+      }
+      const float G_old = load_G(dv, grow);
+      if (nch == 0) sum_occ<D>(sval, s0, s1, grad, g, gr);
+      else load_frow8(w.partial + (int64_t)cb * D, g, gr);
+      if (!hit) dequant8<BITS>(cw, sc, bi, x);
+      apply_optimizer<D>(dv, x, gr, grow, g, G_old);
+      if (hit) {
+        store_frow8(dv.crow + (int64_t)slot * D, g, x);
+      } else if (act == kActInsert) {
         store_frow8(dv.crow + (int64_t)dst * D, g, x);
         if (g == 0) {
           dv.tag[dst] = (int32_t)(grow - td.row_base);
           if (dv.policy == 0) dv.ts[dst] = (int32_t)step;
         }
-        continue;
-      }
-      // issue the row fetch and the Adagrad state before the gradient gather
-      if (act == kActHitStay) load_frow8(dv.crow + (int64_t)slot * D, g, x);
-      else dequant_row<D, BITS, SB16>(rec, g, x);
-      const float G_old = load_G(dv, grow);
-      merged_grad<D>(w, sval, grad, u, g, gr);
-      apply_optimizer<D>(dv, x, gr, grow, g, G_old);
-      if (act == kActHitStay) {
-        store_frow8(dv.crow + (int64_t)slot * D, g, x);
       } else {
         quantize_store<D, BITS, SB16>(x, g, rec, sr, dv.seed, step, (uint32_t)t, (uint32_t)(grow - td.row_base));
       }
@@ -516,7 +572,11 @@ hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int6
   k_chunks_total<<<1, 1, 0, s>>>(w.ctr);
   return dispatch_row(d.dim, d.bits, d.sb16, [&]<int D, int BITS, bool SB16>() -> hipError_t {
     k_partials<D><<<kGrid, 256, 0, s>>>(d, w, sv, grad);
-    if (d.total_slots > 0) k_policy<<<kGrid, 256, 0, s>>>(d, w, step);
+    k_hot_fold<D><<<kGrid, 256, 0, s>>>(w);
+    if (d.total_slots > 0) {
+      k_policy<<<kGrid, 256, 0, s>>>(d, w, step);
+      k_evict<D, BITS, SB16><<<kGrid, 256, 0, s>>>(d, w, sv, grad, step);
+    }
     k_update<D, BITS, SB16><<<kGrid, 256, 0, s>>>(d, w, sv, grad, step);
     return hipGetLastError();
   });

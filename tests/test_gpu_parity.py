@@ -88,6 +88,36 @@ def test_step_parity(torch, case):
         assert s["inserts"] + s["unique_hits"] > 0
 
 
+def _bags_of(rows, per_bag, rng):
+    rows = np.array(rows, dtype=np.int32)
+    rng.shuffle(rows)
+    B = (len(rows) + per_bag - 1) // per_bag
+    off = np.minimum(np.arange(B + 1) * per_bag, len(rows)).astype(np.int32)
+    return rows, off, B
+
+
+@pytest.mark.parametrize("dim", [16, 128])
+def test_lfu_hot_rows_displaced_after_update(torch, dim):
+    """LFU, one set of 2 ways holding rows 1 and 2.  Next step row 1 is hit 70 times
+    while rows 3 and 4 miss 100 and 90 times: row 3 displaces row 2 (not accessed),
+    row 4 displaces row 1 after row 1's own update; rows 1, 3, 4 have > 64 lookups,
+    so their merged gradients come from chunk sums."""
+    cfg = custom_cfg(rows=[64], cache_fraction=2 / 64, assoc=2, policy="lfu", optimizer="adagrad",
+                     rounding="stochastic", bits=4, sb_fp16=True, dim=dim, lr=0.05)
+    log(f"LFU hot-row hit eviction, dim={dim}")
+    o, g = make_pair(cfg, max_indices=1024)
+    assert o.n_sets == [1] and g.n_sets == [1]
+    rng = np.random.default_rng(dim)
+    for rows in ([1, 2], [1] * 70 + [3] * 100 + [4] * 90 + [5, 6, 7]):
+        idx, off, B = _bags_of(rows, 4, rng)
+        grad = (rng.standard_normal((B, 1, dim)) * 0.1).astype(np.float32)
+        step_both(o, g, cfg, {"indices": idx, "offsets": off, "batch": B, "grad": grad}, torch)
+        compare_state(o, g, cfg)
+    s = o.stats(0)
+    assert s["hit_evictions"] == 1 and s["inserts"] == 2 and s["evictions"] == 2
+    assert sorted(o.export_cache(0)["tag"].tolist()) == [3, 4]
+
+
 def test_kaggle_int8_full_size(torch):
     """26 Table-1 tables at full size: 12 steps, outputs every step, whole state at the end."""
     cfg = configs.get("kaggle_int8")
