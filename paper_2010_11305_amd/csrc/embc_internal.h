@@ -96,6 +96,9 @@ struct Work {
   int32_t* uvic_row;     // [L] insert: table-local row displaced from its way, -1 = empty way
   int32_t* uvic_u;       // [L] insert: unique index of that row if it was updated this step, else -1
   float* partial;        // [L/32 + 2][dim] chunk sums
+  int32_t* chunk_owner;  // [L/32 + 2] unique row of each chunk
+  int32_t* tab_first;    // [T+1] first unique row of each table (tab_first[T] = number of unique rows)
+  int32_t* fwd_src;      // [L] forward: cache slot of each lookup, -2-row for a miss, -1 if skipped
   unsigned long long* ctr;  // counters, see kC*
   int64_t max_indices;
   int64_t max_partials;
@@ -117,8 +120,8 @@ enum : int {
 hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int64_t n, hipStream_t s);
 hipError_t launch_reset_state(const Dev& d, hipStream_t s);
 hipError_t launch_init_uniform(const Dev& d, float lo, float hi, uint64_t init_seed, hipStream_t s);
-hipError_t launch_forward(const Dev& d, const int32_t* idx, int64_t L, const int32_t* off, int32_t B,
-                          float* out, hipStream_t s);
+hipError_t launch_forward(const Dev& d, const Work& w, const int32_t* idx, int64_t L, const int32_t* off,
+                          int32_t B, float* out, hipStream_t s);
 hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int64_t L, const int32_t* off,
                            int32_t B, const float* grad, uint64_t step, int key_bits, bool decay,
                            hipStream_t s);

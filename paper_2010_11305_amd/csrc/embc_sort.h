@@ -14,6 +14,11 @@ hipError_t scan_exclusive(const T* in, T* out, int64_t n, const unsigned long lo
 hipError_t sort_pairs(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32_t* vB, int64_t n, int passes, uint32_t* hist,
                       uint32_t* part, int* in_B, hipStream_t s);
 
+// Offsets must be non-decreasing and inside [0, L]; otherwise set the error flag and
+// ctr[kCBadOffsets].
+__global__ void k_check_offsets(Dev dv, const int32_t* __restrict__ off, int64_t nbags, int64_t L,
+                                unsigned long long* __restrict__ ctr);
+
 hipError_t launch_expand(const Dev& dv, const int32_t* idx, int64_t L, const int32_t* off, int32_t B, uint32_t* keys,
                          uint32_t* vals, unsigned long long* ctr, hipStream_t s);
 

@@ -2,6 +2,7 @@
 // pooled[b][t] = sum over the bag of fetch(T_t, C_t, i) (Sec. 3 fetch operator).
 #include "embc_device.h"
 #include "embc_dispatch.h"
+#include "embc_sort.h"
 
 namespace embc {
 
@@ -74,114 +75,136 @@ hipError_t launch_init_uniform(const Dev& d, float lo, float hi, uint64_t init_s
 }
 
 // ---- forward --------------------------------------------------------------------------
-// One group of LPR lanes per bag (64/LPR bags per wave at once); tables are split
-// over the XCDs (XcdSplit), and the groups of an XCD share the bags of its current
-// table.  For each chunk of up to LPR positions, lane j loads index j and probes its
-// set.  The rows are then fetched FU at a time -- all FU loads (FP32 cache row, or
-// codes and scale/bias) issued before any is used -- and summed left to right.  A
-// bag with no valid lookup gives +0.
-constexpr int kFwdUnroll = 4;
+// Two passes.  k_fwd_probe: one thread per lookup (tables split over the XCDs) checks
+// the row, probes its set, and writes a code: the cache slot (hit), -2-row (miss) or
+// -1 (skipped).  k_fwd_gather: one group of LPR
+// lanes per bag (64/LPR bags per wave), tables split over the XCDs; lane j reads the
+// code of position j of each chunk of LPR positions, the rows are fetched FU at a time
+// (all FU loads issued before any is used) and summed left to right.  A bag with no
+// valid lookup gives +0.
+constexpr int kFwdUnroll = 2;
+
+__global__ __launch_bounds__(256) void k_fwd_probe(Dev dv, const int32_t* __restrict__ idx, int64_t L,
+                                                   const int32_t* __restrict__ off, int32_t B,
+                                                   int32_t* __restrict__ src) {
+  const XcdSplit xs(dv.T);
+  const int64_t tid = xs.unit * blockDim.x + threadIdx.x, stride = xs.units * blockDim.x;
+  if (blockIdx.x == 0) {
+    // positions outside every bag are skipped
+    const int64_t first = min<int64_t>(max<int64_t>(off[0], 0), L);
+    const int64_t last = min<int64_t>(max<int64_t>(off[(int64_t)dv.T * B], first), L);
+    for (int64_t p = threadIdx.x; p < first; p += blockDim.x) src[p] = -1;
+    for (int64_t p = last + threadIdx.x; p < L; p += blockDim.x) src[p] = -1;
+  }
+  for (int seg = xs.xcd; seg < xs.segments(dv.T); seg += kXcds) {
+    const int t = seg / xs.parts;
+    const TableDesc td = dv.desc[t];
+    const int64_t a = min<int64_t>(max<int64_t>(off[(int64_t)t * B], 0), L);
+    const int64_t b = min<int64_t>(max<int64_t>(off[(int64_t)(t + 1) * B], a), L);
+    int64_t lo, hi;
+    part_range(a, b, seg % xs.parts, xs.parts, lo, hi);
+    uint32_t ok = 0, hit = 0, bad = 0;
+    for (int64_t p = lo + tid; p < hi; p += stride) {
+      const int32_t r = idx[p];
+      int32_t code = -1;
+      if (r >= 0 && (int64_t)r < td.N) {
+        const int32_t sl = probe_slot(dv, td, r);
+        code = sl >= 0 ? sl : -2 - r;
+        ++ok;
+        hit += sl >= 0;
+      } else {
+        ++bad;
+      }
+      src[p] = code;
+    }
+    // statistics of the segment: one atomic per wave and counter
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      ok += __shfl_xor(ok, o);
+      hit += __shfl_xor(hit, o);
+      bad += __shfl_xor(bad, o);
+    }
+    if ((threadIdx.x & 63) == 0) {
+      unsigned long long* st = dv.stats + (int64_t)t * kNStat;
+      if (ok) atomicAdd(st + kStLookups, (unsigned long long)ok);
+      if (hit) atomicAdd(st + kStHitLookups, (unsigned long long)hit);
+      if (bad) {
+        atomicAdd(st + kStInvalidFwd, (unsigned long long)bad);
+        atomicOr(dv.err, kErrIndex);
+      }
+    }
+  }
+}
 
 template <int D, int BITS, bool SB16>
-__global__ __launch_bounds__(256) void k_forward(Dev dv, const int32_t* __restrict__ idx, int64_t L,
-                                                 const int32_t* __restrict__ off, int32_t B, float* __restrict__ out) {
+__global__ __launch_bounds__(256) void k_fwd_gather(Dev dv, const int32_t* __restrict__ src, int64_t L,
+                                                    const int32_t* __restrict__ off, int32_t B,
+                                                    float* __restrict__ out) {
   constexpr int LPR = Geo<D>::LPR, FU = kFwdUnroll;
   constexpr int GPB = 256 / LPR;
   constexpr int RB = Rec<D, BITS, SB16>::BYTES;
   const int g = threadIdx.x & (LPR - 1);
   const XcdSplit xs(dv.T);
   const int64_t gx = xs.unit * GPB + threadIdx.x / LPR, gstride = xs.units * GPB;
-  int cur_t = -1;
-  uint32_t c_valid = 0, c_hit = 0, c_bad = 0;
-  auto flush = [&]() {
-#pragma unroll
-    for (int o = LPR / 2; o >= 1; o >>= 1) {
-      c_valid += __shfl_xor(c_valid, o, LPR);
-      c_hit += __shfl_xor(c_hit, o, LPR);
-      c_bad += __shfl_xor(c_bad, o, LPR);
-    }
-    if (g == 0 && cur_t >= 0) {
-      unsigned long long* st = dv.stats + (int64_t)cur_t * kNStat;
-      if (c_valid) atomicAdd(st + kStLookups, (unsigned long long)c_valid);
-      if (c_hit) atomicAdd(st + kStHitLookups, (unsigned long long)c_hit);
-      if (c_bad) {
-        atomicAdd(st + kStInvalidFwd, (unsigned long long)c_bad);
-        atomicOr(dv.err, kErrIndex);
-      }
-    }
-    c_valid = c_hit = c_bad = 0;
-  };
   for (int seg = xs.xcd; seg < xs.segments(dv.T); seg += kXcds) {
-   const int t = seg / xs.parts;
-   int64_t blo, bhi;
-   part_range(0, B, seg % xs.parts, xs.parts, blo, bhi);
-   if (t != cur_t) {
-     flush();
-     cur_t = t;
-   }
-   const TableDesc td = dv.desc[t];
-   for (int64_t b = blo + gx; b < bhi; b += gstride) {
-    const int64_t bag = (int64_t)t * B + b;
+    const int t = seg / xs.parts;
+    int64_t blo, bhi;
+    part_range(0, B, seg % xs.parts, xs.parts, blo, bhi);
+    const TableDesc td = dv.desc[t];
     const uint8_t* rec0 = dv.rec + td.row_base * RB;
-    int64_t p0 = off[bag], p1 = off[bag + 1];
-    p0 = p0 < 0 ? 0 : p0;
-    p1 = p1 > L ? L : p1;
-    float acc[8];
+    // codes outside this table's slots and rows are skipped (only malformed offsets produce them)
+    const int64_t slot_lo = td.slot_base, slot_hi = td.slot_base + td.n_sets * dv.assoc;
+    for (int64_t b = blo + gx; b < bhi; b += gstride) {
+      const int64_t bag = (int64_t)t * B + b;
+      int64_t p0 = off[bag], p1 = off[bag + 1];
+      p0 = p0 < 0 ? 0 : p0;
+      p1 = p1 > L ? L : p1;
+      float acc[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) acc[i] = 0.0f;
-    bool first = true;
-    for (int64_t pc = p0; pc < p1; pc += LPR) {
-      const int n = (int)min<int64_t>(LPR, p1 - pc);
-      int32_t r = 0, slot = -1, ok = 0;
-      if (g < n) {
-        r = idx[pc + g];
-        ok = (r >= 0 && (int64_t)r < td.N);
-        if (ok) {
-          slot = probe_slot(dv, td, r);
-          ++c_valid;
-          c_hit += slot >= 0;
-        } else {
-          ++c_bad;
-        }
-      }
-      for (int j = 0; j < n; j += FU) {
-        float raw[FU][8];
-        CodeWords<BITS> cw[FU];
-        float sq[FU], bq[FU];
-        int kind[FU];  // 0 skip, 1 cache row, 2 low-precision row
+      for (int i = 0; i < 8; ++i) acc[i] = 0.0f;
+      bool first = true;
+      for (int64_t pc = p0; pc < p1; pc += LPR) {
+        const int n = (int)min<int64_t>(LPR, p1 - pc);
+        const int32_t code = g < n ? src[pc + g] : -1;
+        for (int j = 0; j < n; j += FU) {
+          float raw[FU][8];
+          CodeWords<BITS> cw[FU];
+          float sq[FU], bq[FU];
+          int kind[FU];  // 0 skip, 1 cache row, 2 low-precision row
 #pragma unroll
-        for (int q = 0; q < FU; ++q) {
-          const int okq = __shfl(ok, j + q, LPR);
-          const int32_t rq = __shfl(r, j + q, LPR);
-          const int32_t sl = __shfl(slot, j + q, LPR);
-          kind[q] = (j + q < n && okq) ? (sl >= 0 ? 1 : 2) : 0;
-          if (kind[q] == 1) {
-            load_frow8(dv.crow + (int64_t)sl * D, g, raw[q]);
-          } else if (kind[q] == 2) {
-            const uint8_t* rec = rec0 + (int64_t)rq * RB;
-            cw[q] = load_code_words<BITS>(rec, g);
-            load_sb<D, BITS, SB16>(rec, sq[q], bq[q]);
+          for (int q = 0; q < FU; ++q) {
+            const int32_t cq = __shfl(code, j + q, LPR);
+            kind[q] = 0;
+            if (j + q < n) {
+              if (cq >= slot_lo && cq < slot_hi) kind[q] = 1;
+              else if (cq <= -2 && (int64_t)(-2 - cq) < td.N) kind[q] = 2;
+            }
+            if (kind[q] == 1) {
+              load_frow8(dv.crow + (int64_t)cq * D, g, raw[q]);
+            } else if (kind[q] == 2) {
+              const uint8_t* rec = rec0 + (int64_t)(-2 - cq) * RB;
+              cw[q] = load_code_words<BITS>(rec, g);
+              load_sb<D, BITS, SB16>(rec, sq[q], bq[q]);
+            }
           }
-        }
 #pragma unroll
-        for (int q = 0; q < FU; ++q) {
-          if (kind[q] == 0) continue;
-          if (kind[q] == 2) dequant8<BITS>(cw[q], sq[q], bq[q], raw[q]);
-          if (first) {
+          for (int q = 0; q < FU; ++q) {
+            if (kind[q] == 0) continue;
+            if (kind[q] == 2) dequant8<BITS>(cw[q], sq[q], bq[q], raw[q]);
+            if (first) {
 #pragma unroll
-            for (int i = 0; i < 8; ++i) acc[i] = raw[q][i];
-            first = false;
-          } else {
+              for (int i = 0; i < 8; ++i) acc[i] = raw[q][i];
+              first = false;
+            } else {
 #pragma unroll
-            for (int i = 0; i < 8; ++i) acc[i] = acc[i] + raw[q][i];
+              for (int i = 0; i < 8; ++i) acc[i] = acc[i] + raw[q][i];
+            }
           }
         }
       }
+      store_frow8(out + ((int64_t)b * dv.T + t) * D, g, acc);
     }
-    store_frow8(out + ((int64_t)b * dv.T + t) * D, g, acc);
-   }
   }
-  flush();
 }
 
 __global__ void k_zero_fwd_stats(Dev dv) {
@@ -192,18 +215,19 @@ __global__ void k_zero_fwd_stats(Dev dv) {
   }
 }
 
-hipError_t launch_forward(const Dev& d, const int32_t* idx, int64_t L, const int32_t* off, int32_t B, float* out,
-                          hipStream_t s) {
+hipError_t launch_forward(const Dev& d, const Work& w, const int32_t* idx, int64_t L, const int32_t* off, int32_t B,
+                          float* out, hipStream_t s) {
   k_zero_fwd_stats<<<1, 256, 0, s>>>(d);
   const int64_t nbags = (int64_t)d.T * B;
   if (nbags == 0) return hipGetLastError();
+  k_check_offsets<<<grid_for(nbags, 2048), 256, 0, s>>>(d, off, nbags, L, w.ctr);
+  if (L > 0) k_fwd_probe<<<2048, 256, 0, s>>>(d, idx, L, off, B, w.fwd_src);
   return dispatch_row(d.dim, d.bits, d.sb16, [&]<int D, int BITS, bool SB16>() -> hipError_t {
     // whole multiples of 8 workgroups (one per XCD), at most 8 per CU
     const int64_t wgs = (nbags * Geo<D>::LPR + 255) / 256;
     int64_t blocks = (wgs + 7) / 8 * 8;
     blocks = blocks < 8 ? 8 : (blocks > 2048 ? 2048 : blocks);
-    const unsigned grid = (unsigned)blocks;
-    k_forward<D, BITS, SB16><<<grid, 256, 0, s>>>(d, idx, L, off, B, out);
+    k_fwd_gather<D, BITS, SB16><<<(unsigned)blocks, 256, 0, s>>>(d, w.fwd_src, L, off, B, out);
     return hipGetLastError();
   });
 }

@@ -326,7 +326,6 @@ __global__ __launch_bounds__(256) void k_expand(Dev dv, const int32_t* __restric
   if (lane == 0 && n_bad) atomicAdd(&dv.stats[(int64_t)t_run * kNStat + kStInvalidBwd], (unsigned long long)n_bad);
 }
 
-// Offsets must be non-decreasing and inside [0, L]; otherwise flag the step.
 __global__ __launch_bounds__(256) void k_check_offsets(Dev dv, const int32_t* __restrict__ off, int64_t nbags,
                                                        int64_t L, unsigned long long* __restrict__ ctr) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;

@@ -22,7 +22,7 @@ namespace embc {
 constexpr int kGrid = 2048;      // blocks of the grid-stride kernels (8 per CU)
 constexpr int32_t kActDone = 4;  // row fully handled by k_policy
 
-constexpr int kUnroll = 4;  // independent row loads in flight per row group
+constexpr int kUnroll = 2;  // independent row loads in flight per row group
 
 // Per-table counts of the active lanes (tables may differ across lanes): one atomic
 // for the lanes sharing the first active lane's table, one per lane for the others.
@@ -192,19 +192,34 @@ __global__ __launch_bounds__(256) void k_hot_fold(Work w) {
 }
 
 // [lo, hi) of the unique rows of table t (rows are sorted table-major).
-__device__ __forceinline__ void table_rows(const Work& w, int64_t nU, int t, int64_t& lo, int64_t& hi) {
-  int64_t a = 0, b = nU;
-  while (a < b) {  // first u with utab[u] >= t
-    const int64_t m = (a + b) >> 1;
-    if (w.utab[m] < t) a = m + 1; else b = m;
+__device__ __forceinline__ void table_rows(const Work& w, int t, int64_t& lo, int64_t& hi) {
+  lo = w.tab_first[t];
+  hi = w.tab_first[t + 1];
+}
+
+// tab_first[t] = first unique row of table t (>= t), tab_first[T] = number of unique rows.
+__global__ void k_tab_first(Work w, int T) {
+  const int64_t nU = (int64_t)w.ctr[kCUnique];
+  for (int t = blockIdx.x * blockDim.x + threadIdx.x; t <= T; t += gridDim.x * blockDim.x) {
+    int64_t a = 0, b = nU;
+    while (a < b) {
+      const int64_t m = (a + b) >> 1;
+      if (w.utab[m] < t) a = m + 1; else b = m;
+    }
+    w.tab_first[t] = (int32_t)a;
   }
-  lo = a;
-  b = nU;
-  while (a < b) {  // first u with utab[u] > t
-    const int64_t m = (a + b) >> 1;
-    if (w.utab[m] <= t) a = m + 1; else b = m;
+}
+
+// chunk_owner[c] = the unique row whose chunk sums include chunk c.
+__global__ __launch_bounds__(256) void k_chunk_owner(Work w) {
+  const int64_t nU = (int64_t)w.ctr[kCUnique];
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < nU; u += stride) {
+    const uint32_t n = w.nch[u];
+    if (n == 0) continue;
+    const int64_t c0 = w.chunk_base[u];
+    for (uint32_t j = 0; j < n; ++j) w.chunk_owner[c0 + j] = (int32_t)u;
   }
-  hi = a;
 }
 
 template <int D>
@@ -221,19 +236,13 @@ __global__ __launch_bounds__(256) void k_partials(Dev dv, Work w, const uint32_t
   for (int seg = xs.xcd; seg < xs.segments(dv.T); seg += kXcds) {
     const int t = seg / xs.parts;
     int64_t ulo, uhi;
-    table_rows(w, nU, t, ulo, uhi);
+    table_rows(w, t, ulo, uhi);
     const int64_t clo_t = ulo < nU ? (int64_t)w.chunk_base[ulo] : nC;
     const int64_t chi_t = uhi < nU ? (int64_t)w.chunk_base[uhi] : nC;
     int64_t clo, chi;
     part_range(clo_t, chi_t, seg % xs.parts, xs.parts, clo, chi);
     for (int64_t c = clo + gx; c < chi; c += gstride) {
-      // unique row owning chunk c: the largest u in [ulo, uhi) with chunk_base[u] <= c
-      int64_t lo = ulo, hi = uhi;
-      while (hi - lo > 1) {
-        const int64_t mid = (lo + hi) >> 1;
-        if ((int64_t)w.chunk_base[mid] <= c) lo = mid; else hi = mid;
-      }
-      const int64_t u = lo;
+      const int64_t u = w.chunk_owner[c];
       const int64_t j = c - (int64_t)w.chunk_base[u];
       const int64_t i0 = (int64_t)w.seg[u] + j * kSumChunk;
       const int64_t i1 = min<int64_t>(i0 + kSumChunk, (int64_t)w.seg[u + 1]);
@@ -466,7 +475,7 @@ __global__ __launch_bounds__(256) void k_evict(Dev dv, Work w, const uint32_t* _
   for (int seg = xs.xcd; seg < xs.segments(dv.T); seg += kXcds) {
     const int t = seg / xs.parts;
     int64_t tlo, thi, lo, hi;
-    table_rows(w, nU, t, tlo, thi);
+    table_rows(w, t, tlo, thi);
     part_range(tlo, thi, seg % xs.parts, xs.parts, lo, hi);
     const TableDesc td = dv.desc[t];
     for (int64_t u = lo + gx; u < hi; u += gstride) {
@@ -505,7 +514,7 @@ __global__ __launch_bounds__(256) void k_update(Dev dv, Work w, const uint32_t* 
   for (int seg = xs.xcd; seg < xs.segments(dv.T); seg += kXcds) {
     const int t = seg / xs.parts;
     int64_t tlo, thi, lo, hi;
-    table_rows(w, nU, t, tlo, thi);
+    table_rows(w, t, tlo, thi);
     part_range(tlo, thi, seg % xs.parts, xs.parts, lo, hi);
     const TableDesc td = dv.desc[t];
     for (int64_t u = lo + gx; u < hi; u += gstride) {
@@ -566,10 +575,12 @@ hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int6
   e = launch_unique(d, sk, L, w.flag, w.pre, w.part, w.uniq_key, w.seg, w.set_first, w.ctr, s);
   if (e != hipSuccess) return e;
   k_probe<<<kGrid, 256, 0, s>>>(d, w, step);
+  k_tab_first<<<1, 256, 0, s>>>(w, d.T);
   e = scan_exclusive<uint32_t>(w.nch, w.chunk_base, L, w.ctr + kCUnique, reinterpret_cast<uint32_t*>(w.part),
                                reinterpret_cast<uint32_t*>(w.ctr + kCScanTotal), s);
   if (e != hipSuccess) return e;
   k_chunks_total<<<1, 1, 0, s>>>(w.ctr);
+  k_chunk_owner<<<kGrid, 256, 0, s>>>(w);
   return dispatch_row(d.dim, d.bits, d.sb16, [&]<int D, int BITS, bool SB16>() -> hipError_t {
     k_partials<D><<<kGrid, 256, 0, s>>>(d, w, sv, grad);
     k_hot_fold<D><<<kGrid, 256, 0, s>>>(w);

@@ -39,7 +39,7 @@ struct Plan {
   size_t o_rec, o_crow, o_tag, o_ts, o_cnt, o_G, o_desc, o_keyb, o_stats, o_err, state_bytes;
   // workspace offsets
   size_t o_kA, o_vA, o_kB, o_vB, o_hist, o_part, o_flag, o_pre, o_uk, o_seg, o_setf, o_urow, o_utab, o_uslot,
-      o_uact, o_udest, o_nch, o_cbase, o_uvrow, o_uvu, o_partial, o_ctr, ws_bytes;
+      o_uact, o_udest, o_nch, o_cbase, o_uvrow, o_uvu, o_partial, o_owner, o_tabf, o_src, o_ctr, ws_bytes;
   int64_t max_partials = 0;
 };
 
@@ -138,6 +138,9 @@ int plan_config(const emb_cache_config* c, Plan* p) {
   p->o_uvu = take(4 * L);
   p->max_partials = (int64_t)(L / (embc::kSumChunk / 2) + 2);
   p->o_partial = take((size_t)p->max_partials * c->dim * 4);
+  p->o_owner = take((size_t)p->max_partials * 4);
+  p->o_tabf = take(4 * (size_t)(T + 1));
+  p->o_src = take(4 * L);
   p->o_ctr = take(8 * embc::kNCounters);
   p->ws_bytes = o;
   return EMB_OK;
@@ -275,6 +278,9 @@ int emb_cache_create(const emb_cache_config* cfg, void* state, size_t state_byte
   w.uvic_row = reinterpret_cast<int32_t*>(wb + p.o_uvrow);
   w.uvic_u = reinterpret_cast<int32_t*>(wb + p.o_uvu);
   w.partial = reinterpret_cast<float*>(wb + p.o_partial);
+  w.chunk_owner = reinterpret_cast<int32_t*>(wb + p.o_owner);
+  w.tab_first = reinterpret_cast<int32_t*>(wb + p.o_tabf);
+  w.fwd_src = reinterpret_cast<int32_t*>(wb + p.o_src);
   w.ctr = reinterpret_cast<unsigned long long*>(wb + p.o_ctr);
   w.max_indices = cfg->max_indices;
   w.max_partials = p.max_partials;
@@ -311,7 +317,7 @@ int emb_cache_forward(emb_cache_t h, const int32_t* indices, int64_t num_indices
   if (!h || batch < 0 || batch > h->cfg.max_batch || num_indices < 0 || num_indices > h->cfg.max_indices)
     return EMB_EINVAL;
   if ((num_indices > 0 && !indices) || !offsets || (batch > 0 && !out)) return EMB_EINVAL;
-  return hip_status(embc::launch_forward(h->dev, indices, num_indices, offsets, batch, out, S(stream)));
+  return hip_status(embc::launch_forward(h->dev, h->work, indices, num_indices, offsets, batch, out, S(stream)));
 }
 
 int emb_cache_backward_update(emb_cache_t h, const int32_t* indices, int64_t num_indices, const int32_t* offsets,

@@ -161,6 +161,8 @@ def test_malformed_offsets_skip_the_step(torch):
     idx = torch.tensor([1, 2, 3, 4, 5], dtype=torch.int32, device="cuda")
     off = torch.tensor([0, 3, 2, 5, 5], dtype=torch.int32, device="cuda")   # decreasing
     grad = torch.ones((4, 1, 16), dtype=torch.float32, device="cuda")
+    g.forward(idx, off, 4)          # results unspecified, but no fault and the flag is set
+    assert g.check() == EMB_EINDEX
     g.backward_update(idx, off, 4, grad)
     assert g.check() == EMB_EINDEX
     after = g.export_rows(0)
