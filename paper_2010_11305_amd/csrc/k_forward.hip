@@ -75,8 +75,8 @@ hipError_t launch_init_uniform(const Dev& d, float lo, float hi, uint64_t init_s
 }
 
 // ---- forward --------------------------------------------------------------------------
-// Two passes.  k_fwd_probe: one thread per lookup (tables split over the XCDs) checks
-// the row, probes its set, and writes a code: the cache slot (hit), -2-row (miss) or
+// Two passes.  k_fwd_probe: up to 4 lanes per lookup (tables split over the XCDs) check
+// the row, probe its set, and write a code: the cache slot (hit), -2-row (miss) or
 // -1 (skipped).  k_fwd_gather: one group of LPR
 // lanes per bag (64/LPR bags per wave), tables split over the XCDs; lane j reads the
 // code of position j of each chunk of LPR positions, the rows are fetched FU at a time
@@ -96,6 +96,12 @@ __global__ __launch_bounds__(256) void k_fwd_probe(Dev dv, const int32_t* __rest
     for (int64_t p = threadIdx.x; p < first; p += blockDim.x) src[p] = -1;
     for (int64_t p = last + threadIdx.x; p < L; p += blockDim.x) src[p] = -1;
   }
+  // QL lanes share one lookup, each comparing W = assoc/QL of the set's tags, so a
+  // wave-wide tag load touches 64/QL sets instead of 64
+  const int A = dv.assoc;
+  const int QL = A < 4 ? A : 4, W = A / QL;
+  const int sub = threadIdx.x % QL;
+  const int64_t ptid = tid / QL, pstride = stride / QL;
   for (int seg = xs.xcd; seg < xs.segments(dv.T); seg += kXcds) {
     const int t = seg / xs.parts;
     const TableDesc td = dv.desc[t];
@@ -104,18 +110,33 @@ __global__ __launch_bounds__(256) void k_fwd_probe(Dev dv, const int32_t* __rest
     int64_t lo, hi;
     part_range(a, b, seg % xs.parts, xs.parts, lo, hi);
     uint32_t ok = 0, hit = 0, bad = 0;
-    for (int64_t p = lo + tid; p < hi; p += stride) {
+    for (int64_t p = lo + ptid; p < hi; p += pstride) {
       const int32_t r = idx[p];
-      int32_t code = -1;
-      if (r >= 0 && (int64_t)r < td.N) {
-        const int32_t sl = probe_slot(dv, td, r);
-        code = sl >= 0 ? sl : -2 - r;
-        ++ok;
-        hit += sl >= 0;
-      } else {
-        ++bad;
+      const bool valid = r >= 0 && (int64_t)r < td.N;
+      int32_t found = -1;
+      if (valid && td.n_sets > 0) {
+        const int64_t base = td.slot_base + (int64_t)((uint32_t)r % (uint32_t)td.n_sets) * A + sub * W;
+        const int32_t* tg = dv.tag + base;
+        if ((W & 3) == 0) {
+          for (int k = 0; k < W; k += 4) {
+            const int4 v = *reinterpret_cast<const int4*>(tg + k);
+            if (v.x == r) found = (int32_t)(base + k);
+            if (v.y == r) found = (int32_t)(base + k + 1);
+            if (v.z == r) found = (int32_t)(base + k + 2);
+            if (v.w == r) found = (int32_t)(base + k + 3);
+          }
+        } else {
+          for (int k = 0; k < W; ++k)
+            if (tg[k] == r) found = (int32_t)(base + k);
+        }
       }
-      src[p] = code;
+      for (int o = 1; o < QL; o <<= 1) found = max(found, __shfl_xor(found, o, QL));
+      if (sub == 0) {
+        src[p] = valid ? (found >= 0 ? found : -2 - r) : -1;
+        ok += valid;
+        hit += found >= 0;
+        bad += !valid;
+      }
     }
     // statistics of the segment: one atomic per wave and counter
 #pragma unroll
