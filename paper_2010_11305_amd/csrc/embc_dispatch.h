@@ -27,6 +27,12 @@ hipError_t dispatch_row(int dim, int bits, int sb16, Fn&& fn) {
 #undef EMBC_DISPATCH_DIM
 }
 
+// Blocks of a grid-stride kernel: as many as are resident at once on the current
+// device (occupancy x compute units, for `threads` per block and no dynamic LDS),
+// rounded down to a multiple of the 8 XCDs.  The whole grid then runs in one round;
+// a larger grid would leave its last blocks running alone after the others end.
+unsigned resident_grid(const void* kernel, int threads = 256);
+
 inline unsigned grid_for(int64_t threads, int64_t cap = 8192) {
   int64_t b = (threads + 255) / 256;
   if (b < 1) b = 1;

@@ -242,12 +242,13 @@ hipError_t launch_forward(const Dev& d, const Work& w, const int32_t* idx, int64
   const int64_t nbags = (int64_t)d.T * B;
   if (nbags == 0) return hipGetLastError();
   k_check_offsets<<<grid_for(nbags, 2048), 256, 0, s>>>(d, off, nbags, L, w.ctr);
-  if (L > 0) k_fwd_probe<<<2048, 256, 0, s>>>(d, idx, L, off, B, w.fwd_src);
+  if (L > 0) k_fwd_probe<<<resident_grid(reinterpret_cast<const void*>(k_fwd_probe)), 256, 0, s>>>(d, idx, L, off, B, w.fwd_src);
   return dispatch_row(d.dim, d.bits, d.sb16, [&]<int D, int BITS, bool SB16>() -> hipError_t {
-    // whole multiples of 8 workgroups (one per XCD), at most 8 per CU
+    // whole multiples of 8 workgroups (one per XCD), at most the resident count
     const int64_t wgs = (nbags * Geo<D>::LPR + 255) / 256;
+    const int64_t cap = resident_grid(reinterpret_cast<const void*>(k_fwd_gather<D, BITS, SB16>));
     int64_t blocks = (wgs + 7) / 8 * 8;
-    blocks = blocks < 8 ? 8 : (blocks > 2048 ? 2048 : blocks);
+    blocks = blocks < 8 ? 8 : (blocks > cap ? cap : blocks);
     k_fwd_gather<D, BITS, SB16><<<(unsigned)blocks, 256, 0, s>>>(d, w.fwd_src, L, off, B, out);
     return hipGetLastError();
   });

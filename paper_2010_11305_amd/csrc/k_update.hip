@@ -19,7 +19,6 @@
 
 namespace embc {
 
-constexpr int kGrid = 2048;      // blocks of the grid-stride kernels (8 per CU)
 constexpr int32_t kActDone = 4;  // row fully handled by k_policy
 
 constexpr int kUnroll = 2;  // independent row loads in flight per row group
@@ -103,35 +102,80 @@ __global__ __launch_bounds__(256) void k_probe(Dev dv, Work w, uint32_t step) {
 // Left-to-right FP32 sum of the gradient rows of occurrences [i0, i1) of the sorted
 // stream (i0 < i1), seeded with the first.  Lane j of the group preloads the row
 // index of occurrence j of each chunk of LPR occurrences; U rows are loaded before
-// they are added in order.
-template <int D>
+// they are added in order.  A row listed more than once in one bag has adjacent
+// occurrences with the same gradient row: with REUSE the repeat adds the row already
+// in registers instead of loading it again (same operands, same sums).  Repeats are
+// frequent only among rows with many lookups, so only their chunk sums use it.
+template <int D, bool REUSE>
 __device__ __forceinline__ void sum_occ(const uint32_t* __restrict__ sval, int64_t i0, int64_t i1,
                                         const float* __restrict__ grad, int g, float (&acc)[8]) {
   constexpr int LPR = Geo<D>::LPR, CPL = 8, U = kUnroll;
   bool first = true;
-  for (int64_t ic = i0; ic < i1; ic += LPR) {
-    const int n = (int)min<int64_t>(LPR, i1 - ic);
-    const uint32_t myv = g < n ? sval[ic + g] : 0u;
-    int j = 0;
-    if (first) {
-      load_frow8(grad + (int64_t)__shfl(myv, 0, LPR) * D, g, acc);
-      first = false;
-      j = 1;
+  if constexpr (!REUSE) {
+    for (int64_t ic = i0; ic < i1; ic += LPR) {
+      const int n = (int)min<int64_t>(LPR, i1 - ic);
+      const uint32_t myv = g < n ? sval[ic + g] : 0u;
+      int j = 0;
+      if (first) {
+        load_frow8(grad + (int64_t)__shfl(myv, 0, LPR) * D, g, acc);
+        first = false;
+        j = 1;
+      }
+      for (; j + U <= n; j += U) {
+        float x[U][CPL];
+#pragma unroll
+        for (int q = 0; q < U; ++q) load_frow8(grad + (int64_t)__shfl(myv, j + q, LPR) * D, g, x[q]);
+#pragma unroll
+        for (int q = 0; q < U; ++q)
+#pragma unroll
+          for (int k = 0; k < CPL; ++k) acc[k] = acc[k] + x[q][k];
+      }
+      for (; j < n; ++j) {
+        float x[CPL];
+        load_frow8(grad + (int64_t)__shfl(myv, j, LPR) * D, g, x);
+#pragma unroll
+        for (int k = 0; k < CPL; ++k) acc[k] = acc[k] + x[k];
+      }
     }
-    for (; j + U <= n; j += U) {
-      float x[U][8];
+  } else {
+    uint32_t pv = 0xFFFFFFFFu;  // gradient row of the last occurrence added (none yet)
+    float last[CPL];
 #pragma unroll
-      for (int q = 0; q < U; ++q) load_frow8(grad + (int64_t)__shfl(myv, j + q, LPR) * D, g, x[q]);
+    for (int k = 0; k < CPL; ++k) last[k] = 0.0f;
+    for (int64_t ic = i0; ic < i1; ic += LPR) {
+      const int n = (int)min<int64_t>(LPR, i1 - ic);
+      const uint32_t myv = g < n ? sval[ic + g] : 0u;
+      for (int j = 0; j < n; j += U) {
+        uint32_t v[U];
+        bool fresh[U];
+        float x[U][CPL];
 #pragma unroll
-      for (int q = 0; q < U; ++q)
+        for (int q = 0; q < U; ++q) {
+          v[q] = __shfl(myv, j + q, LPR);
+          fresh[q] = j + q < n && v[q] != (q == 0 ? pv : v[q - 1]);
+          if (fresh[q]) load_frow8(grad + (int64_t)v[q] * D, g, x[q]);
+        }
 #pragma unroll
-        for (int k = 0; k < CPL; ++k) acc[k] = acc[k] + x[q][k];
-    }
-    for (; j < n; ++j) {
-      float x[8];
-      load_frow8(grad + (int64_t)__shfl(myv, j, LPR) * D, g, x);
+        for (int q = 0; q < U; ++q) {
+          if (j + q < n) {
+            if (!fresh[q]) {
 #pragma unroll
-      for (int k = 0; k < CPL; ++k) acc[k] = acc[k] + x[k];
+              for (int k = 0; k < CPL; ++k) x[q][k] = last[k];
+            }
+            if (first) {
+#pragma unroll
+              for (int k = 0; k < CPL; ++k) acc[k] = x[q][k];
+              first = false;
+            } else {
+#pragma unroll
+              for (int k = 0; k < CPL; ++k) acc[k] = acc[k] + x[q][k];
+            }
+#pragma unroll
+            for (int k = 0; k < CPL; ++k) last[k] = x[q][k];
+            pv = v[q];
+          }
+        }
+      }
     }
   }
 }
@@ -141,7 +185,7 @@ __device__ __forceinline__ void sum_occ(const uint32_t* __restrict__ sval, int64
 template <int D>
 __device__ __forceinline__ void merged_grad(const Work& w, const uint32_t* __restrict__ sval,
                                             const float* __restrict__ grad, int64_t u, int g, float (&acc)[8]) {
-  if (w.nch[u] == 0) sum_occ<D>(sval, w.seg[u], w.seg[u + 1], grad, g, acc);
+  if (w.nch[u] == 0) sum_occ<D, false>(sval, w.seg[u], w.seg[u + 1], grad, g, acc);
   else load_frow8(w.partial + (int64_t)w.chunk_base[u] * D, g, acc);
 }
 
@@ -247,7 +291,7 @@ __global__ __launch_bounds__(256) void k_partials(Dev dv, Work w, const uint32_t
       const int64_t i0 = (int64_t)w.seg[u] + j * kSumChunk;
       const int64_t i1 = min<int64_t>(i0 + kSumChunk, (int64_t)w.seg[u + 1]);
       float acc[8];
-      sum_occ<D>(sval, i0, i1, grad, g, acc);
+      sum_occ<D, true>(sval, i0, i1, grad, g, acc);
       store_frow8(w.partial + c * D, g, acc);
     }
   }
@@ -539,7 +583,7 @@ __global__ __launch_bounds__(256) void k_update(Dev dv, Work w, const uint32_t* 
         load_sb<D, BITS, SB16>(rec, sc, bi);
       }
       const float G_old = load_G(dv, grow);
-      if (nch == 0) sum_occ<D>(sval, s0, s1, grad, g, gr);
+      if (nch == 0) sum_occ<D, false>(sval, s0, s1, grad, g, gr);
       else load_frow8(w.partial + (int64_t)cb * D, g, gr);
       if (!hit) dequant8<BITS>(cw, sc, bi, x);
       apply_optimizer<D>(dv, x, gr, grow, g, G_old);
@@ -574,21 +618,22 @@ hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int6
   const uint32_t* sv = in_B ? w.valsB : w.valsA;
   e = launch_unique(d, sk, L, w.flag, w.pre, w.part, w.uniq_key, w.seg, w.set_first, w.ctr, s);
   if (e != hipSuccess) return e;
-  k_probe<<<kGrid, 256, 0, s>>>(d, w, step);
+  const auto grid = [](auto kernel) { return resident_grid(reinterpret_cast<const void*>(kernel)); };
+  k_probe<<<grid(k_probe), 256, 0, s>>>(d, w, step);
   k_tab_first<<<1, 256, 0, s>>>(w, d.T);
   e = scan_exclusive<uint32_t>(w.nch, w.chunk_base, L, w.ctr + kCUnique, reinterpret_cast<uint32_t*>(w.part),
                                reinterpret_cast<uint32_t*>(w.ctr + kCScanTotal), s);
   if (e != hipSuccess) return e;
   k_chunks_total<<<1, 1, 0, s>>>(w.ctr);
-  k_chunk_owner<<<kGrid, 256, 0, s>>>(w);
+  k_chunk_owner<<<grid(k_chunk_owner), 256, 0, s>>>(w);
   return dispatch_row(d.dim, d.bits, d.sb16, [&]<int D, int BITS, bool SB16>() -> hipError_t {
-    k_partials<D><<<kGrid, 256, 0, s>>>(d, w, sv, grad);
-    k_hot_fold<D><<<kGrid, 256, 0, s>>>(w);
+    k_partials<D><<<grid(k_partials<D>), 256, 0, s>>>(d, w, sv, grad);
+    k_hot_fold<D><<<grid(k_hot_fold<D>), 256, 0, s>>>(w);
     if (d.total_slots > 0) {
-      k_policy<<<kGrid, 256, 0, s>>>(d, w, step);
-      k_evict<D, BITS, SB16><<<kGrid, 256, 0, s>>>(d, w, sv, grad, step);
+      k_policy<<<grid(k_policy), 256, 0, s>>>(d, w, step);
+      k_evict<D, BITS, SB16><<<grid(k_evict<D, BITS, SB16>), 256, 0, s>>>(d, w, sv, grad, step);
     }
-    k_update<D, BITS, SB16><<<kGrid, 256, 0, s>>>(d, w, sv, grad, step);
+    k_update<D, BITS, SB16><<<grid(k_update<D, BITS, SB16>), 256, 0, s>>>(d, w, sv, grad, step);
     return hipGetLastError();
   });
 }

@@ -7,13 +7,40 @@
 
 #include <cmath>
 #include <cstring>
+#include <map>
+#include <mutex>
 #include <new>
+#include <utility>
 #include <vector>
 
 #include "emb_cache.h"
+#include "embc_dispatch.h"
 #include "embc_internal.h"
 
 using embc::TableDesc;
+
+namespace embc {
+
+unsigned resident_grid(const void* kernel, int threads) {
+  static std::mutex mu;
+  static std::map<std::pair<const void*, int>, unsigned> known;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) dev = 0;
+  std::lock_guard<std::mutex> lock(mu);
+  const auto key = std::make_pair(kernel, dev);
+  const auto it = known.find(key);
+  if (it != known.end()) return it->second;
+  int per_cu = 0, cus = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess || per_cu < 1)
+    per_cu = 1;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1) cus = 8;
+  unsigned n = (unsigned)per_cu * (unsigned)cus / 8u * 8u;
+  if (n < 8) n = 8;
+  known[key] = n;
+  return n;
+}
+
+}  // namespace embc
 
 namespace {
 
