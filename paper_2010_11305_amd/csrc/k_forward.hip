@@ -84,9 +84,16 @@ hipError_t launch_init_uniform(const Dev& d, float lo, float hi, uint64_t init_s
 // valid lookup gives +0.
 constexpr int kFwdUnroll = 2;
 
+constexpr int kProbeUnroll = 4;  // lookups in flight per lane group of the probe
+
+// QL = min(assoc, 4) lanes share one lookup, each comparing W = assoc/QL of the set's
+// tags, so a wave-wide tag load touches 64/QL sets instead of 64; every lane group
+// keeps kProbeUnroll lookups in flight (all index loads, then all tag loads).
+template <int W>
 __global__ __launch_bounds__(256) void k_fwd_probe(Dev dv, const int32_t* __restrict__ idx, int64_t L,
                                                    const int32_t* __restrict__ off, int32_t B,
                                                    int32_t* __restrict__ src) {
+  constexpr int PU = kProbeUnroll;
   const XcdSplit xs(dv.T);
   const int64_t tid = xs.unit * blockDim.x + threadIdx.x, stride = xs.units * blockDim.x;
   if (blockIdx.x == 0) {
@@ -96,10 +103,8 @@ __global__ __launch_bounds__(256) void k_fwd_probe(Dev dv, const int32_t* __rest
     for (int64_t p = threadIdx.x; p < first; p += blockDim.x) src[p] = -1;
     for (int64_t p = last + threadIdx.x; p < L; p += blockDim.x) src[p] = -1;
   }
-  // QL lanes share one lookup, each comparing W = assoc/QL of the set's tags, so a
-  // wave-wide tag load touches 64/QL sets instead of 64
   const int A = dv.assoc;
-  const int QL = A < 4 ? A : 4, W = A / QL;
+  const int QL = A / W;  // 1, 2 or 4
   const int sub = threadIdx.x % QL;
   const int64_t ptid = tid / QL, pstride = stride / QL;
   for (int seg = xs.xcd; seg < xs.segments(dv.T); seg += kXcds) {
@@ -109,33 +114,51 @@ __global__ __launch_bounds__(256) void k_fwd_probe(Dev dv, const int32_t* __rest
     const int64_t b = min<int64_t>(max<int64_t>(off[(int64_t)(t + 1) * B], a), L);
     int64_t lo, hi;
     part_range(a, b, seg % xs.parts, xs.parts, lo, hi);
+    const int32_t* tags = dv.tag + td.slot_base + sub * W;
     uint32_t ok = 0, hit = 0, bad = 0;
-    for (int64_t p = lo + ptid; p < hi; p += pstride) {
-      const int32_t r = idx[p];
-      const bool valid = r >= 0 && (int64_t)r < td.N;
-      int32_t found = -1;
-      if (valid && td.n_sets > 0) {
-        const int64_t base = td.slot_base + (int64_t)((uint32_t)r % (uint32_t)td.n_sets) * A + sub * W;
-        const int32_t* tg = dv.tag + base;
-        if ((W & 3) == 0) {
-          for (int k = 0; k < W; k += 4) {
-            const int4 v = *reinterpret_cast<const int4*>(tg + k);
-            if (v.x == r) found = (int32_t)(base + k);
-            if (v.y == r) found = (int32_t)(base + k + 1);
-            if (v.z == r) found = (int32_t)(base + k + 2);
-            if (v.w == r) found = (int32_t)(base + k + 3);
+    for (int64_t p0 = lo + ptid; p0 < hi; p0 += pstride * PU) {
+      int32_t r[PU], found[PU];
+      bool valid[PU];
+#pragma unroll
+      for (int q = 0; q < PU; ++q) {
+        const int64_t p = p0 + q * pstride;
+        r[q] = p < hi ? idx[p] : -1;
+      }
+#pragma unroll
+      for (int q = 0; q < PU; ++q) {
+        valid[q] = r[q] >= 0 && (int64_t)r[q] < td.N;
+        found[q] = -1;
+        if (valid[q] && td.n_sets > 0) {
+          const int64_t set = (int64_t)((uint32_t)r[q] % (uint32_t)td.n_sets);
+          const int32_t* tg = tags + set * A;
+          int32_t tw[W];
+          if constexpr (W % 4 == 0) {
+#pragma unroll
+            for (int k = 0; k < W; k += 4) {
+              const int4 v = *reinterpret_cast<const int4*>(tg + k);
+              tw[k] = v.x; tw[k + 1] = v.y; tw[k + 2] = v.z; tw[k + 3] = v.w;
+            }
+          } else if constexpr (W == 2) {
+            const int2 v = *reinterpret_cast<const int2*>(tg);
+            tw[0] = v.x; tw[1] = v.y;
+          } else {
+            tw[0] = tg[0];
           }
-        } else {
+#pragma unroll
           for (int k = 0; k < W; ++k)
-            if (tg[k] == r) found = (int32_t)(base + k);
+            if (tw[k] == r[q]) found[q] = (int32_t)(td.slot_base + set * A + sub * W + k);
         }
       }
-      for (int o = 1; o < QL; o <<= 1) found = max(found, __shfl_xor(found, o, QL));
-      if (sub == 0) {
-        src[p] = valid ? (found >= 0 ? found : -2 - r) : -1;
-        ok += valid;
-        hit += found >= 0;
-        bad += !valid;
+#pragma unroll
+      for (int q = 0; q < PU; ++q) {
+        for (int o = 1; o < QL; o <<= 1) found[q] = max(found[q], __shfl_xor(found[q], o, QL));
+        const int64_t p = p0 + q * pstride;
+        if (sub == 0 && p < hi) {
+          src[p] = valid[q] ? (found[q] >= 0 ? found[q] : -2 - r[q]) : -1;
+          ok += valid[q];
+          hit += found[q] >= 0;
+          bad += !valid[q];
+        }
       }
     }
     // statistics of the segment: one atomic per wave and counter
@@ -242,7 +265,19 @@ hipError_t launch_forward(const Dev& d, const Work& w, const int32_t* idx, int64
   const int64_t nbags = (int64_t)d.T * B;
   if (nbags == 0) return hipGetLastError();
   k_check_offsets<<<grid_for(nbags, 2048), 256, 0, s>>>(d, off, nbags, L, w.ctr);
-  if (L > 0) k_fwd_probe<<<resident_grid(reinterpret_cast<const void*>(k_fwd_probe)), 256, 0, s>>>(d, idx, L, off, B, w.fwd_src);
+  if (L > 0) {
+    const auto probe = [&](auto kernel) {
+      kernel<<<resident_grid(reinterpret_cast<const void*>(kernel)), 256, 0, s>>>(d, idx, L, off, B, w.fwd_src);
+    };
+    switch (d.assoc <= 4 ? 1 : d.assoc / 4) {
+      case 1: probe(k_fwd_probe<1>); break;
+      case 2: probe(k_fwd_probe<2>); break;
+      case 4: probe(k_fwd_probe<4>); break;
+      case 8: probe(k_fwd_probe<8>); break;
+      case 16: probe(k_fwd_probe<16>); break;
+      default: return hipErrorInvalidValue;
+    }
+  }
   return dispatch_row(d.dim, d.bits, d.sb16, [&]<int D, int BITS, bool SB16>() -> hipError_t {
     // whole multiples of 8 workgroups (one per XCD), at most the resident count
     const int64_t wgs = (nbags * Geo<D>::LPR + 255) / 256;
