@@ -22,6 +22,7 @@ namespace embc {
 
 constexpr uint32_t kKeyInvalid = 0xFFFFFFFFu;  // sort key of a skipped lookup (sorts last)
 constexpr int kSumChunk = 64;                  // occurrences per chunk of a merged-gradient sum
+constexpr uint32_t kFoldDirect = 8;            // chunk sums a row's consumer folds itself (more: k_hot_fold)
 constexpr int kMaxAssoc = 64;
 
 enum : int32_t { kActHitStay = 0, kActHitEvict = 1, kActInsert = 2, kActBypass = 3 };
@@ -81,8 +82,8 @@ struct Work {
   uint32_t* valsB;
   uint32_t* hist;        // radix histograms [256][nblocks]
   unsigned long long* part;  // scan partials
-  unsigned long long* flag;  // packed (set-start << 32 | row-start) flags
-  unsigned long long* pre;   // their exclusive prefix sums
+  unsigned long long* tile_cnt;  // unique rows and touched sets per tile of sorted keys, packed (sets << 32 | rows)
+  unsigned long long* tile_pre;  // their exclusive prefix sums
   uint32_t* uniq_key;    // [L]
   uint32_t* seg;         // [L+1] start of each unique row's occurrences in the sorted stream
   uint32_t* set_first;   // [L+1] first unique row of each touched set
@@ -97,6 +98,7 @@ struct Work {
   int32_t* uvic_u;       // [L] insert: unique index of that row if it was updated this step, else -1
   float* partial;        // [L/32 + 2][dim] chunk sums
   int32_t* chunk_owner;  // [L/32 + 2] unique row of each chunk
+  int32_t* long_rows;    // [L/(64*kFoldDirect) + 1] unique rows with more than kFoldDirect chunk sums
   int32_t* tab_first;    // [T+1] first unique row of each table (tab_first[T] = number of unique rows)
   int32_t* fwd_src;      // [L] forward: cache slot of each lookup, -2-row for a miss, -1 if skipped
   unsigned long long* ctr;  // counters, see kC*
@@ -113,6 +115,7 @@ enum : int {
   kCInserts = 5,
   kCScanTotal = 6,  // scratch total of the last scan
   kCBadOffsets = 7, // offsets of this step failed validation
+  kCLongRows = 8,   // rows whose chunk sums are folded by k_hot_fold
   kNCounters = 16
 };
 
@@ -128,5 +131,6 @@ hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int6
 
 size_t radix_hist_words(int64_t n);
 size_t scan_partial_words(int64_t n);
+size_t uniq_tile_words(int64_t n);
 
 }  // namespace embc

@@ -3,9 +3,8 @@
 //
 //   k_expand       lookups -> (set-major row key, gradient-row index), position order
 //   radix passes   stable LSD radix sort, 8-bit digits, wave-ballot ranking
-//   k_row_flags    first occurrence of each row / of each cache set in the sorted stream
 //   scans          3-phase exclusive prefix sums (u32 / u64)
-//   k_compact      unique-row and touched-set lists
+//   k_uniq_*       unique-row and touched-set lists (first occurrence of each row / set)
 #include "embc_device.h"
 #include "embc_dispatch.h"
 #include "embc_sort.h"
@@ -351,42 +350,122 @@ hipError_t launch_expand(const Dev& dv, const int32_t* idx, int64_t L, const int
 }
 
 // ---- unique rows and touched sets ---------------------------------------------------------
-// flag[i] = (first of its cache set) << 32 | (first of its row); invalid keys get 0.
-__global__ __launch_bounds__(256) void k_row_flags(Dev dv, const uint32_t* __restrict__ sk, int64_t n,
-                                                   unsigned long long* __restrict__ flag,
-                                                   unsigned long long* __restrict__ ctr) {
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
-    const uint32_t k = sk[i];
-    const uint32_t prev = i ? sk[i - 1] : kKeyInvalid;
-    unsigned long long f = 0;
-    if (k == kKeyInvalid) {
-      if (i == 0 || prev != kKeyInvalid) ctr[kCValid] = (unsigned long long)i;
-    } else if (i == 0 || prev != k) {
-      f = 1;
-      const int t = table_of_key(dv.key_base, dv.T, k);
-      const TableDesc td = dv.desc[t];
-      if (td.n_sets > 0) {
-        bool new_set = (i == 0);
-        if (!new_set) {
-          const int tp = table_of_key(dv.key_base, dv.T, prev);
-          new_set = tp != t || ((int64_t)prev - td.key_base) / td.Q != ((int64_t)k - td.key_base) / td.Q;
-        }
-        if (new_set) f |= 1ull << 32;
-      }
+// A row start is a valid key that differs from its predecessor in the sorted stream; a
+// set start is a row start of a cached table whose (table, set) differs from the
+// predecessor's.  Two passes over tiles of kUqTile keys (kUqPer consecutive keys per
+// thread): k_uniq_count writes each tile's counts packed as (sets << 32 | rows); after
+// their exclusive scan, k_uniq_write writes every start at its tile's offset plus its
+// rank inside the tile: the key and first occurrence of each unique row, and the first
+// unique row of each touched set.
+constexpr int kUqPer = 16;
+constexpr int kUqTile = 256 * kUqPer;
+
+size_t uniq_tile_words(int64_t n) { return (size_t)((n + kUqTile - 1) / kUqTile + 1); }
+
+// Table of the keys seen by one thread, with the key range and set stride of that table.
+struct TabCursor {
+  int t = -1;
+  int64_t kb = 0, kb_next = 0, Q = 1;
+  bool cached = false;
+  __device__ void load(const Dev& dv) {
+    kb = dv.key_base[t];
+    kb_next = dv.key_base[t + 1];
+    const TableDesc& td = dv.desc[t];
+    Q = td.Q;
+    cached = td.n_sets > 0;
+  }
+  // position on the table of a valid key (keys only increase after the first call)
+  __device__ void seek(const Dev& dv, uint32_t key) {
+    if (t < 0) {
+      t = table_of_key(dv.key_base, dv.T, key);
+      load(dv);
     }
-    flag[i] = f;
+    while ((int64_t)key >= kb_next) {
+      ++t;
+      load(dv);
+    }
+  }
+  __device__ uint32_t set_of(uint32_t key) const { return (uint32_t)((int64_t)key - kb) / (uint32_t)Q; }
+};
+
+// Walks the thread's keys; calls on_start(i, key, is_set_start) for every row start.
+// Returns the index of the first invalid key if it lies in the thread's range, else -1.
+template <typename F>
+__device__ __forceinline__ int64_t walk_starts(const Dev& dv, const uint32_t* __restrict__ sk, int64_t n,
+                                               int64_t i0, const uint32_t (&k)[kUqPer], F&& on_start) {
+  uint32_t prev = i0 > 0 ? sk[i0 - 1] : kKeyInvalid;
+  TabCursor cur;
+  int pt = -1;        // table of prev (valid prev only)
+  uint32_t pset = 0;  // set of prev (cached table only)
+  if (prev != kKeyInvalid) {
+    cur.seek(dv, prev);
+    pt = cur.t;
+    if (cur.cached) pset = cur.set_of(prev);
+  }
+  int64_t first_invalid = -1;
+#pragma unroll
+  for (int j = 0; j < kUqPer; ++j) {
+    const int64_t i = i0 + j;
+    if (i < n) {
+      const uint32_t key = k[j];
+      if (key == kKeyInvalid) {
+        if (prev != kKeyInvalid || i == 0) first_invalid = i;
+      } else if (i == 0 || key != prev) {
+        cur.seek(dv, key);
+        bool new_set = false;
+        if (cur.cached) {
+          const uint32_t st = cur.set_of(key);
+          new_set = pt != cur.t || st != pset || i == 0;
+          pset = st;
+        }
+        pt = cur.t;
+        on_start(i, key, new_set);
+      }
+      prev = key;
+    }
+  }
+  return first_invalid;
+}
+
+__device__ __forceinline__ void load_tile_keys(const uint32_t* __restrict__ sk, int64_t n, int64_t i0,
+                                               uint32_t (&k)[kUqPer]) {
+  if (i0 + kUqPer <= n) {
+    const uint4* p = reinterpret_cast<const uint4*>(sk + i0);
+#pragma unroll
+    for (int j = 0; j < kUqPer / 4; ++j) {
+      const uint4 v = p[j];
+      k[4 * j] = v.x; k[4 * j + 1] = v.y; k[4 * j + 2] = v.z; k[4 * j + 3] = v.w;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < kUqPer; ++j) k[j] = i0 + j < n ? sk[i0 + j] : kKeyInvalid;
   }
 }
 
-__global__ __launch_bounds__(256) void k_compact(const uint32_t* __restrict__ sk, int64_t n,
-                                                 const unsigned long long* __restrict__ flag,
-                                                 const unsigned long long* __restrict__ pre, uint32_t* __restrict__ uk,
-                                                 uint32_t* __restrict__ seg, uint32_t* __restrict__ set_first,
-                                                 unsigned long long* __restrict__ ctr) {
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (tid == 0) {
+__global__ __launch_bounds__(256) void k_uniq_count(Dev dv, const uint32_t* __restrict__ sk, int64_t n,
+                                                    unsigned long long* __restrict__ tile_cnt,
+                                                    unsigned long long* __restrict__ ctr) {
+  __shared__ unsigned long long lds4[4];
+  const int64_t i0 = (int64_t)blockIdx.x * kUqTile + (int64_t)threadIdx.x * kUqPer;
+  uint32_t k[kUqPer];
+  load_tile_keys(sk, n, i0, k);
+  unsigned long long c = 0;
+  const int64_t fi = walk_starts(dv, sk, n, i0, k, [&](int64_t, uint32_t, bool ns) {
+    c += 1ull + (ns ? (1ull << 32) : 0ull);
+  });
+  if (fi >= 0) ctr[kCValid] = (unsigned long long)fi;
+  unsigned long long tot;
+  block_exclusive_scan<unsigned long long>(c, lds4, tot);
+  if (threadIdx.x == 0) tile_cnt[blockIdx.x] = tot;
+}
+
+__global__ __launch_bounds__(256) void k_uniq_write(Dev dv, const uint32_t* __restrict__ sk, int64_t n,
+                                                    const unsigned long long* __restrict__ tile_pre,
+                                                    uint32_t* __restrict__ uk, uint32_t* __restrict__ seg,
+                                                    uint32_t* __restrict__ set_first,
+                                                    unsigned long long* __restrict__ ctr) {
+  __shared__ unsigned long long lds4[4];
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
     const unsigned long long tot = ctr[kCScanTotal];
     const uint32_t nu = (uint32_t)(tot & 0xFFFFFFFFull), ns = (uint32_t)(tot >> 32);
     ctr[kCUnique] = nu;
@@ -394,26 +473,30 @@ __global__ __launch_bounds__(256) void k_compact(const uint32_t* __restrict__ sk
     seg[nu] = (uint32_t)ctr[kCValid];
     set_first[ns] = nu;
   }
-  for (int64_t i = tid; i < n; i += stride) {
-    const unsigned long long f = flag[i];
-    if (f & 1ull) {
-      const unsigned long long p = pre[i];
-      const uint32_t u = (uint32_t)(p & 0xFFFFFFFFull);
-      uk[u] = sk[i];
-      seg[u] = (uint32_t)i;
-      if (f >> 32) set_first[(uint32_t)(p >> 32)] = u;
-    }
-  }
+  const int64_t i0 = (int64_t)blockIdx.x * kUqTile + (int64_t)threadIdx.x * kUqPer;
+  uint32_t k[kUqPer];
+  load_tile_keys(sk, n, i0, k);
+  unsigned long long c = 0;
+  walk_starts(dv, sk, n, i0, k, [&](int64_t, uint32_t, bool ns) { c += 1ull + (ns ? (1ull << 32) : 0ull); });
+  unsigned long long tot;
+  const unsigned long long base = block_exclusive_scan<unsigned long long>(c, lds4, tot) + tile_pre[blockIdx.x];
+  uint32_t u = (uint32_t)(base & 0xFFFFFFFFull), st = (uint32_t)(base >> 32);
+  walk_starts(dv, sk, n, i0, k, [&](int64_t i, uint32_t key, bool ns) {
+    uk[u] = key;
+    seg[u] = (uint32_t)i;
+    if (ns) set_first[st++] = u;
+    ++u;
+  });
 }
 
-hipError_t launch_unique(const Dev& dv, const uint32_t* sk, int64_t n, unsigned long long* flag,
-                         unsigned long long* pre, unsigned long long* part, uint32_t* uk, uint32_t* seg,
+hipError_t launch_unique(const Dev& dv, const uint32_t* sk, int64_t n, unsigned long long* tile_cnt,
+                         unsigned long long* tile_pre, unsigned long long* part, uint32_t* uk, uint32_t* seg,
                          uint32_t* set_first, unsigned long long* ctr, hipStream_t s) {
-  const unsigned grid = grid_for(n, 4096);
-  k_row_flags<<<grid, 256, 0, s>>>(dv, sk, n, flag, ctr);
-  hipError_t e = scan_exclusive<unsigned long long>(flag, pre, n, nullptr, part, ctr + kCScanTotal, s);
+  const int64_t tiles = (n + kUqTile - 1) / kUqTile;
+  if (tiles > 0) k_uniq_count<<<(unsigned)tiles, 256, 0, s>>>(dv, sk, n, tile_cnt, ctr);
+  hipError_t e = scan_exclusive<unsigned long long>(tile_cnt, tile_pre, tiles, nullptr, part, ctr + kCScanTotal, s);
   if (e != hipSuccess) return e;
-  k_compact<<<grid, 256, 0, s>>>(sk, n, flag, pre, uk, seg, set_first, ctr);
+  k_uniq_write<<<(unsigned)(tiles > 0 ? tiles : 1), 256, 0, s>>>(dv, sk, n, tile_pre, uk, seg, set_first, ctr);
   return hipGetLastError();
 }
 

@@ -5,8 +5,9 @@
 //   k_partials  chunk sums (64 lookups each) of the merged gradient of rows with > 64 lookups
 //   k_policy    per touched set, one wave (one lane per way): which missed rows enter the
 //               cache and which resident each of them displaces (decisions only)
-//   k_hot_fold  per row with > 64 lookups, one workgroup: its chunk sums folded left to
-//               right through LDS; the result replaces the row's first chunk sum
+//   k_hot_fold  per row with > kFoldDirect chunk sums, one workgroup: its chunk sums folded
+//               left to right through LDS; the result replaces the row's first chunk sum
+//               (rows with fewer chunks are folded by the kernel that consumes them)
 //   k_evict     per insert that displaces a resident: the resident's FP32 row (updated
 //               first if it was itself updated this step, LFU) is quantized into T
 //   k_update    per unique row: merged gradient, fetch, optimizer, then the cache way
@@ -180,58 +181,90 @@ __device__ __forceinline__ void sum_occ(const uint32_t* __restrict__ sval, int64
   }
 }
 
-// Merged gradient of unique row u: its lookups directly (<= 64), else the fold of its
-// chunk sums left by k_hot_fold in its first chunk slot.
+// Left-to-right fold of the n >= 1 chunk sums of one row, rows c0 .. c0+n-1 of
+// `partial` (acc = p0, then acc + p1, ...), U rows loaded before they are added.
+template <int D>
+__device__ __forceinline__ void fold_chunks(const float* __restrict__ partial, int64_t c0, uint32_t n, int g,
+                                            float (&acc)[8]) {
+  constexpr int U = kUnroll;
+  load_frow8(partial + c0 * D, g, acc);
+  uint32_t j = 1;
+  for (; j + U <= n; j += U) {
+    float x[U][8];
+#pragma unroll
+    for (int q = 0; q < U; ++q) load_frow8(partial + (c0 + j + q) * D, g, x[q]);
+#pragma unroll
+    for (int q = 0; q < U; ++q)
+#pragma unroll
+      for (int k = 0; k < 8; ++k) acc[k] = acc[k] + x[q][k];
+  }
+  for (; j < n; ++j) {
+    float x[8];
+    load_frow8(partial + (c0 + j) * D, g, x);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) acc[k] = acc[k] + x[k];
+  }
+}
+
+// Merged gradient of unique row u from its lookups (<= 64), its chunk sums (<=
+// kFoldDirect of them) or the fold of its chunk sums left by k_hot_fold in its
+// first chunk slot.
 template <int D>
 __device__ __forceinline__ void merged_grad(const Work& w, const uint32_t* __restrict__ sval,
                                             const float* __restrict__ grad, int64_t u, int g, float (&acc)[8]) {
-  if (w.nch[u] == 0) sum_occ<D, false>(sval, w.seg[u], w.seg[u + 1], grad, g, acc);
+  const uint32_t n = w.nch[u];
+  if (n == 0) sum_occ<D, false>(sval, w.seg[u], w.seg[u + 1], grad, g, acc);
+  else if (n <= kFoldDirect) fold_chunks<D>(w.partial, w.chunk_base[u], n, g, acc);
   else load_frow8(w.partial + (int64_t)w.chunk_base[u] * D, g, acc);
 }
 
-// Fold of the chunk sums of each row with > 64 lookups: acc = p0 + p1 + ... left to right,
-// per column.  A workgroup takes the hot rows among 256 consecutive unique rows and, for
-// each, stages up to R chunk sums at a time in LDS (all threads load), then one thread
-// per column folds them in order.
+// Fold of the chunk sums of each row with more than kFoldDirect of them: acc = p0 +
+// p1 + ... left to right, per column, into the row's first chunk slot.  One workgroup
+// per row (from the list k_chunk_owner builds): all threads stage R chunk sums in LDS,
+// load the next R into registers, and one thread per column folds the staged ones.
 template <int D>
 __global__ __launch_bounds__(256) void k_hot_fold(Work w) {
   constexpr int R = 8192 / D < 256 ? 8192 / D : 256;  // chunk rows per LDS round (32 KiB)
+  constexpr int PER = R * D / 4 / 256;                 // float4 per thread and round
   __shared__ float4 stage[R * D / 4];
-  __shared__ int32_t hot[256];
-  __shared__ int n_hot;
-  const int64_t nU = (int64_t)w.ctr[kCUnique];
+  const int64_t nl = (int64_t)w.ctr[kCLongRows];
   const int tid = threadIdx.x;
-  for (int64_t base = (int64_t)blockIdx.x * 256; base < nU; base += (int64_t)gridDim.x * 256) {
-    if (tid == 0) n_hot = 0;
-    __syncthreads();
-    const int64_t u = base + tid;
-    if (u < nU && w.nch[u] > 0) hot[atomicAdd(&n_hot, 1)] = (int32_t)u;
-    __syncthreads();
-    const int nh = n_hot;
-    for (int h = 0; h < nh; ++h) {
-      const int64_t hu = hot[h];
-      const int64_t c0 = w.chunk_base[hu];
-      const int64_t nch = w.nch[hu];
-      const float4* src = reinterpret_cast<const float4*>(w.partial + c0 * D);
-      float acc = 0.0f;
-      for (int64_t r0 = 0; r0 < nch; r0 += R) {
-        const int rn = (int)min<int64_t>(R, nch - r0);
-        for (int i = tid; i < rn * D / 4; i += 256) stage[i] = src[r0 * D / 4 + i];
-        __syncthreads();
-        if (tid < D) {
-          const float* st = reinterpret_cast<const float*>(stage);
-          int r = 0;
-          if (r0 == 0) {
-            acc = st[tid];
-            r = 1;
-          }
-          for (; r < rn; ++r) acc = acc + st[r * D + tid];
-        }
-        __syncthreads();
-      }
-      if (tid < D) w.partial[c0 * D + tid] = acc;
+  for (int64_t h = blockIdx.x; h < nl; h += gridDim.x) {
+    const int64_t u = w.long_rows[h];
+    const int64_t c0 = w.chunk_base[u];
+    const int64_t nch = w.nch[u];
+    const float4* src = reinterpret_cast<const float4*>(w.partial + c0 * D);
+    const int64_t n4 = nch * (D / 4);
+    float4 nxt[PER];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int64_t i = tid + k * 256;
+      if (i < n4) nxt[k] = src[i];
     }
-    __syncthreads();
+    float acc = 0.0f;
+    for (int64_t r0 = 0; r0 < nch; r0 += R) {
+      const int rn = (int)min<int64_t>(R, nch - r0);
+      __syncthreads();  // the previous round's fold is done with `stage`
+#pragma unroll
+      for (int k = 0; k < PER; ++k)
+        if (tid + k * 256 < rn * (D / 4)) stage[tid + k * 256] = nxt[k];
+      __syncthreads();
+#pragma unroll
+      for (int k = 0; k < PER; ++k) {
+        const int64_t i = (r0 + R) * (D / 4) + tid + k * 256;
+        if (i < n4) nxt[k] = src[i];
+      }
+      if (tid < D) {
+        const float* st = reinterpret_cast<const float*>(stage);
+        int r = 0;
+        if (r0 == 0) {
+          acc = st[tid];
+          r = 1;
+        }
+        for (; r < rn; ++r) acc = acc + st[r * D + tid];
+      }
+    }
+    if (tid < D) w.partial[c0 * D + tid] = acc;
   }
 }
 
@@ -254,7 +287,8 @@ __global__ void k_tab_first(Work w, int T) {
   }
 }
 
-// chunk_owner[c] = the unique row whose chunk sums include chunk c.
+// chunk_owner[c] = the unique row whose chunk sums include chunk c; rows with more
+// than kFoldDirect chunks are listed for k_hot_fold (in any order).
 __global__ __launch_bounds__(256) void k_chunk_owner(Work w) {
   const int64_t nU = (int64_t)w.ctr[kCUnique];
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -263,6 +297,7 @@ __global__ __launch_bounds__(256) void k_chunk_owner(Work w) {
     if (n == 0) continue;
     const int64_t c0 = w.chunk_base[u];
     for (uint32_t j = 0; j < n; ++j) w.chunk_owner[c0 + j] = (int32_t)u;
+    if (n > kFoldDirect) w.long_rows[atomicAdd(&w.ctr[kCLongRows], 1ull)] = (int32_t)u;
   }
 }
 
@@ -584,6 +619,7 @@ __global__ __launch_bounds__(256) void k_update(Dev dv, Work w, const uint32_t* 
       }
       const float G_old = load_G(dv, grow);
       if (nch == 0) sum_occ<D, false>(sval, s0, s1, grad, g, gr);
+      else if (nch <= kFoldDirect) fold_chunks<D>(w.partial, cb, nch, g, gr);
       else load_frow8(w.partial + (int64_t)cb * D, g, gr);
       if (!hit) dequant8<BITS>(cw, sc, bi, x);
       apply_optimizer<D>(dv, x, gr, grow, g, G_old);
@@ -616,7 +652,7 @@ hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int6
   if (e != hipSuccess) return e;
   const uint32_t* sk = in_B ? w.keysB : w.keysA;
   const uint32_t* sv = in_B ? w.valsB : w.valsA;
-  e = launch_unique(d, sk, L, w.flag, w.pre, w.part, w.uniq_key, w.seg, w.set_first, w.ctr, s);
+  e = launch_unique(d, sk, L, w.tile_cnt, w.tile_pre, w.part, w.uniq_key, w.seg, w.set_first, w.ctr, s);
   if (e != hipSuccess) return e;
   const auto grid = [](auto kernel) { return resident_grid(reinterpret_cast<const void*>(kernel)); };
   k_probe<<<grid(k_probe), 256, 0, s>>>(d, w, step);

@@ -65,8 +65,8 @@ struct Plan {
   // state offsets
   size_t o_rec, o_crow, o_tag, o_ts, o_cnt, o_G, o_desc, o_keyb, o_stats, o_err, state_bytes;
   // workspace offsets
-  size_t o_kA, o_vA, o_kB, o_vB, o_hist, o_part, o_flag, o_pre, o_uk, o_seg, o_setf, o_urow, o_utab, o_uslot,
-      o_uact, o_udest, o_nch, o_cbase, o_uvrow, o_uvu, o_partial, o_owner, o_tabf, o_src, o_ctr, ws_bytes;
+  size_t o_kA, o_vA, o_kB, o_vB, o_hist, o_part, o_tcnt, o_tpre, o_uk, o_seg, o_setf, o_urow, o_utab, o_uslot,
+      o_uact, o_udest, o_nch, o_cbase, o_uvrow, o_uvu, o_partial, o_owner, o_long, o_tabf, o_src, o_ctr, ws_bytes;
   int64_t max_partials = 0;
 };
 
@@ -149,8 +149,8 @@ int plan_config(const emb_cache_config* c, Plan* p) {
   p->o_vB = take(4 * L);
   p->o_hist = take(4 * embc::radix_hist_words((int64_t)L));
   p->o_part = take(8 * embc::scan_partial_words((int64_t)L + 256 * 64));
-  p->o_flag = take(8 * L);
-  p->o_pre = take(8 * L);
+  p->o_tcnt = take(8 * embc::uniq_tile_words((int64_t)L));
+  p->o_tpre = take(8 * embc::uniq_tile_words((int64_t)L));
   p->o_uk = take(4 * L);
   p->o_seg = take(4 * (L + 1));
   p->o_setf = take(4 * (L + 1));
@@ -166,6 +166,7 @@ int plan_config(const emb_cache_config* c, Plan* p) {
   p->max_partials = (int64_t)(L / (embc::kSumChunk / 2) + 2);
   p->o_partial = take((size_t)p->max_partials * c->dim * 4);
   p->o_owner = take((size_t)p->max_partials * 4);
+  p->o_long = take(4 * (L / ((size_t)embc::kSumChunk * embc::kFoldDirect) + 1));
   p->o_tabf = take(4 * (size_t)(T + 1));
   p->o_src = take(4 * L);
   p->o_ctr = take(8 * embc::kNCounters);
@@ -290,8 +291,8 @@ int emb_cache_create(const emb_cache_config* cfg, void* state, size_t state_byte
   w.valsB = reinterpret_cast<uint32_t*>(wb + p.o_vB);
   w.hist = reinterpret_cast<uint32_t*>(wb + p.o_hist);
   w.part = reinterpret_cast<unsigned long long*>(wb + p.o_part);
-  w.flag = reinterpret_cast<unsigned long long*>(wb + p.o_flag);
-  w.pre = reinterpret_cast<unsigned long long*>(wb + p.o_pre);
+  w.tile_cnt = reinterpret_cast<unsigned long long*>(wb + p.o_tcnt);
+  w.tile_pre = reinterpret_cast<unsigned long long*>(wb + p.o_tpre);
   w.uniq_key = reinterpret_cast<uint32_t*>(wb + p.o_uk);
   w.seg = reinterpret_cast<uint32_t*>(wb + p.o_seg);
   w.set_first = reinterpret_cast<uint32_t*>(wb + p.o_setf);
@@ -305,6 +306,7 @@ int emb_cache_create(const emb_cache_config* cfg, void* state, size_t state_byte
   w.uvic_row = reinterpret_cast<int32_t*>(wb + p.o_uvrow);
   w.uvic_u = reinterpret_cast<int32_t*>(wb + p.o_uvu);
   w.partial = reinterpret_cast<float*>(wb + p.o_partial);
+  w.long_rows = reinterpret_cast<int32_t*>(wb + p.o_long);
   w.chunk_owner = reinterpret_cast<int32_t*>(wb + p.o_owner);
   w.tab_first = reinterpret_cast<int32_t*>(wb + p.o_tabf);
   w.fwd_src = reinterpret_cast<int32_t*>(wb + p.o_src);
