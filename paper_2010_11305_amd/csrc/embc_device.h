@@ -59,18 +59,37 @@ __device__ __forceinline__ void uniforms8(uint64_t seed, uint32_t step, uint32_t
 
 __device__ __forceinline__ float f16_round(float x) { return __half2float(__float2half(x)); }
 
+// Scale and bias words of a record, loaded raw so that a caller can issue further loads
+// before it converts them (decode_sb).
+template <bool SB16>
+struct SbWords {
+  uint32_t w[SB16 ? 1 : 2];
+};
+
+template <int D, int BITS, bool SB16>
+__device__ __forceinline__ SbWords<SB16> load_sb_words(const uint8_t* rec) {
+  constexpr int CB = Rec<D, BITS, SB16>::CODE_BYTES;
+  SbWords<SB16> r;
+  const uint32_t* p = reinterpret_cast<const uint32_t*>(rec + CB);
+  r.w[0] = p[0];
+  if constexpr (!SB16) r.w[1] = p[1];
+  return r;
+}
+
+template <bool SB16>
+__device__ __forceinline__ void decode_sb(const SbWords<SB16>& r, float& s, float& b) {
+  if constexpr (SB16) {
+    s = __half2float(__ushort_as_half((unsigned short)(r.w[0] & 0xFFFFu)));
+    b = __half2float(__ushort_as_half((unsigned short)(r.w[0] >> 16)));
+  } else {
+    s = __uint_as_float(r.w[0]);
+    b = __uint_as_float(r.w[1]);
+  }
+}
+
 template <int D, int BITS, bool SB16>
 __device__ __forceinline__ void load_sb(const uint8_t* rec, float& s, float& b) {
-  constexpr int CB = Rec<D, BITS, SB16>::CODE_BYTES;
-  if constexpr (SB16) {
-    const uint32_t w = *reinterpret_cast<const uint32_t*>(rec + CB);
-    s = __half2float(__ushort_as_half((unsigned short)(w & 0xFFFFu)));
-    b = __half2float(__ushort_as_half((unsigned short)(w >> 16)));
-  } else {
-    const float* p = reinterpret_cast<const float*>(rec + CB);
-    s = p[0];
-    b = p[1];
-  }
+  decode_sb<SB16>(load_sb_words<D, BITS, SB16>(rec), s, b);
 }
 
 // Raw code words of lane g: INT4 one dword (8 nibbles, column 8g+i in nibble i),

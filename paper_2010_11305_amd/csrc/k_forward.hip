@@ -213,7 +213,7 @@ __global__ __launch_bounds__(256) void k_fwd_gather(Dev dv, const int32_t* __res
         for (int j = 0; j < n; j += FU) {
           float raw[FU][8];
           CodeWords<BITS> cw[FU];
-          float sq[FU], bq[FU];
+          SbWords<SB16> sbw[FU];
           int kind[FU];  // 0 skip, 1 cache row, 2 low-precision row
 #pragma unroll
           for (int q = 0; q < FU; ++q) {
@@ -228,13 +228,17 @@ __global__ __launch_bounds__(256) void k_fwd_gather(Dev dv, const int32_t* __res
             } else if (kind[q] == 2) {
               const uint8_t* rec = rec0 + (int64_t)(-2 - cq) * RB;
               cw[q] = load_code_words<BITS>(rec, g);
-              load_sb<D, BITS, SB16>(rec, sq[q], bq[q]);
+              sbw[q] = load_sb_words<D, BITS, SB16>(rec);
             }
           }
 #pragma unroll
           for (int q = 0; q < FU; ++q) {
             if (kind[q] == 0) continue;
-            if (kind[q] == 2) dequant8<BITS>(cw[q], sq[q], bq[q], raw[q]);
+            if (kind[q] == 2) {
+              float sq, bq;
+              decode_sb<SB16>(sbw[q], sq, bq);
+              dequant8<BITS>(cw[q], sq, bq, raw[q]);
+            }
             if (first) {
 #pragma unroll
               for (int i = 0; i < 8; ++i) acc[i] = raw[q][i];

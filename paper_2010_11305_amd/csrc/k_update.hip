@@ -102,20 +102,22 @@ __global__ __launch_bounds__(256) void k_probe(Dev dv, Work w, uint32_t step) {
 // ---- merged gradient ----------------------------------------------------------------------
 // Left-to-right FP32 sum of the gradient rows of occurrences [i0, i1) of the sorted
 // stream (i0 < i1), seeded with the first.  Lane j of the group preloads the row
-// index of occurrence j of each chunk of LPR occurrences; U rows are loaded before
-// they are added in order.  A row listed more than once in one bag has adjacent
+// index of occurrence j of each chunk of LPR occurrences (for the first chunk the
+// caller may pass them in, myv0); U rows are loaded before they are added in order.  A row listed more than once in one bag has adjacent
 // occurrences with the same gradient row: with REUSE the repeat adds the row already
 // in registers instead of loading it again (same operands, same sums).  Repeats are
 // frequent only among rows with many lookups, so only their chunk sums use it.
 template <int D, bool REUSE>
 __device__ __forceinline__ void sum_occ(const uint32_t* __restrict__ sval, int64_t i0, int64_t i1,
-                                        const float* __restrict__ grad, int g, float (&acc)[8]) {
+                                        const float* __restrict__ grad, int g, float (&acc)[8],
+                                        uint32_t myv0 = 0u, bool have0 = false) {
   constexpr int LPR = Geo<D>::LPR, CPL = 8, U = kUnroll;
   bool first = true;
   if constexpr (!REUSE) {
     for (int64_t ic = i0; ic < i1; ic += LPR) {
       const int n = (int)min<int64_t>(LPR, i1 - ic);
-      const uint32_t myv = g < n ? sval[ic + g] : 0u;
+      // the first chunk's values may have been loaded by the caller (have0)
+      const uint32_t myv = (have0 && ic == i0) ? myv0 : (g < n ? sval[ic + g] : 0u);
       int j = 0;
       if (first) {
         load_frow8(grad + (int64_t)__shfl(myv, 0, LPR) * D, g, acc);
@@ -235,33 +237,40 @@ __global__ __launch_bounds__(256) void k_hot_fold(Work w) {
     const int64_t nch = w.nch[u];
     const float4* src = reinterpret_cast<const float4*>(w.partial + c0 * D);
     const int64_t n4 = nch * (D / 4);
-    float4 nxt[PER];
+    // loads past the row's last chunk sum re-read its last element (kept branch-free,
+    // so that all PER loads are in flight together); those staged values are not folded
+    float nxt[PER][4];
+    const auto fetch = [&](int64_t first) {
 #pragma unroll
-    for (int k = 0; k < PER; ++k) {
-      const int64_t i = tid + k * 256;
-      if (i < n4) nxt[k] = src[i];
-    }
+      for (int k = 0; k < PER; ++k) {
+        const float4 v = src[min<int64_t>(first + tid + k * 256, n4 - 1)];
+        nxt[k][0] = v.x; nxt[k][1] = v.y; nxt[k][2] = v.z; nxt[k][3] = v.w;
+      }
+    };
+    fetch(0);
     float acc = 0.0f;
     for (int64_t r0 = 0; r0 < nch; r0 += R) {
       const int rn = (int)min<int64_t>(R, nch - r0);
       __syncthreads();  // the previous round's fold is done with `stage`
 #pragma unroll
-      for (int k = 0; k < PER; ++k)
-        if (tid + k * 256 < rn * (D / 4)) stage[tid + k * 256] = nxt[k];
+      for (int k = 0; k < PER; ++k) stage[tid + k * 256] = make_float4(nxt[k][0], nxt[k][1], nxt[k][2], nxt[k][3]);
       __syncthreads();
-#pragma unroll
-      for (int k = 0; k < PER; ++k) {
-        const int64_t i = (r0 + R) * (D / 4) + tid + k * 256;
-        if (i < n4) nxt[k] = src[i];
-      }
+      fetch((r0 + R) * (D / 4));
       if (tid < D) {
-        const float* st = reinterpret_cast<const float*>(stage);
+        const float* st = reinterpret_cast<const float*>(stage) + tid;
         int r = 0;
         if (r0 == 0) {
-          acc = st[tid];
+          acc = st[0];
           r = 1;
         }
-        for (; r < rn; ++r) acc = acc + st[r * D + tid];
+        for (; r + 8 <= rn; r += 8) {
+          float v[8];
+#pragma unroll
+          for (int k = 0; k < 8; ++k) v[k] = st[(r + k) * D];
+#pragma unroll
+          for (int k = 0; k < 8; ++k) acc = acc + v[k];
+        }
+        for (; r < rn; ++r) acc = acc + st[r * D];
       }
     }
     if (tid < D) w.partial[c0 * D + tid] = acc;
@@ -579,6 +588,25 @@ __global__ __launch_bounds__(256) void k_evict(Dev dv, Work w, const uint32_t* _
 }
 
 // ---- per unique row: optimizer and write-back ------------------------------------------------
+// Per-row inputs of k_update, loaded one row ahead of their use.
+struct RowMeta {
+  int32_t act, grow, slot, dst;
+  uint32_t nch, s0, s1, cb;
+};
+
+__device__ __forceinline__ RowMeta load_meta(const Work& w, int64_t u) {
+  RowMeta m;
+  m.act = w.uact[u];
+  m.grow = w.urow[u];
+  m.slot = w.uslot[u];
+  m.dst = w.udest[u];
+  m.nch = w.nch[u];
+  m.s0 = w.seg[u];
+  m.s1 = w.seg[u + 1];
+  m.cb = w.chunk_base[u];
+  return m;
+}
+
 template <int D, int BITS, bool SB16>
 __global__ __launch_bounds__(256) void k_update(Dev dv, Work w, const uint32_t* __restrict__ sval,
                                                 const float* __restrict__ grad, uint32_t step) {
@@ -586,7 +614,6 @@ __global__ __launch_bounds__(256) void k_update(Dev dv, Work w, const uint32_t* 
   constexpr int GPB = 256 / LPR;
   constexpr int RB = Rec<D, BITS, SB16>::BYTES;
   const int g = threadIdx.x & (LPR - 1);
-  const int64_t nU = (int64_t)w.ctr[kCUnique];
   const bool sr = dv.rounding != 0;
   const XcdSplit xs(dv.T);
   const int64_t gx = xs.unit * GPB + threadIdx.x / LPR, gstride = xs.units * GPB;
@@ -596,40 +623,46 @@ __global__ __launch_bounds__(256) void k_update(Dev dv, Work w, const uint32_t* 
     table_rows(w, t, tlo, thi);
     part_range(tlo, thi, seg % xs.parts, xs.parts, lo, hi);
     const TableDesc td = dv.desc[t];
+    if (lo + gx >= hi) continue;
+    RowMeta next = load_meta(w, lo + gx);
     for (int64_t u = lo + gx; u < hi; u += gstride) {
-      // every load that does not depend on another is issued before the first use
-      const int32_t act = w.uact[u];
-      const int64_t grow = w.urow[u];
-      const int32_t slot = w.uslot[u];
-      const int32_t dst = w.udest[u];
-      const uint32_t nch = w.nch[u];
-      const uint32_t s0 = w.seg[u], s1 = w.seg[u + 1];
-      const uint32_t cb = w.chunk_base[u];
-      if (act == kActDone) continue;
+      const RowMeta m = next;
+      // the next row's metadata is in flight while this row is handled (the index is
+      // clamped so that the loads are unconditional; the last one is not used)
+      next = load_meta(w, min<int64_t>(u + gstride, hi - 1));
+      if (m.act == kActDone) continue;
+      const int64_t grow = m.grow;
       uint8_t* rec = dv.rec + grow * RB;
+      const bool hit = m.act == kActHitStay;
+      // first level of loads: the first occurrence values, the row, its accumulator
+      const uint32_t n0 = m.nch == 0 ? min<uint32_t>((uint32_t)LPR, m.s1 - m.s0) : 0u;
+      const uint32_t myv0 = (uint32_t)g < n0 ? sval[m.s0 + g] : 0u;
       float x[8], gr[8];
       CodeWords<BITS> cw;
-      float sc = 0.0f, bi = 0.0f;
-      const bool hit = act == kActHitStay;
+      SbWords<SB16> sbw;
       if (hit) {
-        load_frow8(dv.crow + (int64_t)slot * D, g, x);
+        load_frow8(dv.crow + (int64_t)m.slot * D, g, x);
       } else {
         cw = load_code_words<BITS>(rec, g);
-        load_sb<D, BITS, SB16>(rec, sc, bi);
+        sbw = load_sb_words<D, BITS, SB16>(rec);
       }
       const float G_old = load_G(dv, grow);
-      if (nch == 0) sum_occ<D, false>(sval, s0, s1, grad, g, gr);
-      else if (nch <= kFoldDirect) fold_chunks<D>(w.partial, cb, nch, g, gr);
-      else load_frow8(w.partial + (int64_t)cb * D, g, gr);
-      if (!hit) dequant8<BITS>(cw, sc, bi, x);
+      if (m.nch == 0) sum_occ<D, false>(sval, m.s0, m.s1, grad, g, gr, myv0, true);
+      else if (m.nch <= kFoldDirect) fold_chunks<D>(w.partial, m.cb, m.nch, g, gr);
+      else load_frow8(w.partial + (int64_t)m.cb * D, g, gr);
+      if (!hit) {
+        float sc, bi;
+        decode_sb<SB16>(sbw, sc, bi);
+        dequant8<BITS>(cw, sc, bi, x);
+      }
       apply_optimizer<D>(dv, x, gr, grow, g, G_old);
       if (hit) {
-        store_frow8(dv.crow + (int64_t)slot * D, g, x);
-      } else if (act == kActInsert) {
-        store_frow8(dv.crow + (int64_t)dst * D, g, x);
+        store_frow8(dv.crow + (int64_t)m.slot * D, g, x);
+      } else if (m.act == kActInsert) {
+        store_frow8(dv.crow + (int64_t)m.dst * D, g, x);
         if (g == 0) {
-          dv.tag[dst] = (int32_t)(grow - td.row_base);
-          if (dv.policy == 0) dv.ts[dst] = (int32_t)step;
+          dv.tag[m.dst] = (int32_t)(grow - td.row_base);
+          if (dv.policy == 0) dv.ts[m.dst] = (int32_t)step;
         }
       } else {
         quantize_store<D, BITS, SB16>(x, g, rec, sr, dv.seed, step, (uint32_t)t, (uint32_t)(grow - td.row_base));
