@@ -198,18 +198,27 @@ __global__ __launch_bounds__(256) void k_fwd_gather(Dev dv, const int32_t* __res
     const uint8_t* rec0 = dv.rec + td.row_base * RB;
     // codes outside this table's slots and rows are skipped (only malformed offsets produce them)
     const int64_t slot_lo = td.slot_base, slot_hi = td.slot_base + td.n_sets * dv.assoc;
+    if (blo + gx >= bhi) continue;
+    // the offsets of the group's next bag are loaded one bag ahead, the codes of the
+    // next LPR positions one chunk ahead (indices clamped so that the loads are
+    // unconditional; a clamped load is not used)
+    const int32_t* offt = off + (int64_t)t * B;
+    int64_t o0 = offt[blo + gx], o1 = offt[blo + gx + 1];
     for (int64_t b = blo + gx; b < bhi; b += gstride) {
-      const int64_t bag = (int64_t)t * B + b;
-      int64_t p0 = off[bag], p1 = off[bag + 1];
-      p0 = p0 < 0 ? 0 : p0;
-      p1 = p1 > L ? L : p1;
+      const int64_t p0 = o0 < 0 ? 0 : o0;
+      const int64_t p1 = o1 > L ? L : o1;
+      const int64_t nb = min<int64_t>(b + gstride, bhi - 1);
+      o0 = offt[nb];
+      o1 = offt[nb + 1];
       float acc[8];
 #pragma unroll
       for (int i = 0; i < 8; ++i) acc[i] = 0.0f;
       bool first = true;
+      int32_t code_next = p0 + g < p1 ? src[p0 + g] : -1;
       for (int64_t pc = p0; pc < p1; pc += LPR) {
         const int n = (int)min<int64_t>(LPR, p1 - pc);
-        const int32_t code = g < n ? src[pc + g] : -1;
+        const int32_t code = code_next;
+        code_next = pc + LPR + g < p1 ? src[pc + LPR + g] : -1;
         for (int j = 0; j < n; j += FU) {
           float raw[FU][8];
           CodeWords<BITS> cw[FU];
