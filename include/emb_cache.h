@@ -88,7 +88,8 @@ extern "C" {
  *                     k > 0 with k % interval == 0 (0 = never).
  *   seed              key of the stochastic-rounding random stream.
  *   max_batch         bags per table in one call (B); max_indices: indices in
- *                     one call over all tables.  They size the workspace.
+ *                     one call over all tables (1 .. 2^30 - 1).  They size the
+ *                     workspace.
  */
 typedef struct emb_cache_config {
   int32_t num_tables;
@@ -175,7 +176,9 @@ int emb_cache_backward_update(emb_cache_t h, const int32_t* indices, int64_t num
 int emb_cache_get_stats(emb_cache_t h, int32_t table, int64_t* out, void* stream);
 
 /* Synchronize `stream`, then return EMB_EINDEX (and clear the flag) if a
- * kernel has seen an out-of-range index since the last check, else EMB_OK. */
+ * kernel has seen an out-of-range index or malformed offsets since the last
+ * check, EMB_EHIP if a step's sort did not complete (its kernels gave up
+ * waiting on each other; that step's results are unspecified), else EMB_OK. */
 int emb_cache_check(emb_cache_t h, void* stream);
 
 /* Copy rows [row0, row0+n) of table `table` to host buffers, in the canonical

@@ -32,7 +32,8 @@ enum : int {
   kStEvictions, kStEmptyFills, kStHitEvictions, kStInvalidFwd, kStInvalidBwd, kNStat
 };
 
-enum : int { kErrIndex = 1, kErrOffsets = 2 };
+enum : int { kErrIndex = 1, kErrOffsets = 2, kErrSort = 4 };
+constexpr int kMaxPasses = 4;  // 8-bit digits of a 32-bit sort key
 
 // Per-table geometry.  Sort keys are set-major: key = key_base + set*Q + row/n_sets,
 // with set = row % n_sets and Q = ceil(N/n_sets), so that one sort groups the
@@ -80,7 +81,8 @@ struct Work {
   uint32_t* valsA;
   uint32_t* keysB;
   uint32_t* valsB;
-  uint32_t* hist;        // radix histograms [256][nblocks]
+  uint32_t* sort_small;  // radix sort: digit counts, their prefix sums, tile tickets
+  uint32_t* sort_status[2];  // radix sort look-back status words
   unsigned long long* part;  // scan partials
   unsigned long long* tile_cnt;  // unique rows and touched sets per tile of sorted keys, packed (sets << 32 | rows)
   unsigned long long* tile_pre;  // their exclusive prefix sums
@@ -129,7 +131,8 @@ hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int6
                            int32_t B, const float* grad, uint64_t step, int key_bits, bool decay,
                            hipStream_t s);
 
-size_t radix_hist_words(int64_t n);
+size_t sort_status_words(int64_t n);
+constexpr size_t kSortSmallWords = 2 * kMaxPasses * 256 + 64;
 size_t scan_partial_words(int64_t n);
 size_t uniq_tile_words(int64_t n);
 

@@ -9,10 +9,19 @@ template <typename T>
 hipError_t scan_exclusive(const T* in, T* out, int64_t n, const unsigned long long* dev_n, T* part, T* total,
                           hipStream_t s);
 
-// Stable LSD radix sort of n (key, value) pairs over `passes` 8-bit digits,
-// ping-ponging between (kA, vA) and (kB, vB); *in_B tells where the result is.
-hipError_t sort_pairs(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32_t* vB, int64_t n, int passes, uint32_t* hist,
-                      uint32_t* part, int* in_B, hipStream_t s);
+// Scratch of the radix sort, carved from the workspace.
+struct SortScratch {
+  uint32_t* ghist;      // [kMaxPasses][256] digit counts
+  uint32_t* gbase;      // [kMaxPasses][256] their exclusive prefix sums
+  uint32_t* tickets;    // [kMaxPasses] tile tickets
+  uint32_t* status[2];  // [sort_status_words(n)] look-back status words, alternating by pass
+};
+
+// Stable LSD radix sort of n < 2^30 (key, value) pairs over `passes` (<= kMaxPasses)
+// 8-bit digits, ping-ponging between (kA, vA) and (kB, vB); *in_B tells where the
+// result is.  A look-back that waits too long sets kErrSort in *err.
+hipError_t sort_pairs(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32_t* vB, int64_t n, int passes,
+                      const SortScratch& ss, int32_t* err, int* in_B, hipStream_t s);
 
 // Offsets must be non-decreasing and inside [0, L]; otherwise set the error flag and
 // ctr[kCBadOffsets].

@@ -2,7 +2,8 @@
 // row indices of the mini-batch, merge the gradients of each row).
 //
 //   k_expand       lookups -> (set-major row key, gradient-row index), position order
-//   radix passes   stable LSD radix sort, 8-bit digits, wave-ballot ranking
+//   radix passes   stable LSD radix sort, 8-bit digits, wave-ballot ranking, one kernel
+//                  per pass with decoupled look-back
 //   scans          3-phase exclusive prefix sums (u32 / u64)
 //   k_uniq_*       unique-row and touched-set lists (first occurrence of each row / set)
 #include "embc_device.h"
@@ -19,7 +20,6 @@ constexpr int kRadixItems = 16;
 constexpr int kRadixTile = kRadixThreads * kRadixItems;
 constexpr int kRadixWaves = kRadixThreads / 64;
 
-size_t radix_hist_words(int64_t n) { return 256 * (size_t)((n + kRadixTile - 1) / kRadixTile + 1); }
 size_t scan_partial_words(int64_t n) { return (size_t)((n + kScanTile - 1) / kScanTile + 64); }
 
 // ---- block-wide exclusive scan of one value per thread (256 threads) -------------------
@@ -132,43 +132,103 @@ __device__ __forceinline__ uint64_t match_digit(uint32_t d, bool valid) {
   return m;
 }
 
-// Per-tile digit histogram, written digit-major: hist[digit * nblocks + block].
-__global__ __launch_bounds__(kRadixThreads) void k_radix_hist(const uint32_t* __restrict__ keys, int64_t n, int shift,
-                                                              uint32_t* __restrict__ hist, int64_t nblocks) {
-  __shared__ uint32_t h[256];
-  h[threadIdx.x] = 0;
-  __syncthreads();
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  const int64_t base = (int64_t)blockIdx.x * kRadixTile + (int64_t)wv * 64 * kRadixItems;
-  for (int i = 0; i < kRadixItems; ++i) {
-    const int64_t p = base + i * 64 + lane;
-    const bool valid = p < n;
-    const uint32_t d = valid ? (keys[p] >> shift) & 255u : 0u;
-    const uint64_t peers = match_digit(d, valid);
-    if (valid && (peers & lanemask_lt()) == 0) atomicAdd(&h[d], (uint32_t)__popcll(peers));
-  }
-  __syncthreads();
-  hist[(int64_t)threadIdx.x * nblocks + blockIdx.x] = h[threadIdx.x];
+// Stable LSD radix sort, one kernel per 8-bit digit pass ("single sweep"):
+//   k_sort_hist   global histograms of every pass's digit in one read of the keys
+//   k_sort_scan   their exclusive prefix sums: where each digit's run starts
+//   k_sort_pass   per tile of kRadixTile pairs (tiles taken in launch order from an
+//                 atomic ticket): rank the tile's digits, publish the per-digit tile
+//                 counts, find the tile's offset inside each digit's run by looking
+//                 back over the published counts of the preceding tiles (decoupled
+//                 look-back), then scatter through LDS in digit runs.
+// A status word per (tile, digit) holds a 2-bit state and a 30-bit count: not yet
+// published, the tile's own count, or the inclusive count up to and including the
+// tile.  Tiles are numbered in the order their workgroups start, so every tile a
+// look-back waits for is already running; the wait is bounded all the same (after
+// kSortSpinLimit polls the step is flagged as failed and the tile goes on).
+constexpr uint32_t kStAgg = 1u << 30;
+constexpr uint32_t kStPre = 2u << 30;
+constexpr uint32_t kStCount = (1u << 30) - 1;
+constexpr uint32_t kSortSpinLimit = 1u << 20;
+
+size_t sort_status_words(int64_t n) { return 256 * (size_t)((n + kRadixTile - 1) / kRadixTile + 1); }
+
+__device__ __forceinline__ uint32_t status_load(const uint32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void status_store(uint32_t* p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Stable scatter: rank inside the tile by (digit, position), stage in LDS in
-// digit order, then write runs to the digit's global offset.
-__global__ __launch_bounds__(kRadixThreads) void k_radix_scatter(const uint32_t* __restrict__ kin,
-                                                                 const uint32_t* __restrict__ vin,
-                                                                 uint32_t* __restrict__ kout,
-                                                                 uint32_t* __restrict__ vout, int64_t n, int shift,
-                                                                 const uint32_t* __restrict__ hist_scanned,
-                                                                 int64_t nblocks) {
+// ghist [kMaxPasses][256] and the pass tickets must be zero on entry (k_sort_begin).
+// Also clears the status words of the first pass.
+__global__ __launch_bounds__(256) void k_sort_hist(const uint32_t* __restrict__ keys, int64_t n, int passes,
+                                                   uint32_t* __restrict__ ghist, uint32_t* __restrict__ status,
+                                                   int64_t status_words) {
+  __shared__ uint32_t h[kRadixWaves][kMaxPasses][256];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  for (int i = threadIdx.x; i < kRadixWaves * kMaxPasses * 256; i += 256) (&h[0][0][0])[i] = 0;
+  __syncthreads();
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  // whole waves iterate together (the tail lanes count nothing), so that the lanes
+  // sharing lane 0's digit are counted with one atomic: high digits of keys that
+  // are nearly sorted would otherwise all hit one LDS word
+  for (int64_t i0 = (int64_t)blockIdx.x * blockDim.x + wv * 64; i0 < n; i0 += stride) {
+    const int64_t i = i0 + lane;
+    const bool valid = i < n;
+    const uint32_t k = valid ? keys[i] : 0u;
+    for (int p = 0; p < passes; ++p) {
+      const uint32_t d = (k >> (8 * p)) & 255u;
+      const uint32_t d0 = __shfl(d, 0);
+      const uint64_t same = __ballot(valid && d == d0);
+      if (lane == 0) atomicAdd(&h[wv][p][d0], (uint32_t)__popcll(same));
+      if (valid && d != d0) atomicAdd(&h[wv][p][d], 1u);
+    }
+  }
+  __syncthreads();
+  for (int p = 0; p < passes; ++p) {
+    uint32_t c = 0;
+#pragma unroll
+    for (int w = 0; w < kRadixWaves; ++w) c += h[w][p][threadIdx.x];
+    if (c) atomicAdd(&ghist[p * 256 + threadIdx.x], c);
+  }
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < status_words; i += stride) status[i] = 0;
+}
+
+__global__ void k_sort_begin(uint32_t* __restrict__ ghist, uint32_t* __restrict__ tickets) {
+  for (int i = threadIdx.x; i < kMaxPasses * 256; i += blockDim.x) ghist[i] = 0;
+  if (threadIdx.x < kMaxPasses) tickets[threadIdx.x] = 0;
+}
+
+// gbase[p][d] = number of keys whose pass-p digit is below d.
+__global__ __launch_bounds__(256) void k_sort_scan(const uint32_t* __restrict__ ghist, uint32_t* __restrict__ gbase,
+                                                   int passes) {
+  __shared__ uint32_t lds4[4];
+  for (int p = 0; p < passes; ++p) {
+    uint32_t tot;
+    gbase[p * 256 + threadIdx.x] = block_exclusive_scan<uint32_t>(ghist[p * 256 + threadIdx.x], lds4, tot);
+  }
+}
+
+__global__ __launch_bounds__(kRadixThreads) void k_sort_pass(const uint32_t* __restrict__ kin,
+                                                             const uint32_t* __restrict__ vin,
+                                                             uint32_t* __restrict__ kout, uint32_t* __restrict__ vout,
+                                                             int64_t n, int shift, const uint32_t* __restrict__ gbase,
+                                                             uint32_t* __restrict__ status, uint32_t* __restrict__ ticket,
+                                                             uint32_t* __restrict__ next_status,
+                                                             int64_t status_words, int32_t* __restrict__ err) {
   __shared__ uint32_t wcnt[kRadixWaves][256];
   __shared__ uint32_t dpre[256];
   __shared__ uint32_t goff[256];
   __shared__ uint32_t skey[kRadixTile];
   __shared__ uint32_t sval[kRadixTile];
   __shared__ uint32_t lds4[4];
+  __shared__ uint32_t tile_s;
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   for (int i = threadIdx.x; i < kRadixWaves * 256; i += kRadixThreads) (&wcnt[0][0])[i] = 0;
+  if (threadIdx.x == 0) tile_s = atomicAdd(ticket, 1u);
   __syncthreads();
-  const int64_t tile0 = (int64_t)blockIdx.x * kRadixTile;
+  const int64_t tile = tile_s;
+  const int64_t tile0 = tile * kRadixTile;
   const int64_t base = tile0 + (int64_t)wv * 64 * kRadixItems;
   uint32_t k[kRadixItems], v[kRadixItems], rank[kRadixItems];
 #pragma unroll
@@ -177,6 +237,11 @@ __global__ __launch_bounds__(kRadixThreads) void k_radix_scatter(const uint32_t*
     const bool valid = p < n;
     k[i] = valid ? kin[p] : 0xFFFFFFFFu;
     v[i] = valid ? vin[p] : 0u;
+  }
+#pragma unroll
+  for (int i = 0; i < kRadixItems; ++i) {
+    const int64_t p = base + i * 64 + lane;
+    const bool valid = p < n;
     const uint32_t d = (k[i] >> shift) & 255u;
     const uint64_t peers = match_digit(d, valid);
     const uint32_t before = (uint32_t)__popcll(peers & lanemask_lt());
@@ -197,9 +262,34 @@ __global__ __launch_bounds__(kRadixThreads) void k_radix_scatter(const uint32_t*
       wcnt[w][d] = run;
       run += c;
     }
+    uint32_t* st = status + tile * 256 + d;
+    uint32_t excl = 0;
+    if (tile == 0) {
+      status_store(st, kStPre | run);
+    } else {
+      status_store(st, kStAgg | run);
+      int64_t j = tile - 1;
+      uint32_t polls = 0;
+      for (;;) {
+        const uint32_t w = status_load(status + j * 256 + d);
+        const uint32_t state = w & ~kStCount;
+        if (state == 0) {
+          if (++polls > kSortSpinLimit) {
+            atomicOr(err, kErrSort);
+            break;
+          }
+          __builtin_amdgcn_s_sleep(1);
+          continue;
+        }
+        excl += w & kStCount;
+        if (state == kStPre || j == 0) break;
+        --j;
+      }
+      status_store(st, kStPre | (excl + run));
+    }
     uint32_t tot;
     dpre[d] = block_exclusive_scan<uint32_t>(run, lds4, tot);
-    goff[d] = hist_scanned[(int64_t)d * nblocks + blockIdx.x];
+    goff[d] = gbase[d] + excl;
   }
   __syncthreads();
 #pragma unroll
@@ -218,26 +308,36 @@ __global__ __launch_bounds__(kRadixThreads) void k_radix_scatter(const uint32_t*
     const uint32_t key = skey[j];
     const uint32_t d = (key >> shift) & 255u;
     const uint32_t g = goff[d] + (uint32_t)j - dpre[d];
-    kout[g] = key;
-    vout[g] = sval[j];
+    if ((int64_t)g < n) {  // always, unless a look-back gave up
+      kout[g] = key;
+      vout[g] = sval[j];
+    }
+  }
+  // the other status buffer (the previous pass's, finished) is cleared for the next pass
+  if (next_status) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < status_words; i += stride) next_status[i] = 0;
   }
 }
 
-hipError_t sort_pairs(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32_t* vB, int64_t n, int passes, uint32_t* hist,
-                      uint32_t* part, int* in_B, hipStream_t s) {
+hipError_t sort_pairs(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32_t* vB, int64_t n, int passes,
+                      const SortScratch& ss, int32_t* err, int* in_B, hipStream_t s) {
   *in_B = 0;
   if (n <= 0) return hipSuccess;
+  if (passes < 1 || passes > kMaxPasses || n > (int64_t)kStCount) return hipErrorInvalidValue;
   const int64_t nb = (n + kRadixTile - 1) / kRadixTile;
+  const int64_t sw = 256 * nb;
+  k_sort_begin<<<1, 256, 0, s>>>(ss.ghist, ss.tickets);
+  k_sort_hist<<<grid_for(n, 2048), 256, 0, s>>>(kA, n, passes, ss.ghist, ss.status[0], sw);
+  k_sort_scan<<<1, 256, 0, s>>>(ss.ghist, ss.gbase, passes);
   for (int pass = 0; pass < passes; ++pass) {
-    const int shift = 8 * pass;
     const uint32_t* ki = *in_B ? kB : kA;
     const uint32_t* vi = *in_B ? vB : vA;
     uint32_t* ko = *in_B ? kA : kB;
     uint32_t* vo = *in_B ? vA : vB;
-    k_radix_hist<<<(unsigned)nb, kRadixThreads, 0, s>>>(ki, n, shift, hist, nb);
-    hipError_t e = scan_exclusive<uint32_t>(hist, hist, 256 * nb, nullptr, part, nullptr, s);
-    if (e != hipSuccess) return e;
-    k_radix_scatter<<<(unsigned)nb, kRadixThreads, 0, s>>>(ki, vi, ko, vo, n, shift, hist, nb);
+    uint32_t* next = pass + 1 < passes ? ss.status[(pass + 1) & 1] : nullptr;
+    k_sort_pass<<<(unsigned)nb, kRadixThreads, 0, s>>>(ki, vi, ko, vo, n, 8 * pass, ss.gbase + 256 * pass,
+                                                       ss.status[pass & 1], ss.tickets + pass, next, sw, err);
     *in_B = !*in_B;
   }
   return hipGetLastError();

@@ -681,7 +681,9 @@ hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int6
   if (e != hipSuccess) return e;
   const int passes = (key_bits + 7) / 8;
   int in_B = 0;
-  e = sort_pairs(w.keysA, w.valsA, w.keysB, w.valsB, L, passes, w.hist, reinterpret_cast<uint32_t*>(w.part), &in_B, s);
+  const SortScratch ss{w.sort_small, w.sort_small + kMaxPasses * 256, w.sort_small + 2 * kMaxPasses * 256,
+                       {w.sort_status[0], w.sort_status[1]}};
+  e = sort_pairs(w.keysA, w.valsA, w.keysB, w.valsB, L, passes, ss, d.err, &in_B, s);
   if (e != hipSuccess) return e;
   const uint32_t* sk = in_B ? w.keysB : w.keysA;
   const uint32_t* sv = in_B ? w.valsB : w.valsA;

@@ -65,7 +65,7 @@ struct Plan {
   // state offsets
   size_t o_rec, o_crow, o_tag, o_ts, o_cnt, o_G, o_desc, o_keyb, o_stats, o_err, state_bytes;
   // workspace offsets
-  size_t o_kA, o_vA, o_kB, o_vB, o_hist, o_part, o_tcnt, o_tpre, o_uk, o_seg, o_setf, o_urow, o_utab, o_uslot,
+  size_t o_kA, o_vA, o_kB, o_vB, o_ssmall, o_sst0, o_sst1, o_part, o_tcnt, o_tpre, o_uk, o_seg, o_setf, o_urow, o_utab, o_uslot,
       o_uact, o_udest, o_nch, o_cbase, o_uvrow, o_uvu, o_partial, o_owner, o_long, o_tabf, o_src, o_ctr, ws_bytes;
   int64_t max_partials = 0;
 };
@@ -85,7 +85,7 @@ int plan_config(const emb_cache_config* c, Plan* p) {
   if (c->rounding != EMB_ROUND_NEAREST && c->rounding != EMB_ROUND_STOCHASTIC) return EMB_EINVAL;
   if (c->optimizer != EMB_OPT_SGD && c->optimizer != EMB_OPT_ROWWISE_ADAGRAD) return EMB_EINVAL;
   if (!std::isfinite(c->lr) || !std::isfinite(c->eps) || c->eps < 0.0f) return EMB_EINVAL;
-  if (c->max_batch < 1 || c->max_indices < 1 || c->max_indices >= (int64_t)INT32_MAX) return EMB_EINVAL;
+  if (c->max_batch < 1 || c->max_indices < 1 || c->max_indices >= ((int64_t)1 << 30)) return EMB_EINVAL;
   if ((int64_t)c->max_batch * c->num_tables >= (int64_t)UINT32_MAX) return EMB_EINVAL;
 
   const int T = c->num_tables;
@@ -147,7 +147,9 @@ int plan_config(const emb_cache_config* c, Plan* p) {
   p->o_vA = take(4 * L);
   p->o_kB = take(4 * L);
   p->o_vB = take(4 * L);
-  p->o_hist = take(4 * embc::radix_hist_words((int64_t)L));
+  p->o_ssmall = take(4 * embc::kSortSmallWords);
+  p->o_sst0 = take(4 * embc::sort_status_words((int64_t)L));
+  p->o_sst1 = take(4 * embc::sort_status_words((int64_t)L));
   p->o_part = take(8 * embc::scan_partial_words((int64_t)L + 256 * 64));
   p->o_tcnt = take(8 * embc::uniq_tile_words((int64_t)L));
   p->o_tpre = take(8 * embc::uniq_tile_words((int64_t)L));
@@ -253,7 +255,8 @@ int emb_cache_create(const emb_cache_config* cfg, void* state, size_t state_byte
   h->cfg = *cfg;
   h->rows.assign(cfg->rows, cfg->rows + cfg->num_tables);
   h->cfg.rows = h->rows.data();
-  h->key_bits = bit_length((uint64_t)(p.total_keys > 0 ? p.total_keys - 1 : 0));
+  // every valid key is below 2^key_bits - 1, the skipped-lookup key truncated to key_bits
+  h->key_bits = bit_length((uint64_t)p.total_keys);
   if (h->key_bits < 1) h->key_bits = 1;
 
   uint8_t* sb = static_cast<uint8_t*>(state);
@@ -289,7 +292,9 @@ int emb_cache_create(const emb_cache_config* cfg, void* state, size_t state_byte
   w.valsA = reinterpret_cast<uint32_t*>(wb + p.o_vA);
   w.keysB = reinterpret_cast<uint32_t*>(wb + p.o_kB);
   w.valsB = reinterpret_cast<uint32_t*>(wb + p.o_vB);
-  w.hist = reinterpret_cast<uint32_t*>(wb + p.o_hist);
+  w.sort_small = reinterpret_cast<uint32_t*>(wb + p.o_ssmall);
+  w.sort_status[0] = reinterpret_cast<uint32_t*>(wb + p.o_sst0);
+  w.sort_status[1] = reinterpret_cast<uint32_t*>(wb + p.o_sst1);
   w.part = reinterpret_cast<unsigned long long*>(wb + p.o_part);
   w.tile_cnt = reinterpret_cast<unsigned long long*>(wb + p.o_tcnt);
   w.tile_pre = reinterpret_cast<unsigned long long*>(wb + p.o_tpre);
@@ -386,7 +391,7 @@ int emb_cache_check(emb_cache_t h, void* stream) {
     e = hipMemcpyAsync(h->dev.err, &zero, sizeof(zero), hipMemcpyHostToDevice, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) return EMB_EHIP;
-    return EMB_EINDEX;
+    return (flag & embc::kErrSort) ? EMB_EHIP : EMB_EINDEX;
   }
   return EMB_OK;
 }
