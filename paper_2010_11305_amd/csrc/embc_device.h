@@ -30,6 +30,42 @@ struct Rec {
   static constexpr int BYTES = CODE_BYTES + (SB16 ? 4 : 8);
 };
 
+// ---- lane exchange inside a row group ---------------------------------------------------
+// x of lane (lane ^ M), for M < LPR.  Masks 1..8 stay inside a 16-lane DPP row and use
+// DPP moves (quad permutations and row mirrors compose to every xor below 16):
+//   ^1, ^2 = quad_perm [1,0,3,2], [2,3,0,1];  ^4 = half-row mirror (^7) after quad
+//   reverse (^3);  ^8 = row mirror (^15) after half-row mirror (^7).
+// Mask 16 (32-lane groups) goes through the LDS crossbar.
+template <int M>
+__device__ __forceinline__ float xor_lane(float x) {
+  const int v = __float_as_int(x);
+  if constexpr (M == 1) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, false));
+  } else if constexpr (M == 2) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, false));
+  } else if constexpr (M == 4) {
+    const int r = __builtin_amdgcn_mov_dpp(v, 0x1B, 0xF, 0xF, false);
+    return __int_as_float(__builtin_amdgcn_mov_dpp(r, 0x141, 0xF, 0xF, false));
+  } else if constexpr (M == 8) {
+    const int r = __builtin_amdgcn_mov_dpp(v, 0x141, 0xF, 0xF, false);
+    return __int_as_float(__builtin_amdgcn_mov_dpp(r, 0x140, 0xF, 0xF, false));
+  } else {
+    static_assert(M == 16, "lane groups are at most 32 lanes");
+    return __shfl_xor(x, 16, 32);
+  }
+}
+
+// Applies op(x, xor_lane<M>(x)) for M = LPR/2, ..., 1 (a butterfly over the row group).
+template <int LPR, typename Op>
+__device__ __forceinline__ float butterfly(float x, Op op) {
+  if constexpr (LPR > 16) x = op(x, xor_lane<16>(x));
+  if constexpr (LPR > 8) x = op(x, xor_lane<8>(x));
+  if constexpr (LPR > 4) x = op(x, xor_lane<4>(x));
+  if constexpr (LPR > 2) x = op(x, xor_lane<2>(x));
+  if constexpr (LPR > 1) x = op(x, xor_lane<1>(x));
+  return x;
+}
+
 // ---- Philox4x32-10 (Salmon et al., SC'11): 10 rounds, Weyl key schedule -------------
 __device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1) {
 #pragma unroll
@@ -159,11 +195,8 @@ __device__ __forceinline__ void quantize_store(const float (&x)[8], int g, uint8
     mn = fminf(mn, x[i]);
     mx = fmaxf(mx, x[i]);
   }
-#pragma unroll
-  for (int o = LPR / 2; o >= 1; o >>= 1) {
-    mn = fminf(mn, __shfl_xor(mn, o, LPR));
-    mx = fmaxf(mx, __shfl_xor(mx, o, LPR));
-  }
+  mn = butterfly<LPR>(mn, [](float a, float b) { return fminf(a, b); });
+  mx = butterfly<LPR>(mx, [](float a, float b) { return fmaxf(a, b); });
   mn = mn + 0.0f;
   mx = mx + 0.0f;
   float s = (mx - mn) / K;

@@ -358,9 +358,7 @@ __device__ __forceinline__ void apply_optimizer(const Dev& dv, float (&x)[8], co
 #pragma unroll
   for (int i = 0; i < 8; ++i) a[i] = gr[i] * gr[i];
 #pragma unroll
-  for (int o = LPR / 2; o >= 1; o >>= 1)
-#pragma unroll
-    for (int i = 0; i < 8; ++i) a[i] = a[i] + __shfl_xor(a[i], o, LPR);
+  for (int i = 0; i < 8; ++i) a[i] = butterfly<LPR>(a[i], [](float p, float q) { return p + q; });
 #pragma unroll
   for (int h = 4; h >= 1; h >>= 1)
 #pragma unroll
