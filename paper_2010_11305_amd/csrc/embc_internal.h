@@ -99,7 +99,7 @@ struct Work {
   int32_t* uvic_row;     // [L] insert: table-local row displaced from its way, -1 = empty way
   int32_t* uvic_u;       // [L] insert: unique index of that row if it was updated this step, else -1
   float* partial;        // [L/32 + 2][dim] chunk sums
-  int32_t* chunk_owner;  // [L/32 + 2] unique row of each chunk
+  uint2* chunk_span;     // [L/32 + 2] occurrences [x, y) of the sorted stream summed by each chunk
   int32_t* long_rows;    // [L/(64*kFoldDirect) + 1] unique rows with more than kFoldDirect chunk sums
   int32_t* tab_first;    // [T+1] first unique row of each table (tab_first[T] = number of unique rows)
   int32_t* fwd_src;      // [L] forward: cache slot of each lookup, -2-row for a miss, -1 if skipped

@@ -103,80 +103,91 @@ __global__ __launch_bounds__(256) void k_probe(Dev dv, Work w, uint32_t step) {
 // Left-to-right FP32 sum of the gradient rows of occurrences [i0, i1) of the sorted
 // stream (i0 < i1), seeded with the first.  Lane j of the group preloads the row
 // index of occurrence j of each chunk of LPR occurrences (for the first chunk the
-// caller may pass them in, myv0); U rows are loaded before they are added in order.  A row listed more than once in one bag has adjacent
-// occurrences with the same gradient row: with REUSE the repeat adds the row already
-// in registers instead of loading it again (same operands, same sums).  Repeats are
-// frequent only among rows with many lookups, so only their chunk sums use it.
-template <int D, bool REUSE>
+// caller may pass them in, myv0); U rows are loaded before they are added in order.
+template <int D>
 __device__ __forceinline__ void sum_occ(const uint32_t* __restrict__ sval, int64_t i0, int64_t i1,
                                         const float* __restrict__ grad, int g, float (&acc)[8],
                                         uint32_t myv0 = 0u, bool have0 = false) {
   constexpr int LPR = Geo<D>::LPR, CPL = 8, U = kUnroll;
   bool first = true;
-  if constexpr (!REUSE) {
-    for (int64_t ic = i0; ic < i1; ic += LPR) {
-      const int n = (int)min<int64_t>(LPR, i1 - ic);
-      // the first chunk's values may have been loaded by the caller (have0)
-      const uint32_t myv = (have0 && ic == i0) ? myv0 : (g < n ? sval[ic + g] : 0u);
-      int j = 0;
-      if (first) {
-        load_frow8(grad + (int64_t)__shfl(myv, 0, LPR) * D, g, acc);
-        first = false;
-        j = 1;
-      }
-      for (; j + U <= n; j += U) {
-        float x[U][CPL];
-#pragma unroll
-        for (int q = 0; q < U; ++q) load_frow8(grad + (int64_t)__shfl(myv, j + q, LPR) * D, g, x[q]);
-#pragma unroll
-        for (int q = 0; q < U; ++q)
-#pragma unroll
-          for (int k = 0; k < CPL; ++k) acc[k] = acc[k] + x[q][k];
-      }
-      for (; j < n; ++j) {
-        float x[CPL];
-        load_frow8(grad + (int64_t)__shfl(myv, j, LPR) * D, g, x);
-#pragma unroll
-        for (int k = 0; k < CPL; ++k) acc[k] = acc[k] + x[k];
-      }
+  for (int64_t ic = i0; ic < i1; ic += LPR) {
+    const int n = (int)min<int64_t>(LPR, i1 - ic);
+    // the first chunk's values may have been loaded by the caller (have0)
+    const uint32_t myv = (have0 && ic == i0) ? myv0 : (g < n ? sval[ic + g] : 0u);
+    int j = 0;
+    if (first) {
+      load_frow8(grad + (int64_t)__shfl(myv, 0, LPR) * D, g, acc);
+      first = false;
+      j = 1;
     }
-  } else {
-    uint32_t pv = 0xFFFFFFFFu;  // gradient row of the last occurrence added (none yet)
-    float last[CPL];
+    for (; j + U <= n; j += U) {
+      float x[U][CPL];
 #pragma unroll
-    for (int k = 0; k < CPL; ++k) last[k] = 0.0f;
-    for (int64_t ic = i0; ic < i1; ic += LPR) {
-      const int n = (int)min<int64_t>(LPR, i1 - ic);
-      const uint32_t myv = g < n ? sval[ic + g] : 0u;
-      for (int j = 0; j < n; j += U) {
-        uint32_t v[U];
-        bool fresh[U];
-        float x[U][CPL];
+      for (int q = 0; q < U; ++q) load_frow8(grad + (int64_t)__shfl(myv, j + q, LPR) * D, g, x[q]);
 #pragma unroll
-        for (int q = 0; q < U; ++q) {
-          v[q] = __shfl(myv, j + q, LPR);
-          fresh[q] = j + q < n && v[q] != (q == 0 ? pv : v[q - 1]);
-          if (fresh[q]) load_frow8(grad + (int64_t)v[q] * D, g, x[q]);
-        }
+      for (int q = 0; q < U; ++q)
 #pragma unroll
-        for (int q = 0; q < U; ++q) {
-          if (j + q < n) {
-            if (!fresh[q]) {
+        for (int k = 0; k < CPL; ++k) acc[k] = acc[k] + x[q][k];
+    }
+    for (; j < n; ++j) {
+      float x[CPL];
+      load_frow8(grad + (int64_t)__shfl(myv, j, LPR) * D, g, x);
 #pragma unroll
-              for (int k = 0; k < CPL; ++k) x[q][k] = last[k];
-            }
-            if (first) {
+      for (int k = 0; k < CPL; ++k) acc[k] = acc[k] + x[k];
+    }
+  }
+}
+
+constexpr int kChunkUnroll = 4;  // gradient rows in flight per row group in a chunk sum
+
+// Sum of one chunk (occurrences [i0, i1) of the sorted stream, 0 < i1 - i0 <= 64),
+// left to right, seeded with the first.  The occurrence values of the next LPR
+// occurrences are loaded while the current ones are summed, U gradient rows are in
+// flight at a time, and a row listed more than once in one bag (adjacent occurrences
+// with the same gradient row) adds the row already in registers instead of loading it
+// again (same operands, same sums).
+template <int D>
+__device__ __forceinline__ void chunk_sum(const uint32_t* __restrict__ sval, int64_t i0, int64_t i1,
+                                          const float* __restrict__ grad, int g, float (&acc)[8]) {
+  constexpr int LPR = Geo<D>::LPR, CPL = 8, U = kChunkUnroll;
+  bool first = true;
+  uint32_t pv = 0xFFFFFFFFu;  // gradient row of the last occurrence added (none yet)
+  float last[CPL];
 #pragma unroll
-              for (int k = 0; k < CPL; ++k) acc[k] = x[q][k];
-              first = false;
-            } else {
+  for (int k = 0; k < CPL; ++k) last[k] = 0.0f;
+  uint32_t vnext = i0 + g < i1 ? sval[i0 + g] : 0u;
+  for (int64_t ic = i0; ic < i1; ic += LPR) {
+    const int n = (int)min<int64_t>(LPR, i1 - ic);
+    const uint32_t myv = vnext;
+    vnext = ic + LPR + g < i1 ? sval[ic + LPR + g] : 0u;
+    for (int j = 0; j < n; j += U) {
+      uint32_t v[U];
+      bool fresh[U];
+      float x[U][CPL];
 #pragma unroll
-              for (int k = 0; k < CPL; ++k) acc[k] = acc[k] + x[q][k];
-            }
+      for (int q = 0; q < U; ++q) {
+        v[q] = __shfl(myv, j + q, LPR);
+        fresh[q] = j + q < n && v[q] != (q == 0 ? pv : v[q - 1]);
+        if (fresh[q]) load_frow8(grad + (int64_t)v[q] * D, g, x[q]);
+      }
 #pragma unroll
-            for (int k = 0; k < CPL; ++k) last[k] = x[q][k];
-            pv = v[q];
+      for (int q = 0; q < U; ++q) {
+        if (j + q < n) {
+          if (!fresh[q]) {
+#pragma unroll
+            for (int k = 0; k < CPL; ++k) x[q][k] = last[k];
           }
+          if (first) {
+#pragma unroll
+            for (int k = 0; k < CPL; ++k) acc[k] = x[q][k];
+            first = false;
+          } else {
+#pragma unroll
+            for (int k = 0; k < CPL; ++k) acc[k] = acc[k] + x[q][k];
+          }
+#pragma unroll
+          for (int k = 0; k < CPL; ++k) last[k] = x[q][k];
+          pv = v[q];
         }
       }
     }
@@ -215,14 +226,14 @@ template <int D>
 __device__ __forceinline__ void merged_grad(const Work& w, const uint32_t* __restrict__ sval,
                                             const float* __restrict__ grad, int64_t u, int g, float (&acc)[8]) {
   const uint32_t n = w.nch[u];
-  if (n == 0) sum_occ<D, false>(sval, w.seg[u], w.seg[u + 1], grad, g, acc);
+  if (n == 0) sum_occ<D>(sval, w.seg[u], w.seg[u + 1], grad, g, acc);
   else if (n <= kFoldDirect) fold_chunks<D>(w.partial, w.chunk_base[u], n, g, acc);
   else load_frow8(w.partial + (int64_t)w.chunk_base[u] * D, g, acc);
 }
 
 // Fold of the chunk sums of each row with more than kFoldDirect of them: acc = p0 +
 // p1 + ... left to right, per column, into the row's first chunk slot.  One workgroup
-// per row (from the list k_chunk_owner builds): all threads stage R chunk sums in LDS,
+// per row (from the list k_chunk_spans builds): all threads stage R chunk sums in LDS,
 // load the next R into registers, and one thread per column folds the staged ones.
 template <int D>
 __global__ __launch_bounds__(256) void k_hot_fold(Work w) {
@@ -296,16 +307,20 @@ __global__ void k_tab_first(Work w, int T) {
   }
 }
 
-// chunk_owner[c] = the unique row whose chunk sums include chunk c; rows with more
-// than kFoldDirect chunks are listed for k_hot_fold (in any order).
-__global__ __launch_bounds__(256) void k_chunk_owner(Work w) {
+// chunk_span[c] = occurrences [x, y) of the sorted stream that chunk c sums; rows with
+// more than kFoldDirect chunks are listed for k_hot_fold (in any order).
+__global__ __launch_bounds__(256) void k_chunk_spans(Work w) {
   const int64_t nU = (int64_t)w.ctr[kCUnique];
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < nU; u += stride) {
     const uint32_t n = w.nch[u];
     if (n == 0) continue;
     const int64_t c0 = w.chunk_base[u];
-    for (uint32_t j = 0; j < n; ++j) w.chunk_owner[c0 + j] = (int32_t)u;
+    const uint32_t s0 = w.seg[u], s1 = w.seg[u + 1];
+    for (uint32_t j = 0; j < n; ++j) {
+      const uint32_t a = s0 + j * (uint32_t)kSumChunk;
+      w.chunk_span[c0 + j] = make_uint2(a, min(a + (uint32_t)kSumChunk, s1));
+    }
     if (n > kFoldDirect) w.long_rows[atomicAdd(&w.ctr[kCLongRows], 1ull)] = (int32_t)u;
   }
 }
@@ -329,13 +344,14 @@ __global__ __launch_bounds__(256) void k_partials(Dev dv, Work w, const uint32_t
     const int64_t chi_t = uhi < nU ? (int64_t)w.chunk_base[uhi] : nC;
     int64_t clo, chi;
     part_range(clo_t, chi_t, seg % xs.parts, xs.parts, clo, chi);
+    if (clo + gx >= chi) continue;
+    // the next chunk's span is loaded one chunk ahead (clamped index, unconditional load)
+    uint2 next = w.chunk_span[clo + gx];
     for (int64_t c = clo + gx; c < chi; c += gstride) {
-      const int64_t u = w.chunk_owner[c];
-      const int64_t j = c - (int64_t)w.chunk_base[u];
-      const int64_t i0 = (int64_t)w.seg[u] + j * kSumChunk;
-      const int64_t i1 = min<int64_t>(i0 + kSumChunk, (int64_t)w.seg[u + 1]);
+      const uint2 sp = next;
+      next = w.chunk_span[min<int64_t>(c + gstride, chi - 1)];
       float acc[8];
-      sum_occ<D, true>(sval, i0, i1, grad, g, acc);
+      chunk_sum<D>(sval, sp.x, sp.y, grad, g, acc);
       store_frow8(w.partial + c * D, g, acc);
     }
   }
@@ -645,7 +661,7 @@ __global__ __launch_bounds__(256) void k_update(Dev dv, Work w, const uint32_t* 
         sbw = load_sb_words<D, BITS, SB16>(rec);
       }
       const float G_old = load_G(dv, grow);
-      if (m.nch == 0) sum_occ<D, false>(sval, m.s0, m.s1, grad, g, gr, myv0, true);
+      if (m.nch == 0) sum_occ<D>(sval, m.s0, m.s1, grad, g, gr, myv0, true);
       else if (m.nch <= kFoldDirect) fold_chunks<D>(w.partial, m.cb, m.nch, g, gr);
       else load_frow8(w.partial + (int64_t)m.cb * D, g, gr);
       if (!hit) {
@@ -694,7 +710,7 @@ hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int6
                                reinterpret_cast<uint32_t*>(w.ctr + kCScanTotal), s);
   if (e != hipSuccess) return e;
   k_chunks_total<<<1, 1, 0, s>>>(w.ctr);
-  k_chunk_owner<<<grid(k_chunk_owner), 256, 0, s>>>(w);
+  k_chunk_spans<<<grid(k_chunk_spans), 256, 0, s>>>(w);
   return dispatch_row(d.dim, d.bits, d.sb16, [&]<int D, int BITS, bool SB16>() -> hipError_t {
     k_partials<D><<<grid(k_partials<D>), 256, 0, s>>>(d, w, sv, grad);
     k_hot_fold<D><<<grid(k_hot_fold<D>), 256, 0, s>>>(w);

@@ -66,7 +66,7 @@ struct Plan {
   size_t o_rec, o_crow, o_tag, o_ts, o_cnt, o_G, o_desc, o_keyb, o_stats, o_err, state_bytes;
   // workspace offsets
   size_t o_kA, o_vA, o_kB, o_vB, o_ssmall, o_sst0, o_sst1, o_part, o_tcnt, o_tpre, o_uk, o_seg, o_setf, o_urow, o_utab, o_uslot,
-      o_uact, o_udest, o_nch, o_cbase, o_uvrow, o_uvu, o_partial, o_owner, o_long, o_tabf, o_src, o_ctr, ws_bytes;
+      o_uact, o_udest, o_nch, o_cbase, o_uvrow, o_uvu, o_partial, o_span, o_long, o_tabf, o_src, o_ctr, ws_bytes;
   int64_t max_partials = 0;
 };
 
@@ -167,7 +167,7 @@ int plan_config(const emb_cache_config* c, Plan* p) {
   p->o_uvu = take(4 * L);
   p->max_partials = (int64_t)(L / (embc::kSumChunk / 2) + 2);
   p->o_partial = take((size_t)p->max_partials * c->dim * 4);
-  p->o_owner = take((size_t)p->max_partials * 4);
+  p->o_span = take((size_t)p->max_partials * 8);
   p->o_long = take(4 * (L / ((size_t)embc::kSumChunk * embc::kFoldDirect) + 1));
   p->o_tabf = take(4 * (size_t)(T + 1));
   p->o_src = take(4 * L);
@@ -312,7 +312,7 @@ int emb_cache_create(const emb_cache_config* cfg, void* state, size_t state_byte
   w.uvic_u = reinterpret_cast<int32_t*>(wb + p.o_uvu);
   w.partial = reinterpret_cast<float*>(wb + p.o_partial);
   w.long_rows = reinterpret_cast<int32_t*>(wb + p.o_long);
-  w.chunk_owner = reinterpret_cast<int32_t*>(wb + p.o_owner);
+  w.chunk_span = reinterpret_cast<uint2*>(wb + p.o_span);
   w.tab_first = reinterpret_cast<int32_t*>(wb + p.o_tabf);
   w.fwd_src = reinterpret_cast<int32_t*>(wb + p.o_src);
   w.ctr = reinterpret_cast<unsigned long long*>(wb + p.o_ctr);
