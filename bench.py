@@ -25,6 +25,35 @@ from paper_2010_11305_amd import configs, workload  # noqa: E402
 
 METRIC = "pooled lookups/sec + achieved HBM GB/s (fwd+bwd+update), 1 MI355X"
 HBM_PEAK_GBS = 8000.0
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "industrial_step_hbm_counters.md")
+# sources that determine the row-update kernel's code (its HBM counters go stale when they change)
+UPDATE_KERNEL_SOURCES = ["k_update.hip", "embc_device.h", "embc_internal.h", "embc_dispatch.h", "embc_sort.h"]
+
+
+def update_kernel_digest():
+    import hashlib
+    h = hashlib.sha256()
+    for f in UPDATE_KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2010_11305_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_update_traffic():
+    """HBM bytes per k_update launch from the committed counter summary (FETCH_SIZE x 2 +
+    WRITE_SIZE x 1, see that file's calibration), or None when the summary was taken on
+    other kernel sources."""
+    try:
+        text = open(COUNTERS_FILE).read()
+    except OSError:
+        return None
+    vals = dict(line.split(":", 1) for line in text.splitlines() if line.startswith("k_update_"))
+    try:
+        if vals["k_update_source_digest"].strip() != update_kernel_digest():
+            return None
+        return float(vals["k_update_hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def describe(cfg):
@@ -64,6 +93,28 @@ def algorithmic_bytes(cfg, st, B, decay_step=False):
     if cfg["optimizer"] == "adagrad":
         bwd += 8 * U
     return fwd, bwd
+
+
+def update_kernel_bytes(cfg, st):
+    """Algorithmic bytes of the row-update kernel (k_update) for one table and one step.
+
+    It handles every unique row except the residents displaced after their own update
+    (E_h, handled with the evictions): per row it reads the row (phi from the cache
+    for a hit, rho from T for a miss) and the merged gradient (phi), reads and writes the
+    Adagrad accumulator (8), and writes the row to its slot (phi: hit or insert) or to
+    T (rho: bypass), plus tag and LRU stamp of an insert (8; 4 under LFU).
+    """
+    d = cfg["dim"]
+    phi = 4 * d
+    rho = d * cfg["bits"] // 8 + (4 if cfg["sb_fp16"] else 8)
+    U, Uh, Eh = st["unique"], st["unique_hits"], st["hit_evictions"]
+    Uins, Ubyp = st["inserts"], st["bypasses"]
+    rows = U - Eh
+    b = phi * (Uh - Eh) + rho * (Uins + Ubyp) + phi * rows
+    b += phi * (Uh - Eh) + phi * Uins + rho * Ubyp + (8 if cfg["policy"] == "lru" else 4) * Uins
+    if cfg["optimizer"] == "adagrad":
+        b += 8 * rows
+    return b
 
 
 def cpu_baseline(cfg, steps, budget_s):
@@ -164,6 +215,7 @@ def main():
     torch.cuda.synchronize()
     print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
 
+    emb.set_update_timing(True)  # HIP events around k_update, on the library's stream
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
@@ -174,6 +226,8 @@ def main():
     t_end.record()
     torch.cuda.synchronize()
     total_ms = t_start.elapsed_time(t_end)
+    upd_ms = emb.update_times(args.steps)
+    emb.set_update_timing(False)
     fwd_ms = [e[0].elapsed_time(e[1]) for e in evs]
     bwd_ms = [e[1].elapsed_time(e[2]) for e in evs]
     ms_per_step = total_ms / args.steps
@@ -181,7 +235,7 @@ def main():
     print(f"[bench] timed {args.steps} steps: {ms_per_step:.3f} ms/step", file=sys.stderr, flush=True)
 
     # algorithmic bytes from the statistics of further steps of the same stream
-    fwd_b, bwd_b, n_st = 0, 0, 0
+    fwd_b, bwd_b, upd_b, n_st = 0, 0, 0, 0
     hit_lk, all_lk = 0, 0
     for k in range(args.stats_steps):
         step(args.warmup + args.steps + k)
@@ -190,11 +244,15 @@ def main():
             f, b = algorithmic_bytes(cfg, st, B)
             fwd_b += f
             bwd_b += b
+            upd_b += update_kernel_bytes(cfg, st)
             hit_lk += st["hit_lookups"]
             all_lk += st["lookups"]
         n_st += 1
     fwd_b /= n_st
     bwd_b /= n_st
+    upd_b /= n_st
+    upd_avg = float(np.mean(upd_ms)) if len(upd_ms) else float("nan")
+    upd_gbs = upd_b / (upd_avg * 1e-3) / 1e9
     status = emb.check()
     step_bytes = fwd_b + bwd_b
     gbs = step_bytes / (ms_per_step * 1e-3) / 1e9
@@ -224,9 +282,13 @@ def main():
         "bwd_ms_p90": float(np.percentile(bwd_ms, 90)),
         "hit_rate_lookups": hit_lk / max(all_lk, 1),
         "status": status,
-        "roofline": {"bound": "hbm", "kernel": "k_forward (tag probe + gather/dequant + sum-pool)",
-                     "achieved": fwd_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": fwd_gbs / HBM_PEAK_GBS,
-                     "traffic": None},
+        "roofline": {"bound": "hbm", "kernel": "k_update (merged gradient, fetch, row-wise Adagrad, write-back)",
+                     "achieved": upd_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": upd_gbs / HBM_PEAK_GBS,
+                     "traffic": measured_update_traffic(), "kernel_ms": upd_avg,
+                     "algorithmic_bytes_per_launch": upd_b},
+        "roofline_forward": {"bound": "hbm", "kernels": "k_fwd_probe + k_fwd_gather (whole forward call)",
+                             "achieved": fwd_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                             "frac": fwd_gbs / HBM_PEAK_GBS, "algorithmic_bytes_per_call": fwd_b},
     }
     if not args.no_cpu_baseline:
         print("[bench] CPU oracle baseline ...", file=sys.stderr, flush=True)

@@ -212,6 +212,17 @@ int emb_cache_import_cache(emb_cache_t h, int32_t table, const float* rows, cons
 int emb_cache_get_step(emb_cache_t h, uint64_t* step);
 int emb_cache_set_step(emb_cache_t h, uint64_t step);
 
+/* Measurement support (not needed for training).  While enabled, every
+ * backward_update records two HIP events on its stream, around its row-update
+ * kernel (per unique row: merged gradient, fetch, optimizer, write-back to the
+ * cache or T); the events of the last 64 calls are kept.  Host-only call. */
+int emb_cache_set_update_timing(emb_cache_t h, int32_t enable);
+
+/* Durations in milliseconds of that kernel in the last n timed backward_update
+ * calls, oldest first, n = min(max, 64, calls timed since enabling) written to
+ * *n.  Waits for those events to complete. */
+int emb_cache_get_update_times(emb_cache_t h, float* ms, int32_t max, int32_t* n);
+
 /* Static string for a status code. */
 const char* emb_cache_status_string(int status);
 

@@ -127,9 +127,10 @@ hipError_t launch_reset_state(const Dev& d, hipStream_t s);
 hipError_t launch_init_uniform(const Dev& d, float lo, float hi, uint64_t init_seed, hipStream_t s);
 hipError_t launch_forward(const Dev& d, const Work& w, const int32_t* idx, int64_t L, const int32_t* off,
                           int32_t B, float* out, hipStream_t s);
+// update_events: nullptr, or two events recorded on `s` around the row-update kernel.
 hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int64_t L, const int32_t* off,
                            int32_t B, const float* grad, uint64_t step, int key_bits, bool decay,
-                           hipStream_t s);
+                           const hipEvent_t* update_events, hipStream_t s);
 
 size_t sort_status_words(int64_t n);
 constexpr size_t kSortSmallWords = 2 * kMaxPasses * 256 + 64;

@@ -687,7 +687,8 @@ __global__ __launch_bounds__(256) void k_update(Dev dv, Work w, const uint32_t* 
 
 // ---- one training step ----------------------------------------------------------------------
 hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int64_t L, const int32_t* off, int32_t B,
-                           const float* grad, uint64_t step64, int key_bits, bool decay, hipStream_t s) {
+                           const float* grad, uint64_t step64, int key_bits, bool decay,
+                           const hipEvent_t* update_events, hipStream_t s) {
   const uint32_t step = (uint32_t)step64;
   k_bwd_begin<<<1, 256, 0, s>>>(d, w.ctr, L);
   if (decay && d.cnt) k_decay<<<grid_for(d.total_rows), 256, 0, s>>>(d.cnt, d.total_rows);
@@ -718,7 +719,15 @@ hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int6
       k_policy<<<grid(k_policy), 256, 0, s>>>(d, w, step);
       k_evict<D, BITS, SB16><<<grid(k_evict<D, BITS, SB16>), 256, 0, s>>>(d, w, sv, grad, step);
     }
+    if (update_events) {
+      const hipError_t e2 = hipEventRecord(update_events[0], s);
+      if (e2 != hipSuccess) return e2;
+    }
     k_update<D, BITS, SB16><<<grid(k_update<D, BITS, SB16>), 256, 0, s>>>(d, w, sv, grad, step);
+    if (update_events) {
+      const hipError_t e2 = hipEventRecord(update_events[1], s);
+      if (e2 != hipSuccess) return e2;
+    }
     return hipGetLastError();
   });
 }

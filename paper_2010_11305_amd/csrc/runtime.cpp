@@ -186,6 +186,14 @@ struct emb_cache {
   embc::Work work;
   uint64_t step = 0;
   int key_bits = 1;
+  // measurement: event pairs around the row-update kernel of the last kTimedCalls calls
+  static constexpr int kTimedCalls = 64;
+  bool timing = false;
+  std::vector<hipEvent_t> tev;
+  uint64_t timed = 0;
+  ~emb_cache() {
+    for (hipEvent_t e : tev) (void)hipEventDestroy(e);
+  }
 };
 
 namespace {
@@ -361,9 +369,12 @@ int emb_cache_backward_update(emb_cache_t h, const int32_t* indices, int64_t num
   if ((num_indices > 0 && !indices) || !offsets || (batch > 0 && !grad_out)) return EMB_EINVAL;
   const int K = h->cfg.lfu_decay_interval;
   const bool decay = h->cfg.policy == EMB_LFU && K > 0 && h->step > 0 && h->step % (uint64_t)K == 0;
+  const hipEvent_t* tev = nullptr;
+  if (h->timing) tev = &h->tev[2 * (h->timed % emb_cache::kTimedCalls)];
   const hipError_t e = embc::launch_backward(h->dev, h->work, indices, num_indices, offsets, batch, grad_out,
-                                             h->step, h->key_bits, decay, S(stream));
+                                             h->step, h->key_bits, decay, tev, S(stream));
   if (e != hipSuccess) return EMB_EHIP;
+  if (h->timing) h->timed += 1;
   h->step += 1;
   return EMB_OK;
 }
@@ -534,6 +545,32 @@ int emb_cache_import_cache(emb_cache_t h, int32_t table, const float* rows, cons
     e = hipMemcpyAsync(h->dev.ts + td.slot_base, lru_stamp, 4 * (size_t)slots, hipMemcpyHostToDevice, s);
   if (e == hipSuccess) e = hipStreamSynchronize(s);
   return hip_status(e);
+}
+
+int emb_cache_set_update_timing(emb_cache_t h, int32_t enable) {
+  if (!h) return EMB_EINVAL;
+  if (enable && h->tev.empty()) {
+    h->tev.assign(2 * emb_cache::kTimedCalls, nullptr);
+    for (hipEvent_t& e : h->tev)
+      if (hipEventCreate(&e) != hipSuccess) return EMB_EHIP;
+  }
+  h->timing = enable != 0;
+  h->timed = 0;
+  return EMB_OK;
+}
+
+int emb_cache_get_update_times(emb_cache_t h, float* ms, int32_t max, int32_t* n) {
+  if (!h || !n || max < 0 || (max > 0 && !ms)) return EMB_EINVAL;
+  uint64_t k = h->timed < (uint64_t)emb_cache::kTimedCalls ? h->timed : (uint64_t)emb_cache::kTimedCalls;
+  if (k > (uint64_t)max) k = (uint64_t)max;
+  for (uint64_t i = 0; i < k; ++i) {
+    const uint64_t call = h->timed - k + i;
+    hipEvent_t* ev = &h->tev[2 * (call % emb_cache::kTimedCalls)];
+    if (hipEventSynchronize(ev[1]) != hipSuccess || hipEventElapsedTime(&ms[i], ev[0], ev[1]) != hipSuccess)
+      return EMB_EHIP;
+  }
+  *n = (int32_t)k;
+  return EMB_OK;
 }
 
 int emb_cache_get_step(emb_cache_t h, uint64_t* step) {

@@ -90,6 +90,8 @@ def load():
         "emb_cache_import_cache": [P, i32, P, P, P, P],
         "emb_cache_get_step": [P, c.POINTER(u64)],
         "emb_cache_set_step": [P, u64],
+        "emb_cache_set_update_timing": [P, i32],
+        "emb_cache_get_update_times": [P, P, i32, c.POINTER(i32)],
     }
     for name, args in sig.items():
         f = getattr(L, name)
@@ -247,6 +249,17 @@ class EmbCache:
     @step.setter
     def step(self, s: int):
         _check(load().emb_cache_set_step(self._h, int(s)), "set_step")
+
+    # ---- measurement ----------------------------------------------------------------------
+    def set_update_timing(self, enable: bool):
+        _check(load().emb_cache_set_update_timing(self._h, 1 if enable else 0), "set_update_timing")
+
+    def update_times(self, max_n: int = 64) -> np.ndarray:
+        """Durations (ms) of the row-update kernel in the last timed backward calls."""
+        ms = np.zeros(max_n, dtype=np.float32)
+        n = ctypes.c_int32()
+        _check(load().emb_cache_get_update_times(self._h, _np(ms), max_n, ctypes.byref(n)), "get_update_times")
+        return ms[: n.value].copy()
 
     def export_rows(self, t: int, row0: int = 0, n: int | None = None) -> dict:
         n = int(self.cfg["rows"][t]) - row0 if n is None else n

@@ -194,3 +194,18 @@ def test_determinism_and_resume(torch):
     for key in a:
         assert np.array_equal(a[key], b[key]), key
     assert np.array_equal(g1.export_cache(0)["crow"], g3.export_cache(0)["crow"])
+
+
+def test_update_timing_events(torch):
+    """The measurement events around the row-update kernel: one duration per timed call,
+    and timing does not change results."""
+    cfg = custom_cfg(batch=64)
+    log("update timing events")
+    o, g = make_pair(cfg)
+    g.set_update_timing(True)
+    for k in range(3):
+        step_both(o, g, cfg, workload.make_step(cfg, k), torch)
+    ms = g.update_times(8)
+    g.set_update_timing(False)
+    assert ms.shape == (3,) and np.all(ms > 0) and np.all(ms < 1000)
+    compare_state(o, g, cfg)
