@@ -33,8 +33,11 @@
  *   with empty ways lowest, candidates by (PV desc, row asc), the k-th candidate
  *   takes the k-th victim while strictly higher, stopping at the first failure);
  *   LRU timestamp = step counter; LFU count += occurrences, halved every
- *   `lfu_decay_interval` steps; gradient sum in chunks of 64 occurrences
- *   (each chunk left to right, then the chunk partials left to right);
+ *   `lfu_decay_interval` steps; gradient sum of a row in position order: up to
+ *   512 occurrences in chunks of 64 (each chunk left to right, then the chunk
+ *   partials left to right), more than 512 by bag blocks of 32768/d bags (the
+ *   occurrences of each block left to right, then the non-empty block partials
+ *   left to right);
  *   row-wise Adagrad G += mean(g^2) with a halving-tree sum; SR uniform from
  *   Philox4x32-10 keyed on (seed, step, table, row, col).
  */
@@ -429,7 +432,9 @@ static int cand_cmp(const void *a, const void *b) { /* PV descending, row ascend
 
 enum { ACT_HIT_STAY = 0, ACT_HIT_EVICT = 1, ACT_INSERT = 2, ACT_BYPASS = 3 };
 
-#define SUM_CHUNK 64
+#define SUM_CHUNK 64        /* occurrences per chunk of a merged-gradient sum */
+#define SUM_BLOCK_ABOVE 512 /* rows with more occurrences sum by bag blocks */
+#define BLOCK_FLOATS 32768  /* a bag block spans 32768/d bags */
 
 void orc_backward_update(orc_t *o, const int32_t *idx, int64_t n_idx, const int32_t *off, int32_t B,
                          const float *grad) {
@@ -488,14 +493,25 @@ void orc_backward_update(orc_t *o, const int32_t *idx, int64_t n_idx, const int3
     float *x = (float *)malloc(sizeof(float) * (size_t)(U * d + 1));
     float *part = (float *)malloc(sizeof(float) * (size_t)d);
 
-    /* 3. merged gradient of each unique row: chunks of 64 occurrences, each
-     *    summed left to right, then the chunk sums left to right */
+    /* 3. merged gradient of each unique row, occurrences in position order.  Up to
+     *    512 occurrences: groups of 64 consecutive occurrences (one group when there
+     *    are at most 64), each summed left to right, then the group sums left to
+     *    right.  More than 512: groups by bag block (bags [k*NB, (k+1)*NB) with
+     *    NB = 32768/d), each non-empty group summed left to right, then the group
+     *    sums left to right in block order. */
+    const int32_t NB = BLOCK_FLOATS / d;
     for (int64_t u = 0; u < U; ++u) {
       urow[u] = occ[ustart[u]].row;
       float *gu = g + u * d;
+      const int by_block = ustart[u + 1] - ustart[u] > SUM_BLOCK_ABOVE;
       int64_t first_chunk = 1;
-      for (int64_t c0 = ustart[u]; c0 < ustart[u + 1]; c0 += SUM_CHUNK) {
-        int64_t c1 = c0 + SUM_CHUNK < ustart[u + 1] ? c0 + SUM_CHUNK : ustart[u + 1];
+      for (int64_t c0 = ustart[u], c1; c0 < ustart[u + 1]; c0 = c1) {
+        if (by_block) {
+          c1 = c0 + 1;
+          while (c1 < ustart[u + 1] && occ[c1].bag / NB == occ[c0].bag / NB) ++c1;
+        } else {
+          c1 = c0 + SUM_CHUNK < ustart[u + 1] ? c0 + SUM_CHUNK : ustart[u + 1];
+        }
         const float *g0 = grad + ((int64_t)occ[c0].bag * T + t) * d;
         for (int j = 0; j < d; ++j) part[j] = g0[j];
         for (int64_t i = c0 + 1; i < c1; ++i) {

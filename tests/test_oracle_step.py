@@ -121,6 +121,59 @@ def test_merged_gradient_exact_for_hot_row():
     assert np.count_nonzero(idx == 7) > 64 * 5  # spans several chunks of the merged sum
 
 
+def test_merged_gradient_exact_for_hot_row_over_bag_blocks():
+    """d = 128: bag blocks of 32768/128 = 256 bags; a row with more than 512 lookups
+    spread over 1024 bags (four blocks).  With exactly-representable gradients the
+    merged gradient is the exact sum, however it is grouped."""
+    cfg = custom_cfg(rows=[40], dim=128, cache_fraction=1.0, assoc=64, batch=1024, lr=1.0)
+    o = oracle_from_cfg(cfg)
+    o.init_uniform()
+    x0 = effective_table(o, 0)
+    rng = np.random.default_rng(11)
+    lens = rng.integers(1, 4, size=1024)
+    off = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    idx = np.where(rng.random(off[-1]) < 0.5, 3, rng.integers(0, 40, off[-1])).astype(np.int32)
+    g = exact_grad(cfg, 0)
+    o.backward_update(idx, off, 1024, g)
+    x1 = effective_table(o, 0)
+    assert np.count_nonzero(idx == 3) > 512
+    for r in (3, int(idx[0])):
+        tot = [Fraction(0)] * 128
+        for b in range(1024):
+            n = int(np.count_nonzero(idx[off[b]:off[b + 1]] == r))
+            if n:
+                for j in range(128):
+                    tot[j] += n * Fraction(float(g[b, 0, j]))
+        for j in range(128):
+            assert x1[r, j] == round_f32(Fraction(float(x0[r, j])) - tot[j]), (r, j)
+
+
+def test_merged_gradient_grouping_of_a_row_with_many_lookups():
+    """Which grouping the merged sum of a row with more than 512 lookups uses, seen
+    through FP32 absorption.  Row 0 is looked up once in each of 600 bags, d = 128
+    (bag blocks of 256 bags: [0,256), [256,512), [512,600)); every column of the
+    output gradient is 2^24 in bag 0, -2^24 in bag 300 and 1 elsewhere.
+      by blocks:   2^24 absorbs the 255 ones of block 0 (2^24 + 1 rounds to 2^24);
+                   block 1 is (44 - 2^24) + 211 = 255 - 2^24 exactly; block 2 is 88;
+                   fold: 2^24 + (255 - 2^24) = 255, then 255 + 88 = 343.
+      sequential:  2^24 absorbs 299 ones, -2^24 gives 0, then 211 + 88 = 299.
+      64-chunks:   2^24 (+63 lost), +192, + (44 - 2^24 + 19), +192, +64, +24 = 535.
+    So the row's new value is x0 - 343 (SGD, lr 1, FP32 cache row)."""
+    cfg = custom_cfg(rows=[8], dim=128, cache_fraction=1.0, assoc=8, batch=600, lr=1.0)
+    o = oracle_from_cfg(cfg)
+    o.init_uniform()
+    x0 = effective_table(o, 0)
+    off = np.arange(601, dtype=np.int32)
+    idx = np.zeros(600, dtype=np.int32)
+    g = np.ones((600, 1, 128), dtype=np.float32)
+    g[0] = 2.0**24
+    g[300] = -(2.0**24)
+    o.backward_update(idx, off, 600, g)
+    x1 = effective_table(o, 0)
+    for j in range(128):
+        assert x1[0, j] == round_f32(Fraction(float(x0[0, j])) - 343), j
+
+
 # ---- P9: full-coverage cache = plain FP32 training ----------------------------------------------
 def _full_coverage_cfg(**kw):
     # N = 1000, 1.024 * 1000 = 1024 slots in 32 sets of 32 ways; at most 32 rows map to a set
