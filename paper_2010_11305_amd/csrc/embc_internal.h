@@ -21,8 +21,12 @@
 namespace embc {
 
 constexpr uint32_t kKeyInvalid = 0xFFFFFFFFu;  // sort key of a skipped lookup (sorts last)
-constexpr int kSumChunk = 64;                  // occurrences per chunk of a merged-gradient sum
-constexpr uint32_t kFoldDirect = 8;            // chunk sums a row's consumer folds itself (more: k_hot_fold)
+// Merged gradient of a row (its lookups in position order): up to kBlockAbove lookups
+// in chunks of kSumChunk consecutive lookups; more by bag blocks of kBlockFloats/d
+// bags (one block of FP32 gradient rows is 128 KiB, staged in LDS once for all rows).
+constexpr int kSumChunk = 64;
+constexpr uint32_t kBlockAbove = 512;
+constexpr int kBlockFloats = 32768;
 constexpr int kMaxAssoc = 64;
 
 enum : int32_t { kActHitStay = 0, kActHitEvict = 1, kActInsert = 2, kActBypass = 3 };
@@ -100,7 +104,12 @@ struct Work {
   int32_t* uvic_u;       // [L] insert: unique index of that row if it was updated this step, else -1
   float* partial;        // [L/32 + 2][dim] chunk sums
   uint2* chunk_span;     // [L/32 + 2] occurrences [x, y) of the sorted stream summed by each chunk
-  int32_t* long_rows;    // [L/(64*kFoldDirect) + 1] unique rows with more than kFoldDirect chunk sums
+  uint32_t* ubig;        // [L] 1 for a row with more than kBlockAbove lookups, then its exclusive prefix
+  int32_t* big_rows;     // [max_big] unique row of each such row ("big row"), in unique-row order
+  uint32_t* bbound;      // [max_big][max_nblk + 1] first occurrence of each bag block of a big row
+  float* bpart;          // [max_big][max_nblk][dim] block sums of the big rows
+  int64_t max_big;
+  int32_t max_nblk;
   int32_t* tab_first;    // [T+1] first unique row of each table (tab_first[T] = number of unique rows)
   int32_t* fwd_src;      // [L] forward: cache slot of each lookup, -2-row for a miss, -1 if skipped
   unsigned long long* ctr;  // counters, see kC*
@@ -117,7 +126,7 @@ enum : int {
   kCInserts = 5,
   kCScanTotal = 6,  // scratch total of the last scan
   kCBadOffsets = 7, // offsets of this step failed validation
-  kCLongRows = 8,   // rows whose chunk sums are folded by k_hot_fold
+  kCBig = 8,        // big rows
   kNCounters = 16
 };
 

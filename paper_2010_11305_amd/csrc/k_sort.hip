@@ -346,8 +346,8 @@ hipError_t sort_pairs(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32_t* vB, in
 // ---- lookups -> sort pairs ----------------------------------------------------------------
 // One wave per 64 consecutive bags (global bag = t*B + b); each position of those
 // bags finds its bag by a binary search over the 64 lane-held bag starts.
-// key: set-major row key (kKeyInvalid for an out-of-range row); value: index of
-// the bag's gradient row in grad_out [B][T][d], i.e. b*T + t.
+// key: set-major row key (kKeyInvalid for an out-of-range row); value: the bag b
+// within its table (its gradient row in grad_out [B][T][d] is b*T + t).
 __global__ __launch_bounds__(256) void k_expand(Dev dv, const int32_t* __restrict__ idx, int64_t L,
                                                 const int32_t* __restrict__ off, int32_t B,
                                                 uint32_t* __restrict__ keys, uint32_t* __restrict__ vals,
@@ -412,7 +412,7 @@ __global__ __launch_bounds__(256) void k_expand(Dev dv, const int32_t* __restric
         atomicOr(dv.err, kErrIndex);
       }
       keys[p] = key;
-      vals[p] = (uint32_t)((int64_t)b * dv.T + t);
+      vals[p] = (uint32_t)b;
     }
   }
   // lookups of the wave's first table: one atomic per wave

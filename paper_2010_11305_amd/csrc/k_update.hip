@@ -2,12 +2,12 @@
 //
 // After the sort (k_sort.hip) the lookups are grouped by row, the rows by set:
 //   k_probe     per unique row: residency (slot or miss), LRU stamp / LFU count update
-//   k_partials  chunk sums (64 lookups each) of the merged gradient of rows with > 64 lookups
+//   k_partials  chunk sums (64 lookups each) of the merged gradient of rows with 65..512 lookups
 //   k_policy    per touched set, one wave (one lane per way): which missed rows enter the
 //               cache and which resident each of them displaces (decisions only)
-//   k_hot_fold  per row with > kFoldDirect chunk sums, one workgroup: its chunk sums folded
-//               left to right through LDS; the result replaces the row's first chunk sum
-//               (rows with fewer chunks are folded by the kernel that consumes them)
+//   k_block_partials  per (table, bag block): the block's gradient rows staged in LDS
+//               once, the block sums of every row with > 512 lookups; k_block_fold
+//               folds them per row (chunk sums are folded by the kernel that uses them)
 //   k_evict     per insert that displaces a resident: the resident's FP32 row (updated
 //               first if it was itself updated this step, LFU) is quantized into T
 //   k_update    per unique row: merged gradient, fetch, optimizer, then the cache way
@@ -42,6 +42,13 @@ __device__ __forceinline__ void wave_stat_add(unsigned long long* stats, int t, 
 }
 
 __global__ void k_chunks_total(unsigned long long* ctr) { ctr[kCChunks] = ctr[kCScanTotal] & 0xFFFFFFFFull; }
+
+// After the scan of the big-row flags: their total, also as ubig[nU].
+__global__ void k_big_total(Work w) {
+  const unsigned long long nb = w.ctr[kCScanTotal] & 0xFFFFFFFFull;
+  w.ctr[kCBig] = nb;
+  w.ubig[w.ctr[kCUnique]] = (uint32_t)nb;
+}
 
 __global__ void k_bwd_begin(Dev dv, unsigned long long* ctr, int64_t L) {
   for (int i = threadIdx.x; i < dv.T; i += blockDim.x) {
@@ -85,7 +92,10 @@ __global__ __launch_bounds__(256) void k_probe(Dev dv, Work w, uint32_t step) {
       w.utab[u] = t;
       w.uslot[u] = slot;
       w.uact[u] = slot >= 0 ? kActHitStay : kActBypass;
-      w.nch[u] = count > (uint32_t)kSumChunk ? (count + kSumChunk - 1) / kSumChunk : 0u;
+      // chunks of kSumChunk lookups for 64 < count <= kBlockAbove; bag blocks above
+      const bool big = count > kBlockAbove;
+      w.nch[u] = count > (uint32_t)kSumChunk && !big ? (count + kSumChunk - 1) / kSumChunk : 0u;
+      w.ubig[u] = big ? 1u : 0u;
       if (dv.policy == 0) {
         if (slot >= 0) dv.ts[slot] = (int32_t)step;
       } else {
@@ -100,30 +110,49 @@ __global__ __launch_bounds__(256) void k_probe(Dev dv, Work w, uint32_t step) {
 }
 
 // ---- merged gradient ----------------------------------------------------------------------
-// Left-to-right FP32 sum of the gradient rows of occurrences [i0, i1) of the sorted
-// stream (i0 < i1), seeded with the first.  Lane j of the group preloads the row
-// index of occurrence j of each chunk of LPR occurrences (for the first chunk the
-// caller may pass them in, myv0); U rows are loaded before they are added in order.
+// R9 order: a row's lookups in position order; up to kSumChunk of them summed left to
+// right (seeded with the first); up to kBlockAbove in chunks of kSumChunk consecutive
+// lookups (k_partials), the chunk sums folded left to right; more by bag blocks of
+// NB = kBlockFloats/d bags (k_block_partials), the non-empty block sums folded left
+// to right.  The sort's value of a lookup is its bag b within the table.
+
+// Gradient rows of table t: grad_out is [B][T][d], so bag b's row is row b*T + t (an
+// index below 2^32: B*T < 2^32 is checked when the handle is created).
 template <int D>
-__device__ __forceinline__ void sum_occ(const uint32_t* __restrict__ sval, int64_t i0, int64_t i1,
-                                        const float* __restrict__ grad, int g, float (&acc)[8],
-                                        uint32_t myv0 = 0u, bool have0 = false) {
+struct GradRows {
+  const float* grad;
+  uint32_t T, t;
+  __device__ const float* row(uint32_t b) const { return grad + (int64_t)(b * T + t) * D; }
+};
+
+template <int D>
+__device__ __forceinline__ GradRows<D> grad_rows(const float* grad, int t, int T) {
+  return GradRows<D>{grad, (uint32_t)T, (uint32_t)t};
+}
+
+// Left-to-right sum of the gradient rows of occurrences [i0, i1) of the sorted
+// stream (i0 < i1), seeded with the first.  Lane j of the group preloads the bag of
+// occurrence j of each run of LPR occurrences (for the first run the caller may pass
+// them in, myv0); U rows are loaded before they are added in order.
+template <int D>
+__device__ __forceinline__ void sum_occ(const uint32_t* __restrict__ sval, int64_t i0, int64_t i1, GradRows<D> gr,
+                                        int g, float (&acc)[8], uint32_t myv0 = 0u, bool have0 = false) {
   constexpr int LPR = Geo<D>::LPR, CPL = 8, U = kUnroll;
   bool first = true;
   for (int64_t ic = i0; ic < i1; ic += LPR) {
     const int n = (int)min<int64_t>(LPR, i1 - ic);
-    // the first chunk's values may have been loaded by the caller (have0)
+    // the first run's values may have been loaded by the caller (have0)
     const uint32_t myv = (have0 && ic == i0) ? myv0 : (g < n ? sval[ic + g] : 0u);
     int j = 0;
     if (first) {
-      load_frow8(grad + (int64_t)__shfl(myv, 0, LPR) * D, g, acc);
+      load_frow8(gr.row(__shfl(myv, 0, LPR)), g, acc);
       first = false;
       j = 1;
     }
     for (; j + U <= n; j += U) {
       float x[U][CPL];
 #pragma unroll
-      for (int q = 0; q < U; ++q) load_frow8(grad + (int64_t)__shfl(myv, j + q, LPR) * D, g, x[q]);
+      for (int q = 0; q < U; ++q) load_frow8(gr.row(__shfl(myv, j + q, LPR)), g, x[q]);
 #pragma unroll
       for (int q = 0; q < U; ++q)
 #pragma unroll
@@ -131,7 +160,7 @@ __device__ __forceinline__ void sum_occ(const uint32_t* __restrict__ sval, int64
     }
     for (; j < n; ++j) {
       float x[CPL];
-      load_frow8(grad + (int64_t)__shfl(myv, j, LPR) * D, g, x);
+      load_frow8(gr.row(__shfl(myv, j, LPR)), g, x);
 #pragma unroll
       for (int k = 0; k < CPL; ++k) acc[k] = acc[k] + x[k];
     }
@@ -141,17 +170,17 @@ __device__ __forceinline__ void sum_occ(const uint32_t* __restrict__ sval, int64
 constexpr int kChunkUnroll = 4;  // gradient rows in flight per row group in a chunk sum
 
 // Sum of one chunk (occurrences [i0, i1) of the sorted stream, 0 < i1 - i0 <= 64),
-// left to right, seeded with the first.  The occurrence values of the next LPR
-// occurrences are loaded while the current ones are summed, U gradient rows are in
-// flight at a time, and a row listed more than once in one bag (adjacent occurrences
-// with the same gradient row) adds the row already in registers instead of loading it
-// again (same operands, same sums).
+// left to right, seeded with the first.  The bags of the next LPR occurrences are
+// loaded while the current ones are summed, U gradient rows are in flight at a
+// time, and a row listed more than once in one bag (adjacent occurrences with the
+// same bag) adds the row already in registers instead of loading it again (same
+// operands, same sums).
 template <int D>
-__device__ __forceinline__ void chunk_sum(const uint32_t* __restrict__ sval, int64_t i0, int64_t i1,
-                                          const float* __restrict__ grad, int g, float (&acc)[8]) {
+__device__ __forceinline__ void chunk_sum(const uint32_t* __restrict__ sval, int64_t i0, int64_t i1, GradRows<D> gr,
+                                          int g, float (&acc)[8]) {
   constexpr int LPR = Geo<D>::LPR, CPL = 8, U = kChunkUnroll;
   bool first = true;
-  uint32_t pv = 0xFFFFFFFFu;  // gradient row of the last occurrence added (none yet)
+  uint32_t pv = 0xFFFFFFFFu;  // bag of the last occurrence added (none yet)
   float last[CPL];
 #pragma unroll
   for (int k = 0; k < CPL; ++k) last[k] = 0.0f;
@@ -168,7 +197,7 @@ __device__ __forceinline__ void chunk_sum(const uint32_t* __restrict__ sval, int
       for (int q = 0; q < U; ++q) {
         v[q] = __shfl(myv, j + q, LPR);
         fresh[q] = j + q < n && v[q] != (q == 0 ? pv : v[q - 1]);
-        if (fresh[q]) load_frow8(grad + (int64_t)v[q] * D, g, x[q]);
+        if (fresh[q]) load_frow8(gr.row(v[q]), g, x[q]);
       }
 #pragma unroll
       for (int q = 0; q < U; ++q) {
@@ -219,72 +248,223 @@ __device__ __forceinline__ void fold_chunks(const float* __restrict__ partial, i
   }
 }
 
-// Merged gradient of unique row u from its lookups (<= 64), its chunk sums (<=
-// kFoldDirect of them) or the fold of its chunk sums left by k_hot_fold in its
-// first chunk slot.
+// Left-to-right fold of the non-empty block sums of big row h (blocks 0 .. nblk-1),
+// seeded with the first; U blocks (bounds and sums) are loaded at a time.  The sum
+// slot of an empty block holds no value and is not added.
 template <int D>
-__device__ __forceinline__ void merged_grad(const Work& w, const uint32_t* __restrict__ sval,
-                                            const float* __restrict__ grad, int64_t u, int g, float (&acc)[8]) {
-  const uint32_t n = w.nch[u];
-  if (n == 0) sum_occ<D>(sval, w.seg[u], w.seg[u + 1], grad, g, acc);
-  else if (n <= kFoldDirect) fold_chunks<D>(w.partial, w.chunk_base[u], n, g, acc);
-  else load_frow8(w.partial + (int64_t)w.chunk_base[u] * D, g, acc);
+__device__ __forceinline__ void fold_blocks(const Work& w, int64_t h, int nblk, int g, float (&acc)[8]) {
+  constexpr int U = 4;
+  const uint32_t* bb = w.bbound + h * (int64_t)(w.max_nblk + 1);
+  const float* bp = w.bpart + h * (int64_t)w.max_nblk * D;
+  bool first = true;
+  uint32_t prev = bb[0];
+  for (int k0 = 0; k0 < nblk; k0 += U) {
+    uint32_t nx[U];
+    float x[U][8];
+#pragma unroll
+    for (int q = 0; q < U; ++q) {
+      const int k = min(k0 + q, nblk - 1);
+      nx[q] = bb[k + 1];
+      load_frow8(bp + (int64_t)k * D, g, x[q]);
+    }
+#pragma unroll
+    for (int q = 0; q < U; ++q) {
+      if (k0 + q < nblk && nx[q] > prev) {
+        if (first) {
+#pragma unroll
+          for (int k = 0; k < 8; ++k) acc[k] = x[q][k];
+          first = false;
+        } else {
+#pragma unroll
+          for (int k = 0; k < 8; ++k) acc[k] = acc[k] + x[q][k];
+        }
+      }
+      if (k0 + q < nblk) prev = nx[q];
+    }
+  }
 }
 
-// Fold of the chunk sums of each row with more than kFoldDirect of them: acc = p0 +
-// p1 + ... left to right, per column, into the row's first chunk slot.  One workgroup
-// per row (from the list k_chunk_spans builds): all threads stage R chunk sums in LDS,
-// load the next R into registers, and one thread per column folds the staged ones.
+// Fold of the block sums of every big row (one row group per row), left in the
+// row's first block slot.
 template <int D>
-__global__ __launch_bounds__(256) void k_hot_fold(Work w) {
-  constexpr int R = 8192 / D < 256 ? 8192 / D : 256;  // chunk rows per LDS round (32 KiB)
-  constexpr int PER = R * D / 4 / 256;                 // float4 per thread and round
-  __shared__ float4 stage[R * D / 4];
-  const int64_t nl = (int64_t)w.ctr[kCLongRows];
-  const int tid = threadIdx.x;
-  for (int64_t h = blockIdx.x; h < nl; h += gridDim.x) {
-    const int64_t u = w.long_rows[h];
-    const int64_t c0 = w.chunk_base[u];
-    const int64_t nch = w.nch[u];
-    const float4* src = reinterpret_cast<const float4*>(w.partial + c0 * D);
-    const int64_t n4 = nch * (D / 4);
-    // loads past the row's last chunk sum re-read its last element (kept branch-free,
-    // so that all PER loads are in flight together); those staged values are not folded
-    float nxt[PER][4];
-    const auto fetch = [&](int64_t first) {
-#pragma unroll
-      for (int k = 0; k < PER; ++k) {
-        const float4 v = src[min<int64_t>(first + tid + k * 256, n4 - 1)];
-        nxt[k][0] = v.x; nxt[k][1] = v.y; nxt[k][2] = v.z; nxt[k][3] = v.w;
+__global__ __launch_bounds__(256) void k_block_fold(Work w, int nblk) {
+  constexpr int LPR = Geo<D>::LPR, GPB = 256 / LPR;
+  const int g = threadIdx.x & (LPR - 1);
+  const int64_t nbig = (int64_t)w.ctr[kCBig];
+  for (int64_t h = (int64_t)blockIdx.x * GPB + threadIdx.x / LPR; h < nbig; h += (int64_t)gridDim.x * GPB) {
+    float acc[8];
+    fold_blocks<D>(w, h, nblk, g, acc);
+    store_frow8(w.bpart + h * (int64_t)w.max_nblk * D, g, acc);
+  }
+}
+
+// Merged gradient of unique row u (occurrences [s0, s1) of the sorted stream).
+template <int D>
+__device__ __forceinline__ void merged_grad(const Work& w, const uint32_t* __restrict__ sval, GradRows<D> gr,
+                                            int64_t u, int g, float (&acc)[8]) {
+  const uint32_t s0 = w.seg[u], s1 = w.seg[u + 1];
+  if (s1 - s0 > kBlockAbove) load_frow8(w.bpart + (int64_t)w.ubig[u] * w.max_nblk * D, g, acc);
+  else if (w.nch[u] > 0) fold_chunks<D>(w.partial, w.chunk_base[u], w.nch[u], g, acc);
+  else sum_occ<D>(sval, s0, s1, gr, g, acc);
+}
+
+// bbound[h][k] = first occurrence of big row h whose bag lies in block k or after
+// (k = 0 .. nblk; bbound[h][nblk] = the end of its occurrences): one thread per
+// (row, block) binary-searches the row's occurrences, whose bags ascend.
+__global__ __launch_bounds__(256) void k_block_bounds(Work w, const uint32_t* __restrict__ sval, int nb_shift,
+                                                      int nblk) {
+  const int64_t nbig = (int64_t)w.ctr[kCBig];
+  const int64_t n = nbig * (nblk + 1);
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += stride) {
+    const int64_t h = e / (nblk + 1);
+    const int k = (int)(e - h * (nblk + 1));
+    const int64_t u = w.big_rows[h];
+    uint32_t a = w.seg[u], b = w.seg[u + 1];  // first occurrence with bag >= k*NB lies in [a, b]
+    if (k < nblk) {
+      const uint32_t key = (uint32_t)k << nb_shift;
+      while (a < b) {
+        const uint32_t m = a + (b - a) / 2;
+        if (sval[m] < key) a = m + 1; else b = m;
       }
-    };
-    fetch(0);
-    float acc = 0.0f;
-    for (int64_t r0 = 0; r0 < nch; r0 += R) {
-      const int rn = (int)min<int64_t>(R, nch - r0);
-      __syncthreads();  // the previous round's fold is done with `stage`
+    } else {
+      a = b;
+    }
+    w.bbound[h * (int64_t)(w.max_nblk + 1) + k] = a;
+  }
+}
+
+// Block sums of the big rows: per (table t, bag block k), the gradient rows of the
+// block's NB bags are staged in LDS (128 KiB) once; then one group of GL = min(64, d)
+// lanes per big row of t (CL = d/GL columns per lane; rows taken longest first) sums
+// the row's occurrences in the block left to right (seeded with the first).  The bags of 4*GL occurrences are
+// loaded at a time (4 per lane) and U staged rows are read at a time.
+// Tables split over the XCDs.
+constexpr int kBlockThreads = 1024;
+
+template <int D>
+__global__ __launch_bounds__(kBlockThreads) void k_block_partials(Dev dv, Work w, const uint32_t* __restrict__ sval,
+                                                                  const float* __restrict__ grad, int32_t B,
+                                                                  int nblk) {
+  constexpr int NB = kBlockFloats / D;
+  constexpr int GL = D < 64 ? D : 64;  // lanes per row group
+  constexpr int CL = D / GL;           // columns per lane (1, 2 or 4)
+  constexpr int GPB = kBlockThreads / GL;
+  constexpr int U = 16;
+  constexpr int PER = kBlockFloats / 4 / kBlockThreads;  // float4 staged per thread
+  __shared__ float4 stage[kBlockFloats / 4];
+  __shared__ uint32_t lrow[kBlockThreads], lr0[kBlockThreads], lr1[kBlockThreads], cnt_s[4];
+  const float* sf = reinterpret_cast<const float*>(stage);
+  const int l = threadIdx.x & (GL - 1);
+  const XcdSplit xs(dv.T);
+  for (int seg = xs.xcd; seg < xs.segments(dv.T); seg += kXcds) {
+    const int t = seg / xs.parts;
+    const int64_t h0 = w.ubig[w.tab_first[t]], h1 = w.ubig[w.tab_first[t + 1]];
+    if (h0 == h1) continue;
+    int64_t klo, khi;
+    part_range(0, nblk, seg % xs.parts, xs.parts, klo, khi);
+    for (int64_t k = klo + xs.unit; k < khi; k += xs.units) {
+      const int64_t bag0 = k * NB;
+      const int nrows = (int)min<int64_t>(NB, (int64_t)B - bag0);
+      __syncthreads();  // the previous block's sums are done with `stage`
+      {
+        float4 v[PER];
 #pragma unroll
-      for (int k = 0; k < PER; ++k) stage[tid + k * 256] = make_float4(nxt[k][0], nxt[k][1], nxt[k][2], nxt[k][3]);
+        for (int q = 0; q < PER; ++q) {
+          const int i = q * kBlockThreads + threadIdx.x;
+          const int r = min(i / (D / 4), nrows - 1);  // rows past the last bag re-read it (not used)
+          v[q] = reinterpret_cast<const float4*>(grad + ((bag0 + r) * dv.T + t) * D)[i % (D / 4)];
+        }
+#pragma unroll
+        for (int q = 0; q < PER; ++q) stage[q * kBlockThreads + threadIdx.x] = v[q];
+      }
       __syncthreads();
-      fetch((r0 + R) * (D / 4));
-      if (tid < D) {
-        const float* st = reinterpret_cast<const float*>(stage) + tid;
-        int r = 0;
-        if (r0 == 0) {
-          acc = st[0];
-          r = 1;
+      // the table's big rows, kBlockThreads at a time: their ranges in this block are
+      // listed in LDS with the rows of more than 4*GL occurrences first, and the row
+      // groups take list entries in order (the longest sums start first)
+      for (int64_t hc = h0; hc < h1; hc += kBlockThreads) {
+        const int nr = (int)min<int64_t>(kBlockThreads, h1 - hc);
+        if (threadIdx.x == 0) {
+          cnt_s[0] = 0;  // rows with more than 4*GL occurrences in the block
+          cnt_s[1] = 0;  // list positions taken by those rows
+          cnt_s[2] = 0;  // list positions taken by the others (after them)
+          cnt_s[3] = 0;  // next list entry for a row group
         }
-        for (; r + 8 <= rn; r += 8) {
-          float v[8];
-#pragma unroll
-          for (int k = 0; k < 8; ++k) v[k] = st[(r + k) * D];
-#pragma unroll
-          for (int k = 0; k < 8; ++k) acc = acc + v[k];
+        __syncthreads();
+        uint32_t r0 = 0, r1 = 0;
+        bool heavy = false;
+        if ((int)threadIdx.x < nr) {
+          const uint32_t* bb = w.bbound + (hc + threadIdx.x) * (int64_t)(w.max_nblk + 1);
+          r0 = bb[k];
+          r1 = bb[k + 1];
+          heavy = r1 - r0 > 4u * GL;
+          if (heavy) atomicAdd(&cnt_s[0], 1u);
         }
-        for (; r < rn; ++r) acc = acc + st[r * D];
+        __syncthreads();
+        if ((int)threadIdx.x < nr) {
+          const uint32_t pos = heavy ? atomicAdd(&cnt_s[1], 1u) : cnt_s[0] + atomicAdd(&cnt_s[2], 1u);
+          lrow[pos] = (uint32_t)threadIdx.x;
+          lr0[pos] = r0;
+          lr1[pos] = r1;
+        }
+        __syncthreads();
+        for (;;) {
+          uint32_t e = 0;
+          if (l == 0) e = atomicAdd(&cnt_s[3], 1u);
+          e = __shfl(e, 0, GL);
+          if ((int)e >= nr) break;
+          const int64_t h = hc + lrow[e];
+          const uint32_t i0 = lr0[e], i1 = lr1[e];
+          if (i0 >= i1) continue;
+          // the sum starts from -0, the identity of IEEE addition: adding the first
+          // term gives exactly that term, as in the seeded left-to-right sum
+          float acc[CL];
+#pragma unroll
+          for (int c = 0; c < CL; ++c) acc[c] = -0.0f;
+          // runs of 4*GL occurrences: lane l holds the bags (relative to the block) of
+          // occurrences 4l .. 4l+3 of the run; occurrence j of the run is component j%4
+          // of lane j/4.  Every occurrence in [i0, i1) lies in the block; indices past
+          // i1 re-read the last one (a bag of the block, not added).
+          uint32_t rnext[4];  // the next run's bags, loaded one run ahead
+#pragma unroll
+          for (int c = 0; c < 4; ++c) rnext[c] = sval[min(i0 + 4 * l + c, i1 - 1)];
+          for (uint32_t ic = i0; ic < i1; ic += 4 * GL) {
+            const int n = min(4 * GL, (int)(i1 - ic));
+            uint32_t rv[4];
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+              rv[c] = rnext[c] - (uint32_t)bag0;
+              rnext[c] = sval[min(ic + 4 * GL + 4 * l + c, i1 - 1)];
+            }
+            const auto batch = [&](int j, int m) {  // occurrences j .. j+m-1 of the run, m <= U
+              float x[U][CL];
+#pragma unroll
+              for (int q = 0; q < U; ++q) {
+                // U is a multiple of 4 and j of U: the component is static
+                uint32_t v;
+                if constexpr (GL == 64) v = __builtin_amdgcn_readlane(rv[q % 4], (j + q) / 4);
+                else v = __shfl(rv[q % 4], (j + q) / 4, GL);
+                const float* r = sf + (size_t)v * D + l * CL;
+#pragma unroll
+                for (int c = 0; c < CL; ++c) x[q][c] = r[c];
+              }
+#pragma unroll
+              for (int q = 0; q < U; ++q)
+                if (q < m)
+#pragma unroll
+                  for (int c = 0; c < CL; ++c) acc[c] = acc[c] + x[q][c];
+            };
+            int j = 0;
+            for (; j + U <= n; j += U) batch(j, U);  // full batches: no per-term test
+            if (j < n) batch(j, n - j);
+          }
+          float* o = w.bpart + (h * (int64_t)w.max_nblk + k) * D + l * CL;
+#pragma unroll
+          for (int c = 0; c < CL; ++c) o[c] = acc[c];
+        }
+        __syncthreads();  // every group is done with the list before it is rebuilt
       }
     }
-    if (tid < D) w.partial[c0 * D + tid] = acc;
   }
 }
 
@@ -307,21 +487,21 @@ __global__ void k_tab_first(Work w, int T) {
   }
 }
 
-// chunk_span[c] = occurrences [x, y) of the sorted stream that chunk c sums; rows with
-// more than kFoldDirect chunks are listed for k_hot_fold (in any order).
+// chunk_span[c] = occurrences [x, y) of the sorted stream that chunk c sums, and
+// big_rows[h] = the unique row of big row h (ubig holds the big rows' prefix count).
 __global__ __launch_bounds__(256) void k_chunk_spans(Work w) {
   const int64_t nU = (int64_t)w.ctr[kCUnique];
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < nU; u += stride) {
     const uint32_t n = w.nch[u];
+    const uint32_t s0 = w.seg[u], s1 = w.seg[u + 1];
+    if (s1 - s0 > kBlockAbove) w.big_rows[w.ubig[u]] = (int32_t)u;
     if (n == 0) continue;
     const int64_t c0 = w.chunk_base[u];
-    const uint32_t s0 = w.seg[u], s1 = w.seg[u + 1];
     for (uint32_t j = 0; j < n; ++j) {
       const uint32_t a = s0 + j * (uint32_t)kSumChunk;
       w.chunk_span[c0 + j] = make_uint2(a, min(a + (uint32_t)kSumChunk, s1));
     }
-    if (n > kFoldDirect) w.long_rows[atomicAdd(&w.ctr[kCLongRows], 1ull)] = (int32_t)u;
   }
 }
 
@@ -345,13 +525,14 @@ __global__ __launch_bounds__(256) void k_partials(Dev dv, Work w, const uint32_t
     int64_t clo, chi;
     part_range(clo_t, chi_t, seg % xs.parts, xs.parts, clo, chi);
     if (clo + gx >= chi) continue;
+    const GradRows gr = grad_rows<D>(grad, t, dv.T);
     // the next chunk's span is loaded one chunk ahead (clamped index, unconditional load)
     uint2 next = w.chunk_span[clo + gx];
     for (int64_t c = clo + gx; c < chi; c += gstride) {
       const uint2 sp = next;
       next = w.chunk_span[min<int64_t>(c + gstride, chi - 1)];
       float acc[8];
-      chunk_sum<D>(sval, sp.x, sp.y, grad, g, acc);
+      chunk_sum<D>(sval, sp.x, sp.y, gr, g, acc);
       store_frow8(w.partial + c * D, g, acc);
     }
   }
@@ -593,7 +774,7 @@ __global__ __launch_bounds__(256) void k_evict(Dev dv, Work w, const uint32_t* _
         // the displaced resident was updated this step (LFU): its new value goes to T
         const float Gv = load_G(dv, vgrow);
         float gv[8];
-        merged_grad<D>(w, sval, grad, vu, g, gv);
+        merged_grad<D>(w, sval, grad_rows<D>(grad, t, dv.T), vu, g, gv);
         apply_optimizer<D>(dv, xv, gv, vgrow, g, Gv);
       }
       quantize_store<D, BITS, SB16>(xv, g, dv.rec + vgrow * RB, sr, dv.seed, step, (uint32_t)t, (uint32_t)vrow);
@@ -637,6 +818,7 @@ __global__ __launch_bounds__(256) void k_update(Dev dv, Work w, const uint32_t* 
     table_rows(w, t, tlo, thi);
     part_range(tlo, thi, seg % xs.parts, xs.parts, lo, hi);
     const TableDesc td = dv.desc[t];
+    const GradRows gtab = grad_rows<D>(grad, t, dv.T);
     if (lo + gx >= hi) continue;
     RowMeta next = load_meta(w, lo + gx);
     for (int64_t u = lo + gx; u < hi; u += gstride) {
@@ -649,7 +831,8 @@ __global__ __launch_bounds__(256) void k_update(Dev dv, Work w, const uint32_t* 
       uint8_t* rec = dv.rec + grow * RB;
       const bool hit = m.act == kActHitStay;
       // first level of loads: the first occurrence values, the row, its accumulator
-      const uint32_t n0 = m.nch == 0 ? min<uint32_t>((uint32_t)LPR, m.s1 - m.s0) : 0u;
+      const bool big = m.s1 - m.s0 > kBlockAbove;
+      const uint32_t n0 = m.nch == 0 && !big ? min<uint32_t>((uint32_t)LPR, m.s1 - m.s0) : 0u;
       const uint32_t myv0 = (uint32_t)g < n0 ? sval[m.s0 + g] : 0u;
       float x[8], gr[8];
       CodeWords<BITS> cw;
@@ -661,9 +844,9 @@ __global__ __launch_bounds__(256) void k_update(Dev dv, Work w, const uint32_t* 
         sbw = load_sb_words<D, BITS, SB16>(rec);
       }
       const float G_old = load_G(dv, grow);
-      if (m.nch == 0) sum_occ<D>(sval, m.s0, m.s1, grad, g, gr, myv0, true);
-      else if (m.nch <= kFoldDirect) fold_chunks<D>(w.partial, m.cb, m.nch, g, gr);
-      else load_frow8(w.partial + (int64_t)m.cb * D, g, gr);
+      if (big) load_frow8(w.bpart + (int64_t)w.ubig[u] * w.max_nblk * D, g, gr);
+      else if (m.nch > 0) fold_chunks<D>(w.partial, m.cb, m.nch, g, gr);
+      else sum_occ<D>(sval, m.s0, m.s1, gtab, g, gr, myv0, true);
       if (!hit) {
         float sc, bi;
         decode_sb<SB16>(sbw, sc, bi);
@@ -711,10 +894,23 @@ hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int6
                                reinterpret_cast<uint32_t*>(w.ctr + kCScanTotal), s);
   if (e != hipSuccess) return e;
   k_chunks_total<<<1, 1, 0, s>>>(w.ctr);
+  e = scan_exclusive<uint32_t>(w.ubig, w.ubig, L, w.ctr + kCUnique, reinterpret_cast<uint32_t*>(w.part),
+                               reinterpret_cast<uint32_t*>(w.ctr + kCScanTotal), s);
+  if (e != hipSuccess) return e;
+  k_big_total<<<1, 1, 0, s>>>(w);
   k_chunk_spans<<<grid(k_chunk_spans), 256, 0, s>>>(w);
+  // bag blocks of NB = kBlockFloats/d bags (a power of two) for the big rows
+  const int nb_shift = __builtin_ctz((unsigned)(kBlockFloats / d.dim));
+  const int nblk = (int)(((int64_t)B + (kBlockFloats / d.dim) - 1) / (kBlockFloats / d.dim));
+  if (nblk > w.max_nblk) return hipErrorInvalidValue;
+  if (nblk > 0) k_block_bounds<<<grid(k_block_bounds), 256, 0, s>>>(w, sv, nb_shift, nblk);
   return dispatch_row(d.dim, d.bits, d.sb16, [&]<int D, int BITS, bool SB16>() -> hipError_t {
     k_partials<D><<<grid(k_partials<D>), 256, 0, s>>>(d, w, sv, grad);
-    k_hot_fold<D><<<grid(k_hot_fold<D>), 256, 0, s>>>(w);
+    if (nblk > 0) {
+      k_block_partials<D><<<resident_grid(reinterpret_cast<const void*>(k_block_partials<D>), kBlockThreads),
+                            kBlockThreads, 0, s>>>(d, w, sv, grad, B, nblk);
+      k_block_fold<D><<<grid(k_block_fold<D>), 256, 0, s>>>(w, nblk);
+    }
     if (d.total_slots > 0) {
       k_policy<<<grid(k_policy), 256, 0, s>>>(d, w, step);
       k_evict<D, BITS, SB16><<<grid(k_evict<D, BITS, SB16>), 256, 0, s>>>(d, w, sv, grad, step);

@@ -66,8 +66,10 @@ struct Plan {
   size_t o_rec, o_crow, o_tag, o_ts, o_cnt, o_G, o_desc, o_keyb, o_stats, o_err, state_bytes;
   // workspace offsets
   size_t o_kA, o_vA, o_kB, o_vB, o_ssmall, o_sst0, o_sst1, o_part, o_tcnt, o_tpre, o_uk, o_seg, o_setf, o_urow, o_utab, o_uslot,
-      o_uact, o_udest, o_nch, o_cbase, o_uvrow, o_uvu, o_partial, o_span, o_long, o_tabf, o_src, o_ctr, ws_bytes;
+      o_uact, o_udest, o_nch, o_cbase, o_uvrow, o_uvu, o_partial, o_span, o_ubig, o_brows, o_bbound, o_bpart, o_tabf, o_src, o_ctr, ws_bytes;
   int64_t max_partials = 0;
+  int64_t max_big = 0;
+  int32_t max_nblk = 0;
 };
 
 bool is_pow2(int64_t v) { return v > 0 && (v & (v - 1)) == 0; }
@@ -168,7 +170,15 @@ int plan_config(const emb_cache_config* c, Plan* p) {
   p->max_partials = (int64_t)(L / (embc::kSumChunk / 2) + 2);
   p->o_partial = take((size_t)p->max_partials * c->dim * 4);
   p->o_span = take((size_t)p->max_partials * 8);
-  p->o_long = take(4 * (L / ((size_t)embc::kSumChunk * embc::kFoldDirect) + 1));
+  p->o_ubig = take(4 * (L + 1));
+  p->max_big = (int64_t)(L / (embc::kBlockAbove + 1) + 1);
+  {
+    const int64_t nb = embc::kBlockFloats / c->dim;
+    p->max_nblk = (int32_t)((c->max_batch + nb - 1) / nb);
+  }
+  p->o_brows = take(4 * (size_t)p->max_big);
+  p->o_bbound = take(4 * (size_t)p->max_big * (size_t)(p->max_nblk + 1));
+  p->o_bpart = take(4 * (size_t)p->max_big * (size_t)p->max_nblk * (size_t)c->dim);
   p->o_tabf = take(4 * (size_t)(T + 1));
   p->o_src = take(4 * L);
   p->o_ctr = take(8 * embc::kNCounters);
@@ -319,7 +329,12 @@ int emb_cache_create(const emb_cache_config* cfg, void* state, size_t state_byte
   w.uvic_row = reinterpret_cast<int32_t*>(wb + p.o_uvrow);
   w.uvic_u = reinterpret_cast<int32_t*>(wb + p.o_uvu);
   w.partial = reinterpret_cast<float*>(wb + p.o_partial);
-  w.long_rows = reinterpret_cast<int32_t*>(wb + p.o_long);
+  w.ubig = reinterpret_cast<uint32_t*>(wb + p.o_ubig);
+  w.big_rows = reinterpret_cast<int32_t*>(wb + p.o_brows);
+  w.bbound = reinterpret_cast<uint32_t*>(wb + p.o_bbound);
+  w.bpart = reinterpret_cast<float*>(wb + p.o_bpart);
+  w.max_big = p.max_big;
+  w.max_nblk = p.max_nblk;
   w.chunk_span = reinterpret_cast<uint2*>(wb + p.o_span);
   w.tab_first = reinterpret_cast<int32_t*>(wb + p.o_tabf);
   w.fwd_src = reinterpret_cast<int32_t*>(wb + p.o_src);
