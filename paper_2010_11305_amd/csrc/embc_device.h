@@ -136,12 +136,17 @@ struct CodeWords {
   uint32_t w[BITS == 8 ? 2 : 1];
 };
 
-template <int BITS>
+template <int BITS, bool NT = false>
 __device__ __forceinline__ CodeWords<BITS> load_code_words(const uint8_t* rec, int g) {
   CodeWords<BITS> c;
   const uint32_t* p = reinterpret_cast<const uint32_t*>(rec) + g * (BITS == 8 ? 2 : 1);
-  c.w[0] = p[0];
-  if constexpr (BITS == 8) c.w[1] = p[1];
+  if constexpr (NT) {
+    c.w[0] = __builtin_nontemporal_load(p);
+    if constexpr (BITS == 8) c.w[1] = __builtin_nontemporal_load(p + 1);
+  } else {
+    c.w[0] = p[0];
+    if constexpr (BITS == 8) c.w[1] = p[1];
+  }
   return c;
 }
 
@@ -171,6 +176,24 @@ __device__ __forceinline__ void load_frow8(const float* row, int g, float (&x)[8
   const float4 a = p[0], b = p[1];
   x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
   x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+}
+
+// Nontemporal forms for data touched once per kernel (a row fetched and written back,
+// a pooled output): the hint keeps such lines from displacing, in L2, the lines that
+// other lanes still read (gradient rows, hot cache rows).
+typedef float f4v __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ void load_frow8_nt(const float* row, int g, float (&x)[8]) {
+  const f4v* p = reinterpret_cast<const f4v*>(row) + 2 * g;
+  const f4v a = __builtin_nontemporal_load(p), b = __builtin_nontemporal_load(p + 1);
+  x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+  x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+}
+
+__device__ __forceinline__ void store_frow8_nt(float* row, int g, const float (&x)[8]) {
+  f4v* p = reinterpret_cast<f4v*>(row) + 2 * g;
+  __builtin_nontemporal_store(f4v{x[0], x[1], x[2], x[3]}, p);
+  __builtin_nontemporal_store(f4v{x[4], x[5], x[6], x[7]}, p + 1);
 }
 
 __device__ __forceinline__ void store_frow8(float* row, int g, const float (&x)[8]) {
@@ -231,8 +254,8 @@ __device__ __forceinline__ void quantize_store(const float (&x)[8], int g, uint8
     }
   }
   uint32_t* p = reinterpret_cast<uint32_t*>(rec) + g * (BITS == 8 ? 2 : 1);
-  p[0] = w0;
-  if constexpr (BITS == 8) p[1] = w1;
+  __builtin_nontemporal_store(w0, p);  // a record is written once per step
+  if constexpr (BITS == 8) __builtin_nontemporal_store(w1, p + 1);
   if (g == 0) {
     uint32_t* ps = reinterpret_cast<uint32_t*>(rec + CB);
     if constexpr (SB16) {
@@ -281,7 +304,11 @@ __device__ __forceinline__ int32_t probe_slot(const Dev& dv, const TableDesc& td
 // (table t, part p; P parts per table so that there are at least 8 segments) and
 // XCD x takes segments x, x+8, ...; inside an XCD, its workgroups share a segment.
 // Every segment sees the same L2, so a table's hot cache rows, tags and gradient
-// rows are fetched into one L2 instead of eight.
+// rows are fetched into one L2 instead of eight.  With `even`, P makes T*P a
+// multiple of 8, so every XCD gets the same number of segments (e.g. 100 tables:
+// 2 parts, 25 segments per XCD instead of 13 or 12 tables); kernels whose reads
+// are mostly private to a row take that, those that share a table's lines across
+// rows (tags, gradient rows) keep one part per table.
 constexpr int kXcds = 8;
 
 struct XcdSplit {
@@ -289,11 +316,12 @@ struct XcdSplit {
   int64_t unit;     // this workgroup's index among the XCD's workgroups
   int64_t units;    // workgroups per XCD
   int parts;        // parts per table
-  __device__ XcdSplit(int T) {
+  __device__ XcdSplit(int T, bool even = false) {
     xcd = blockIdx.x % kXcds;
     unit = blockIdx.x / kXcds;
     units = gridDim.x / kXcds;
-    parts = T >= kXcds ? 1 : (kXcds + T - 1) / T;
+    if (even) parts = kXcds / min(T & -T, kXcds);
+    else parts = T >= kXcds ? 1 : (kXcds + T - 1) / T;
   }
   __device__ int segments(int T) const { return T * parts; }
 };

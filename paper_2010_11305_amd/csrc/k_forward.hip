@@ -259,7 +259,7 @@ __global__ __launch_bounds__(256) void k_fwd_gather(Dev dv, const int32_t* __res
           }
         }
       }
-      store_frow8(out + ((int64_t)b * dv.T + t) * D, g, acc);
+      store_frow8_nt(out + ((int64_t)b * dv.T + t) * D, g, acc);
     }
   }
 }

@@ -356,7 +356,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_block_partials(Dev dv, Work w
   __shared__ uint32_t lrow[kBlockThreads], lr0[kBlockThreads], lr1[kBlockThreads], cnt_s[4];
   const float* sf = reinterpret_cast<const float*>(stage);
   const int l = threadIdx.x & (GL - 1);
-  const XcdSplit xs(dv.T);
+  const XcdSplit xs(dv.T, true);
   for (int seg = xs.xcd; seg < xs.segments(dv.T); seg += kXcds) {
     const int t = seg / xs.parts;
     const int64_t h0 = w.ubig[w.tab_first[t]], h1 = w.ubig[w.tab_first[t + 1]];
@@ -561,13 +561,16 @@ __device__ __forceinline__ void apply_optimizer(const Dev& dv, float (&x)[8], co
 #pragma unroll
     for (int i = 0; i < h; ++i) a[i] = a[i] + a[i + h];
   const float Gn = G_old + a[0] * (1.0f / (float)D);
-  if (g == 0) dv.G[grow] = Gn;
+  if (g == 0) __builtin_nontemporal_store(Gn, dv.G + grow);
   const float rate = dv.lr / (__builtin_sqrtf(Gn) + dv.eps);
 #pragma unroll
   for (int i = 0; i < 8; ++i) x[i] = __builtin_fmaf(-rate, gr[i], x[i]);
 }
 
-__device__ __forceinline__ float load_G(const Dev& dv, int64_t grow) { return dv.optimizer ? dv.G[grow] : 0.0f; }
+// The accumulator of a row is read and written once per step (nontemporal).
+__device__ __forceinline__ float load_G(const Dev& dv, int64_t grow) {
+  return dv.optimizer ? __builtin_nontemporal_load(dv.G + grow) : 0.0f;
+}
 
 // ---- replacement decision, one wave per touched set ------------------------------------------
 struct PolicyLds {
@@ -753,7 +756,7 @@ __global__ __launch_bounds__(256) void k_evict(Dev dv, Work w, const uint32_t* _
   const int g = threadIdx.x & (LPR - 1);
   const int64_t nU = (int64_t)w.ctr[kCUnique];
   const bool sr = dv.rounding != 0;
-  const XcdSplit xs(dv.T);
+  const XcdSplit xs(dv.T, true);
   const int64_t gx = xs.unit * GPB + threadIdx.x / LPR, gstride = xs.units * GPB;
   for (int seg = xs.xcd; seg < xs.segments(dv.T); seg += kXcds) {
     const int t = seg / xs.parts;
@@ -769,7 +772,7 @@ __global__ __launch_bounds__(256) void k_evict(Dev dv, Work w, const uint32_t* _
       if (act != kActInsert || vrow < 0) continue;
       const int64_t vgrow = td.row_base + vrow;
       float xv[8];
-      load_frow8(dv.crow + (int64_t)dst * D, g, xv);
+      load_frow8_nt(dv.crow + (int64_t)dst * D, g, xv);
       if (vu >= 0) {
         // the displaced resident was updated this step (LFU): its new value goes to T
         const float Gv = load_G(dv, vgrow);
@@ -810,7 +813,7 @@ __global__ __launch_bounds__(256) void k_update(Dev dv, Work w, const uint32_t* 
   constexpr int RB = Rec<D, BITS, SB16>::BYTES;
   const int g = threadIdx.x & (LPR - 1);
   const bool sr = dv.rounding != 0;
-  const XcdSplit xs(dv.T);
+  const XcdSplit xs(dv.T, true);
   const int64_t gx = xs.unit * GPB + threadIdx.x / LPR, gstride = xs.units * GPB;
   for (int seg = xs.xcd; seg < xs.segments(dv.T); seg += kXcds) {
     const int t = seg / xs.parts;
@@ -838,9 +841,9 @@ __global__ __launch_bounds__(256) void k_update(Dev dv, Work w, const uint32_t* 
       CodeWords<BITS> cw;
       SbWords<SB16> sbw;
       if (hit) {
-        load_frow8(dv.crow + (int64_t)m.slot * D, g, x);
+        load_frow8_nt(dv.crow + (int64_t)m.slot * D, g, x);
       } else {
-        cw = load_code_words<BITS>(rec, g);
+        cw = load_code_words<BITS, true>(rec, g);
         sbw = load_sb_words<D, BITS, SB16>(rec);
       }
       const float G_old = load_G(dv, grow);
@@ -854,9 +857,9 @@ __global__ __launch_bounds__(256) void k_update(Dev dv, Work w, const uint32_t* 
       }
       apply_optimizer<D>(dv, x, gr, grow, g, G_old);
       if (hit) {
-        store_frow8(dv.crow + (int64_t)m.slot * D, g, x);
+        store_frow8_nt(dv.crow + (int64_t)m.slot * D, g, x);
       } else if (m.act == kActInsert) {
-        store_frow8(dv.crow + (int64_t)m.dst * D, g, x);
+        store_frow8_nt(dv.crow + (int64_t)m.dst * D, g, x);
         if (g == 0) {
           dv.tag[m.dst] = (int32_t)(grow - td.row_base);
           if (dv.policy == 0) dv.ts[m.dst] = (int32_t)step;
