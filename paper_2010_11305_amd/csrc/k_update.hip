@@ -786,23 +786,30 @@ __global__ __launch_bounds__(256) void k_evict(Dev dv, Work w, const uint32_t* _
 }
 
 // ---- per unique row: optimizer and write-back ------------------------------------------------
-// Per-row inputs of k_update, loaded one row ahead of their use.
-struct RowMeta {
-  int32_t act, grow, slot, dst;
-  uint32_t nch, s0, s1, cb;
-};
+// The inputs of k_update for unique row u, packed into one 16-byte word once the
+// replacement decisions are final (one load per row instead of eight):
+//   x = global row;  y = cache slot (a hit: its way; an insert: the way it takes);
+//   z = the bag of its one occurrence if the row has one lookup, else its first
+//       occurrence in the sorted stream;  w = lookups | kind << 30 (lookups < 2^30).
+// A row with one lookup (most rows) then loads its gradient row together with its
+// own row and accumulator, one dependent load fewer.
+constexpr uint32_t kKindHit = 0, kKindInsert = 1, kKindBypass = 2, kKindDone = 3;
+constexpr uint32_t kLookupMask = (1u << 30) - 1;
 
-__device__ __forceinline__ RowMeta load_meta(const Work& w, int64_t u) {
-  RowMeta m;
-  m.act = w.uact[u];
-  m.grow = w.urow[u];
-  m.slot = w.uslot[u];
-  m.dst = w.udest[u];
-  m.nch = w.nch[u];
-  m.s0 = w.seg[u];
-  m.s1 = w.seg[u + 1];
-  m.cb = w.chunk_base[u];
-  return m;
+__global__ __launch_bounds__(256) void k_pack_meta(Work w, const uint32_t* __restrict__ sval) {
+  const int64_t nU = (int64_t)w.ctr[kCUnique];
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < nU; u += stride) {
+    const int32_t act = w.uact[u];
+    const uint32_t s0 = w.seg[u], n = w.seg[u + 1] - s0;
+    const uint32_t kind = act == kActHitStay ? kKindHit
+                          : act == kActInsert ? kKindInsert
+                          : act == kActBypass ? kKindBypass
+                                              : kKindDone;
+    const int32_t cs = kind == kKindHit ? w.uslot[u] : kind == kKindInsert ? w.udest[u] : -1;
+    const uint32_t z = n == 1 ? sval[s0] : s0;
+    w.umeta[u] = make_uint4((uint32_t)w.urow[u], (uint32_t)cs, z, n | (kind << 30));
+  }
 }
 
 template <int D, int BITS, bool SB16>
@@ -823,46 +830,50 @@ __global__ __launch_bounds__(256) void k_update(Dev dv, Work w, const uint32_t* 
     const TableDesc td = dv.desc[t];
     const GradRows gtab = grad_rows<D>(grad, t, dv.T);
     if (lo + gx >= hi) continue;
-    RowMeta next = load_meta(w, lo + gx);
+    uint4 next = w.umeta[lo + gx];
     for (int64_t u = lo + gx; u < hi; u += gstride) {
-      const RowMeta m = next;
-      // the next row's metadata is in flight while this row is handled (the index is
-      // clamped so that the loads are unconditional; the last one is not used)
-      next = load_meta(w, min<int64_t>(u + gstride, hi - 1));
-      if (m.act == kActDone) continue;
-      const int64_t grow = m.grow;
+      const uint4 m = next;
+      // the next row's inputs are in flight while this row is handled (the index is
+      // clamped so that the load is unconditional; the last one is not used)
+      next = w.umeta[min<int64_t>(u + gstride, hi - 1)];
+      const uint32_t kind = m.w >> 30, n = m.w & kLookupMask;
+      if (kind == kKindDone) continue;
+      const int64_t grow = m.x;
       uint8_t* rec = dv.rec + grow * RB;
-      const bool hit = m.act == kActHitStay;
-      // first level of loads: the first occurrence values, the row, its accumulator
-      const bool big = m.s1 - m.s0 > kBlockAbove;
-      const uint32_t n0 = m.nch == 0 && !big ? min<uint32_t>((uint32_t)LPR, m.s1 - m.s0) : 0u;
-      const uint32_t myv0 = (uint32_t)g < n0 ? sval[m.s0 + g] : 0u;
+      const bool hit = kind == kKindHit;
+      const bool big = n > kBlockAbove;
+      // first level of loads: the row, its accumulator, and the gradient row (one
+      // lookup) or the first occurrence values (2 to kSumChunk lookups)
       float x[8], gr[8];
+      // both loads unconditional (a row with more lookups re-reads bag 0's gradient
+      // row; the position index is clamped into the row's occurrences, or 0)
+      load_frow8(gtab.row(n == 1 ? m.z : 0u), g, gr);
+      const uint32_t myv0 = sval[n == 1 ? 0u : m.z + min<uint32_t>((uint32_t)g, n - 1)];
       CodeWords<BITS> cw;
       SbWords<SB16> sbw;
       if (hit) {
-        load_frow8_nt(dv.crow + (int64_t)m.slot * D, g, x);
+        load_frow8_nt(dv.crow + (int64_t)(int32_t)m.y * D, g, x);
       } else {
         cw = load_code_words<BITS, true>(rec, g);
         sbw = load_sb_words<D, BITS, SB16>(rec);
       }
       const float G_old = load_G(dv, grow);
       if (big) load_frow8(w.bpart + (int64_t)w.ubig[u] * w.max_nblk * D, g, gr);
-      else if (m.nch > 0) fold_chunks<D>(w.partial, m.cb, m.nch, g, gr);
-      else sum_occ<D>(sval, m.s0, m.s1, gtab, g, gr, myv0, true);
+      else if (n > (uint32_t)kSumChunk)
+        fold_chunks<D>(w.partial, w.chunk_base[u], (n + kSumChunk - 1) / kSumChunk, g, gr);
+      else if (n > 1) sum_occ<D>(sval, m.z, m.z + n, gtab, g, gr, myv0, true);
       if (!hit) {
         float sc, bi;
         decode_sb<SB16>(sbw, sc, bi);
         dequant8<BITS>(cw, sc, bi, x);
       }
       apply_optimizer<D>(dv, x, gr, grow, g, G_old);
-      if (hit) {
-        store_frow8_nt(dv.crow + (int64_t)m.slot * D, g, x);
-      } else if (m.act == kActInsert) {
-        store_frow8_nt(dv.crow + (int64_t)m.dst * D, g, x);
-        if (g == 0) {
-          dv.tag[m.dst] = (int32_t)(grow - td.row_base);
-          if (dv.policy == 0) dv.ts[m.dst] = (int32_t)step;
+      if (hit || kind == kKindInsert) {
+        const int64_t cs = (int32_t)m.y;
+        store_frow8_nt(dv.crow + cs * D, g, x);
+        if (!hit && g == 0) {
+          dv.tag[cs] = (int32_t)(grow - td.row_base);
+          if (dv.policy == 0) dv.ts[cs] = (int32_t)step;
         }
       } else {
         quantize_store<D, BITS, SB16>(x, g, rec, sr, dv.seed, step, (uint32_t)t, (uint32_t)(grow - td.row_base));
@@ -918,6 +929,7 @@ hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int6
       k_policy<<<grid(k_policy), 256, 0, s>>>(d, w, step);
       k_evict<D, BITS, SB16><<<grid(k_evict<D, BITS, SB16>), 256, 0, s>>>(d, w, sv, grad, step);
     }
+    k_pack_meta<<<grid(k_pack_meta), 256, 0, s>>>(w, sv);
     if (update_events) {
       const hipError_t e2 = hipEventRecord(update_events[0], s);
       if (e2 != hipSuccess) return e2;
