@@ -70,6 +70,8 @@ def lib():
         L.orc_f16_bits_to_f32.argtypes = [c.c_uint16]
         L.orc_round_to_f16.restype = c.c_float
         L.orc_round_to_f16.argtypes = [c.c_float]
+        L.orc_f16_round.restype = c.c_uint16
+        L.orc_f16_round.argtypes = [c.c_float, c.c_int, c.c_float]
         L.orc_quantize_row.argtypes = [
             P, c.c_int, c.c_int, c.c_int, c.c_int, c.c_uint64, c.c_uint32, c.c_uint32, c.c_uint32,
             P, c.POINTER(c.c_float), c.POINTER(c.c_float),
@@ -111,6 +113,8 @@ class Oracle:
         self.T = len(self.rows)
         self.dim = int(dim)
         self.bits = int(bits)
+        # an FP16 table exports its binary16 bit patterns; integer codes one per byte
+        self.code_dtype = np.uint16 if self.bits == 16 else np.uint8
         self.sb_fp16 = bool(sb_fp16)
         self.policy = policy
         cfg = _Cfg(self.T, self.dim, self.bits, int(self.sb_fp16), float(cache_fraction), int(assoc),
@@ -166,7 +170,7 @@ class Oracle:
 
     def export_rows(self, t, row0=0, n=None):
         n = self.rows[t] - row0 if n is None else n
-        codes = np.empty((n, self.dim), dtype=np.uint8)
+        codes = np.empty((n, self.dim), dtype=self.code_dtype)
         scale = np.empty(n, dtype=np.float32)
         bias = np.empty(n, dtype=np.float32)
         cnt = np.empty(n, dtype=np.int32)
@@ -176,7 +180,7 @@ class Oracle:
 
     def import_rows(self, t, row0, codes=None, scale=None, bias=None, cnt=None, G=None):
         arrs = [codes, scale, bias, cnt, G]
-        dts = [np.uint8, np.float32, np.float32, np.int32, np.float32]
+        dts = [self.code_dtype, np.float32, np.float32, np.int32, np.float32]
         arrs = [None if a is None else np.ascontiguousarray(a, dtype=dt) for a, dt in zip(arrs, dts)]
         n = next(len(a) for a in arrs if a is not None)
         lib().orc_import_rows(self._h, t, row0, n, *[_ptr(a) for a in arrs])
@@ -213,6 +217,12 @@ def f32_to_f16_bits(x: float) -> int:
 
 def f16_bits_to_f32(h: int) -> float:
     return float(lib().orc_f16_bits_to_f32(h))
+
+
+def f16_round(x: float, stochastic: bool = False, u: float = 0.0) -> int:
+    """Down-conversion of one value into binary16 bits: nearest-even, or stochastic
+    with the uniform u (see orc_f16_round)."""
+    return int(lib().orc_f16_round(x, int(bool(stochastic)), u))
 
 
 def quantize_row(x, bits, sb_fp16=False, stochastic=False, seed=0, step=0, table=0, row=0):

@@ -22,9 +22,12 @@
  *                     gradients"): sort rows, merge the gradients of the same row,
  *                     apply one update per unique row.
  *   quantization   -- Sec. 3 "Precision" and Alg. 1: row-wise uniform min-max,
- *                     b = min, s = (max-min)/(2^bits-1), codes in [0, 2^bits-1].
+ *                     b = min, s = (max-min)/(2^bits-1), codes in [0, 2^bits-1]
+ *                     for INT8, INT4 and INT2; or the IEEE binary16 value of each
+ *                     element for an FP16 table (no (s,b)).
  *   rounding       -- Sec. 3 "Rounding": nearest with ties to even, or stochastic
- *                     rounding with E[q] = v.
+ *                     rounding with E[q] = v, between consecutive codes or between
+ *                     the two FP16 values one unit in the last place apart.
  *
  * Readings taken where the paper is silent (each is listed in the design notes):
  *   hash h(i) = i mod n_sets; n_sets = max(1, floor(floor(frac*N)/assoc)), 0 when
@@ -68,7 +71,7 @@ enum {
 typedef struct {
   int32_t num_tables;
   int32_t dim;
-  int32_t bits;               /* 8 or 4 */
+  int32_t bits;               /* 8, 4 or 2 (integer codes), or 16 (FP16 table) */
   int32_t sb_fp16;            /* 0: (s,b) in FP32; 1: (s,b) rounded to FP16 */
   double cache_fraction;
   int32_t assoc;
@@ -83,7 +86,8 @@ typedef struct {
 
 typedef struct {
   int64_t N, n_sets, slots;
-  uint8_t *code;   /* [N][d], one code per byte */
+  uint8_t *code;   /* [N][d], one code per byte (integer precisions) */
+  uint16_t *h16;   /* [N][d], binary16 bit patterns (FP16 table) */
   float *scale;    /* [N] (FP16-representable values when sb_fp16) */
   float *bias;     /* [N] */
   float *crow;     /* [slots][d] FP32 cache rows */
@@ -208,6 +212,37 @@ float orc_f16_bits_to_f32(uint16_t h) {
 
 float orc_round_to_f16(float x) { return orc_f16_bits_to_f32(orc_f32_to_f16_bits(x)); }
 
+/* The binary16 value next to h in increasing (up = 1) or decreasing (up = 0)
+ * order, for finite h.  Magnitudes are ordered like their bit patterns; the sign
+ * bit flips the direction, and +0 and -0 both step to the smallest subnormal of
+ * the stepping direction. */
+static uint16_t f16_step(uint16_t h, int up) {
+  uint16_t sign = h & 0x8000u, mag = h & 0x7FFFu;
+  if (mag == 0) return up ? 0x0001u : 0x8001u;
+  int grow = (sign == 0) == (up != 0);      /* moving away from zero */
+  return (uint16_t)(sign | (grow ? mag + 1u : mag - 1u));
+}
+
+/* Down-conversion of one FP32 value into binary16 (Sec. 3 "Rounding" with FP16
+ * as the low-precision domain).  Nearest: IEEE round to nearest, ties to even
+ * (overflow to infinity).  Stochastic: x- <= x <= x+ are consecutive finite
+ * binary16 values and x+ is taken with probability (x - x-)/(x+ - x-), i.e. when
+ * u < (x - x-)/(x+ - x-) for the uniform u of this element; x beyond the largest
+ * finite value (65504) saturates to it; an exactly representable x is kept; NaN
+ * stays NaN. */
+uint16_t orc_f16_round(float x, int stochastic, float u) {
+  uint16_t h = orc_f32_to_f16_bits(x);
+  if (!stochastic || isnan(x)) return h;
+  if (x > 65504.0f) return 0x7BFFu;
+  if (x < -65504.0f) return 0xFBFFu;
+  float y = orc_f16_bits_to_f32(h);
+  if (y == x) return h;
+  uint16_t lo_h = y < x ? h : f16_step(h, 0);
+  uint16_t hi_h = y < x ? f16_step(h, 1) : h;
+  float lo = orc_f16_bits_to_f32(lo_h), hi = orc_f16_bits_to_f32(hi_h);
+  return (u < (x - lo) / (hi - lo)) ? hi_h : lo_h;
+}
+
 /* ------------------------------------------------------------------------- */
 /* Alg. 1 (row-wise IntN quantization with uniform min-max parameters).        */
 /* ------------------------------------------------------------------------- */
@@ -268,7 +303,7 @@ void orc_destroy(orc_t *o) {
   if (o->tab) {
     for (int t = 0; t < o->cfg.num_tables; ++t) {
       orc_table *tb = &o->tab[t];
-      free(tb->code); free(tb->scale); free(tb->bias); free(tb->crow);
+      free(tb->code); free(tb->h16); free(tb->scale); free(tb->bias); free(tb->crow);
       free(tb->tag); free(tb->ts); free(tb->cnt); free(tb->G);
     }
     free(o->tab);
@@ -277,8 +312,8 @@ void orc_destroy(orc_t *o) {
 }
 
 orc_t *orc_create(const orc_config *cfg, const int64_t *rows) {
-  if (cfg->num_tables < 1 || cfg->dim < 1 || (cfg->bits != 8 && cfg->bits != 4) || cfg->assoc < 1)
-    return NULL;
+  if (cfg->num_tables < 1 || cfg->dim < 1 || cfg->assoc < 1) return NULL;
+  if (cfg->bits != 16 && cfg->bits != 8 && cfg->bits != 4 && cfg->bits != 2) return NULL;
   orc_t *o = (orc_t *)calloc(1, sizeof(orc_t));
   o->cfg = *cfg;
   o->tab = (orc_table *)calloc((size_t)cfg->num_tables, sizeof(orc_table));
@@ -288,7 +323,8 @@ orc_t *orc_create(const orc_config *cfg, const int64_t *rows) {
     tb->N = rows[t];
     tb->n_sets = n_sets_of(cfg, tb->N);
     tb->slots = tb->n_sets * cfg->assoc;
-    tb->code = (uint8_t *)calloc((size_t)(tb->N * d), 1);
+    if (cfg->bits == 16) tb->h16 = (uint16_t *)calloc((size_t)(tb->N * d), sizeof(uint16_t));
+    else tb->code = (uint8_t *)calloc((size_t)(tb->N * d), 1);
     tb->scale = (float *)calloc((size_t)tb->N, sizeof(float));
     tb->bias = (float *)calloc((size_t)tb->N, sizeof(float));
     tb->crow = (float *)calloc((size_t)(tb->slots * d) + 1, sizeof(float));
@@ -297,7 +333,7 @@ orc_t *orc_create(const orc_config *cfg, const int64_t *rows) {
     for (int64_t k = 0; k < tb->slots; ++k) { tb->tag[k] = -1; tb->ts[k] = -1; }
     tb->cnt = (int32_t *)calloc((size_t)tb->N, sizeof(int32_t));
     tb->G = (float *)calloc((size_t)tb->N, sizeof(float));
-    if (!tb->code || !tb->scale || !tb->bias || !tb->crow || !tb->tag || !tb->ts || !tb->cnt || !tb->G) {
+    if (!(tb->code || tb->h16) || !tb->scale || !tb->bias || !tb->crow || !tb->tag || !tb->ts || !tb->cnt || !tb->G) {
       orc_destroy(o);
       return NULL;
     }
@@ -325,8 +361,12 @@ void orc_init_uniform(orc_t *o, float lo, float hi, uint64_t init_seed) {
     for (int64_t r = 0; r < tb->N; ++r) {
       for (int j = 0; j < d; ++j)
         x[j] = fmaf(orc_uniform(init_seed, 0xFFFFFFFFu, (uint32_t)t, (uint32_t)r, (uint32_t)j), width, lo);
-      orc_quantize_row(x, d, o->cfg.bits, o->cfg.sb_fp16, 0, 0, 0, 0, 0,
-                       tb->code + r * d, &tb->scale[r], &tb->bias[r]);
+      if (o->cfg.bits == 16) {
+        for (int j = 0; j < d; ++j) tb->h16[r * d + j] = orc_f16_round(x[j], 0, 0.0f);
+      } else {
+        orc_quantize_row(x, d, o->cfg.bits, o->cfg.sb_fp16, 0, 0, 0, 0, 0,
+                         tb->code + r * d, &tb->scale[r], &tb->bias[r]);
+      }
     }
     for (int64_t k = 0; k < tb->slots; ++k) { tb->tag[k] = -1; tb->ts[k] = -1; }
     memset(tb->crow, 0, sizeof(float) * (size_t)(tb->slots * d));
@@ -353,6 +393,8 @@ static void fetch_row(const orc_t *o, const orc_table *tb, int64_t r, float *x) 
   int64_t k = find_slot(o, tb, r);
   if (k >= 0) {
     memcpy(x, tb->crow + k * d, sizeof(float) * (size_t)d);
+  } else if (o->cfg.bits == 16) {
+    for (int j = 0; j < d; ++j) x[j] = orc_f16_bits_to_f32(tb->h16[r * d + j]);
   } else {
     for (int j = 0; j < d; ++j) x[j] = dequant(tb->code[r * d + j], tb->scale[r], tb->bias[r]);
   }
@@ -361,6 +403,14 @@ static void fetch_row(const orc_t *o, const orc_table *tb, int64_t r, float *x) 
 /* Down-convert an FP32 row into the low-precision table T. */
 static void store_low_precision(orc_t *o, int t, int64_t r, const float *x) {
   orc_table *tb = &o->tab[t];
+  if (o->cfg.bits == 16) {
+    for (int j = 0; j < o->cfg.dim; ++j) {
+      float u = o->cfg.stochastic ? orc_uniform(o->cfg.seed, (uint32_t)o->step, (uint32_t)t, (uint32_t)r, (uint32_t)j)
+                                  : 0.0f;
+      tb->h16[r * o->cfg.dim + j] = orc_f16_round(x[j], o->cfg.stochastic, u);
+    }
+    return;
+  }
   orc_quantize_row(x, o->cfg.dim, o->cfg.bits, o->cfg.sb_fp16, o->cfg.stochastic, o->cfg.seed,
                    (uint32_t)o->step, (uint32_t)t, (uint32_t)r, tb->code + r * o->cfg.dim,
                    &tb->scale[r], &tb->bias[r]);
@@ -551,6 +601,8 @@ void orc_backward_update(orc_t *o, const int32_t *idx, int64_t n_idx, const int3
       int64_t r = urow[u];
       if (uslot[u] >= 0) {
         memcpy(xu, tb->crow + uslot[u] * d, sizeof(float) * (size_t)d);
+      } else if (c->bits == 16) {
+        for (int j = 0; j < d; ++j) xu[j] = orc_f16_bits_to_f32(tb->h16[r * d + j]);
       } else {
         for (int j = 0; j < d; ++j) xu[j] = dequant(tb->code[r * d + j], tb->scale[r], tb->bias[r]);
       }
@@ -717,24 +769,27 @@ void orc_stats(const orc_t *o, int t, int64_t *out) {
   for (int k = 0; k < ORC_NSTAT; ++k) out[k] = o->tab[t].stat[k];
 }
 
-/* Rows [row0, row0+n) of table t: codes [n][d] (one per byte), scale, bias,
- * LFU counts and Adagrad accumulators.  NULL outputs are skipped. */
-void orc_export_rows(const orc_t *o, int t, int64_t row0, int64_t n, uint8_t *codes, float *scale,
+/* Rows [row0, row0+n) of table t: codes [n][d] (one per byte; for an FP16 table
+ * the binary16 bit patterns, two bytes each), scale, bias (0 for FP16), LFU counts
+ * and Adagrad accumulators.  NULL outputs are skipped. */
+void orc_export_rows(const orc_t *o, int t, int64_t row0, int64_t n, void *codes, float *scale,
                      float *bias, int32_t *cnt, float *G) {
   const orc_table *tb = &o->tab[t];
   int d = o->cfg.dim;
-  if (codes) memcpy(codes, tb->code + row0 * d, (size_t)(n * d));
+  if (codes && o->cfg.bits == 16) memcpy(codes, tb->h16 + row0 * d, sizeof(uint16_t) * (size_t)(n * d));
+  else if (codes) memcpy(codes, tb->code + row0 * d, (size_t)(n * d));
   if (scale) memcpy(scale, tb->scale + row0, sizeof(float) * (size_t)n);
   if (bias) memcpy(bias, tb->bias + row0, sizeof(float) * (size_t)n);
   if (cnt) memcpy(cnt, tb->cnt + row0, sizeof(int32_t) * (size_t)n);
   if (G) memcpy(G, tb->G + row0, sizeof(float) * (size_t)n);
 }
 
-void orc_import_rows(orc_t *o, int t, int64_t row0, int64_t n, const uint8_t *codes, const float *scale,
+void orc_import_rows(orc_t *o, int t, int64_t row0, int64_t n, const void *codes, const float *scale,
                      const float *bias, const int32_t *cnt, const float *G) {
   orc_table *tb = &o->tab[t];
   int d = o->cfg.dim;
-  if (codes) memcpy(tb->code + row0 * d, codes, (size_t)(n * d));
+  if (codes && o->cfg.bits == 16) memcpy(tb->h16 + row0 * d, codes, sizeof(uint16_t) * (size_t)(n * d));
+  else if (codes) memcpy(tb->code + row0 * d, codes, (size_t)(n * d));
   if (scale) memcpy(tb->scale + row0, scale, sizeof(float) * (size_t)n);
   if (bias) memcpy(tb->bias + row0, bias, sizeof(float) * (size_t)n);
   if (cnt) memcpy(tb->cnt + row0, cnt, sizeof(int32_t) * (size_t)n);

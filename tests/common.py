@@ -21,9 +21,9 @@ def custom_cfg(**kw):
 
 def effective_table(o, t):
     """FP32 view of table t: cache row when resident, else the dequantized row."""
-    from exact import dequant_exact
+    from exact import decode_rows
     r = o.export_rows(t)
-    eff = dequant_exact(r["codes"], r["scale"], r["bias"])
+    eff = decode_rows(r["codes"], r["scale"], r["bias"])
     c = o.export_cache(t)
     for k in np.nonzero(c["tag"] >= 0)[0]:
         eff[c["tag"][k]] = c["crow"][k]

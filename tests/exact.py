@@ -52,3 +52,42 @@ def dequant_exact(codes, scale, bias):
                 cache[key] = v
             o[i, j] = v
     return out
+
+
+def decode_rows(codes, scale, bias):
+    """FP32 rows of exported low-precision rows: binary16 bit patterns (uint16 codes,
+    an FP16 table) widen exactly; integer codes dequantize as q*s+b rounded once."""
+    codes = np.asarray(codes)
+    if codes.dtype == np.uint16:
+        return codes.view(np.float16).astype(np.float32)
+    return dequant_exact(codes, scale, bias)
+
+
+def f16_neighbours(x):
+    """(x-, x+): the consecutive binary16 values around float32 x, |x| <= 65504,
+    from numpy's float16 type (equal when x is representable)."""
+    h = np.float16(x)
+    if float(h) == float(x):
+        return h, h
+    if float(h) > float(x):
+        return np.nextafter(h, np.float16(-np.inf)), h
+    return h, np.nextafter(h, np.float16(np.inf))
+
+
+def f16_round_ref(x, stochastic=False, u=0.0):
+    """binary16 bits of float32 x: numpy's nearest-even conversion, or stochastic
+    rounding between the finite neighbours, x+ when u < (x - x-)/(x+ - x-) in exact
+    rationals; beyond 65504 stochastic rounding saturates."""
+    x = np.float32(x)
+    if not stochastic or np.isnan(x):
+        with np.errstate(over="ignore"):
+            return int(np.float16(x).view(np.uint16))
+    if x > 65504:
+        return int(np.float16(65504).view(np.uint16))
+    if x < -65504:
+        return int(np.float16(-65504).view(np.uint16))
+    lo, hi = f16_neighbours(x)
+    if lo == hi:
+        return int(lo.view(np.uint16))
+    p = (Fraction(float(x)) - Fraction(float(lo))) / (Fraction(float(hi)) - Fraction(float(lo)))
+    return int((hi if Fraction(float(u)) < p else lo).view(np.uint16))

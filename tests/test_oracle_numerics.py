@@ -20,7 +20,7 @@ GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
 
 # ---- P1: code ranges and the min/max end points ------------------------------------------
-@pytest.mark.parametrize("bits", [8, 4])
+@pytest.mark.parametrize("bits", [8, 4, 2])
 def test_codes_in_range_and_endpoints(bits):
     K = 2**bits - 1
     rng = np.random.default_rng(10 + bits)
@@ -207,3 +207,86 @@ def test_requantize_idempotent_fp16_sb(bits):
         y = dequant_exact(c1, s1, b1)
         c2, s2, b2 = oracle.quantize_row(y, bits, sb_fp16=True)
         assert np.array_equal(c1, c2) and b2 == b1 and s2 == s1
+
+
+# ---- P4b: FP16 table rounding (Sec. 3 "Rounding" with FP16 as the low precision) ------------
+def _f16_samples(rng):
+    return np.concatenate([
+        rng.standard_normal(3000).astype(np.float32) * np.float32(0.05),
+        (rng.random(800) * 2**-14).astype(np.float32) * rng.choice([-1, 1], 800).astype(np.float32),
+        (rng.random(300) * 2**-23).astype(np.float32),
+        rng.uniform(-65504, 65504, 300).astype(np.float32),
+        np.array([0.0, -0.0, 1.0, -1.0, 65504.0, -65504.0, 65519.0, 65520.0, 7e4, -7e4, 2**-24, 2**-25,
+                  3 * 2**-26, 1 + 2**-11, 1 + 3 * 2**-11, np.inf, -np.inf], dtype=np.float32),
+    ])
+
+
+def test_fp16_table_nearest_matches_numpy():
+    from exact import f16_round_ref
+    for x in _f16_samples(np.random.default_rng(21)):
+        assert oracle.f16_round(float(x)) == f16_round_ref(x), x
+
+
+def test_fp16_table_stochastic_threshold_is_exact():
+    """x+ exactly when u < (x - x-)/(x+ - x-), checked at the uniforms straddling the
+    threshold (the uniforms are multiples of 2^-24)."""
+    from exact import f16_neighbours, f16_round_ref
+    rng = np.random.default_rng(22)
+    xs = [x for x in _f16_samples(rng) if np.isfinite(x)]
+    for x in xs:
+        us = [0.0, 1 - 2**-24, float(rng.random())]
+        if abs(x) <= 65504:
+            lo, hi = f16_neighbours(x)
+            if lo != hi:
+                p = (float(x) - float(lo)) / (float(hi) - float(lo))
+                k = int(np.floor(p * 2**24))
+                us += [(k - 1) * 2**-24, k * 2**-24, (k + 1) * 2**-24]
+        for u in us:
+            if 0 <= u < 1:
+                got = oracle.f16_round(float(x), True, u)
+                assert got == f16_round_ref(x, True, u), (x, u)
+                if abs(x) <= 65504:
+                    lo, hi = f16_neighbours(x)
+                    assert got in (int(lo.view(np.uint16)), int(hi.view(np.uint16)))
+    assert oracle.f16_round(7e4, True, 0.5) == 0x7BFF and oracle.f16_round(-7e4, True, 0.5) == 0xFBFF
+    assert np.isnan(oracle.f16_bits_to_f32(oracle.f16_round(float("nan"), True, 0.5)))
+
+
+def test_fp16_table_stochastic_unbiased():
+    """Mean over draws of the pinned uniform equals x within 4 sigma (plus the 2^-24
+    resolution of the uniform times the unit in the last place)."""
+    xs = np.array([0.1, -0.3, 1 + 2**-12, 3e-6, -2.5e-7, 0.0375, 1000.3], dtype=np.float32)
+    M = 3000
+    from exact import f16_neighbours
+    for i, x in enumerate(xs):
+        vals = [oracle.f16_bits_to_f32(oracle.f16_round(float(x), True, oracle.uniform(9, k, 0, i, 0)))
+                for k in range(M)]
+        lo, hi = (float(v) for v in f16_neighbours(x))
+        p = (float(x) - lo) / (hi - lo)
+        sd = (hi - lo) * np.sqrt(p * (1 - p) / M)
+        assert abs(np.mean(vals) - float(x)) <= 4 * sd + (hi - lo) * 2**-24, x
+        assert set(vals) <= {lo, hi}
+
+
+# ---- P1b/P2b: INT2 ---------------------------------------------------------------------------
+def test_int2_codes_and_ties_to_even():
+    x = np.array([0, 3, 0.5, 1.5, 2.5, 1, 2, 0.25, 0.75, 2.75, 1.25, 2.25, 3, 0, 1.75, 1.4], dtype=np.float32)
+    codes, s, b = oracle.quantize_row(x, 2)
+    assert s == 1 and b == 0
+    assert list(codes) == [0, 3, 0, 2, 2, 1, 2, 0, 1, 3, 1, 2, 3, 0, 2, 1]
+
+
+def test_int2_stochastic_rounding_unbiased():
+    fr = [0.0, 0.5, 0.25, 0.75, 0.1, 0.9, 0.3, 0.6, 0.125, 0.875, 0.0, 0.0, 0.5, 0.2]
+    x = np.array([0.0, 3.0] + [1 + f for f in fr], dtype=np.float32)
+    M = 3000
+    acc = np.zeros(x.size)
+    for step in range(M):
+        codes, s, b = oracle.quantize_row(x, 2, stochastic=True, seed=78, step=step, table=1, row=5)
+        assert s == 1 and b == 0
+        lo = np.floor(x).astype(int)
+        assert np.all((codes == lo) | (codes == lo + 1))
+        acc += codes
+    frac = x - np.floor(x)
+    bound = 4 * np.sqrt(frac * (1 - frac) / M) + 2.0**-24
+    assert np.all(np.abs(acc / M - x) <= bound + 1e-12)

@@ -18,7 +18,7 @@ import numpy as np
 import pytest
 
 from common import custom_cfg, effective_table, exact_grad, oracle_from_cfg
-from exact import dequant_exact, fma32, round_f32
+from exact import decode_rows, dequant_exact, f16_round_ref, fma32, round_f32
 import oracle
 from paper_2010_11305_amd import configs, workload
 
@@ -35,6 +35,8 @@ def _run(o, cfg, steps, grad_fn=None, first=0):
 @pytest.mark.parametrize("name,over", [
     ("tiny", {}),
     ("tiny", {"bits": 4, "sb_fp16": True, "rounding": "stochastic", "policy": "lfu"}),
+    ("tiny", {"bits": 16, "rounding": "stochastic"}),
+    ("tiny", {"bits": 2, "sb_fp16": True, "assoc": 1}),
 ])
 def test_forward_matches_bruteforce(name, over):
     cfg = configs.get(name, **over)
@@ -226,7 +228,8 @@ def test_full_coverage_matches_numpy_rowwise_adagrad():
 
 
 # ---- P10: no cache = plain low-precision training ------------------------------------------------
-@pytest.mark.parametrize("bits,sb16,sr", [(8, False, False), (4, True, True)])
+@pytest.mark.parametrize("bits,sb16,sr", [(8, False, False), (4, True, True), (2, False, True), (16, False, False),
+                                          (16, False, True)])
 def test_no_cache_is_plain_low_precision_training(bits, sb16, sr):
     cfg = custom_cfg(cache_fraction=0.0, bits=bits, sb_fp16=sb16, rounding="stochastic" if sr else "nearest")
     o = oracle_from_cfg(cfg)
@@ -247,9 +250,14 @@ def test_no_cache_is_plain_low_precision_training(bits, sb16, sr):
                 for j in range(16):
                     tot[j] += n * Fraction(float(g[b, 0, j]))
             gsum = np.array([round_f32(v) for v in tot], dtype=np.float32)
-            x = dequant_exact(before["codes"][r], before["scale"][r], before["bias"][r])
+            x = decode_rows(before["codes"][r], before["scale"][r], before["bias"][r]).reshape(-1)
             lr = np.float32(cfg["lr"])
             xn = np.array([fma32(-lr, gsum[j], x[j]) for j in range(16)], dtype=np.float32)
+            if bits == 16:
+                # binary16 of each element, independently of the oracle's conversion
+                c = [f16_round_ref(xn[j], sr, oracle.uniform(cfg["seed"], k, 0, r, j)) for j in range(16)]
+                assert list(after["codes"][r]) == c
+                continue
             c, s, b_ = oracle.quantize_row(xn, bits, sb16, sr, cfg["seed"], k, 0, r)
             assert np.array_equal(after["codes"][r], c) and after["scale"][r] == s and after["bias"][r] == b_
         untouched = np.setdiff1d(np.arange(1000), touched)
@@ -266,6 +274,8 @@ INV_CASES = [
     dict(assoc=32, cache_fraction=0.2, policy="lfu", lfu_decay_interval=3, bits=4, sb_fp16=True,
          rounding="stochastic", optimizer="adagrad"),
     dict(assoc=8, cache_fraction=0.1, batch=300, pooling=("uniform", 1, 12)),
+    dict(bits=16, rounding="stochastic", policy="lfu", optimizer="adagrad"),
+    dict(bits=2, sb_fp16=True, assoc=8, rounding="stochastic"),
 ]
 
 
