@@ -3,8 +3,9 @@
  * EmbeddingBag training step of "Mixed-Precision Embedding Using a Cache".
  *
  * The method (Sec. 3 of the paper): each embedding table T is stored in a
- * precision lower than FP32 -- here INT8 or INT4 codes with one (scale, bias)
- * pair per row ("Precision" knob, row-wise uniform min-max quantization) --
+ * precision lower than FP32 -- FP16 elements, or INT8, INT4 or INT2 codes with
+ * one (scale, bias) pair per row ("Precision" knob, row-wise uniform min-max
+ * quantization) --
  * and is augmented with an FP32 cache C of n sets x alpha ways ("Cache
  * Structure" knob).  fetch(T,C,i) returns the FP32 cache row when row i is
  * resident in set h(i), else the up-converted low-precision row;
@@ -48,8 +49,10 @@ extern "C" {
 #define EMB_EHIP 4   /* a HIP runtime call failed */
 
 /* ---- knobs (Sec. 3) ---------------------------------------------------------- */
-#define EMB_INT8 8 /* precision: codes in [0, 255], one byte per element */
-#define EMB_INT4 4 /* precision: codes in [0, 15], two per byte, even column in the low nibble */
+#define EMB_FP16 16 /* precision: IEEE binary16 elements, no scale/bias (sb_dtype is ignored) */
+#define EMB_INT8 8  /* precision: codes in [0, 255], one byte per element */
+#define EMB_INT4 4  /* precision: codes in [0, 15], two per byte, even column in the low nibble */
+#define EMB_INT2 2  /* precision: codes in [0, 3], four per byte, column 4k+i in bits 2i..2i+1 of byte k */
 #define EMB_SB_FP32 0 /* per-row (scale, bias) stored as FP32 (the paper's choice) */
 #define EMB_SB_FP16 1 /* per-row (scale, bias) rounded to FP16 (nearest even) */
 #define EMB_LRU 0 /* priority = step of last access, per cached row */
@@ -79,6 +82,8 @@ extern "C" {
  * optimizer.
  *   rows[t]           rows of table t, 1 <= rows[t] < 2^31.
  *   dim               row width d: 16, 32, 64, 128 or 256.
+ *   precision         EMB_FP16, EMB_INT8, EMB_INT4 or EMB_INT2; sb_dtype
+ *                     (EMB_SB_FP32 or EMB_SB_FP16) applies to integer codes.
  *   cache_fraction    FP32 cache rows per table = floor(cache_fraction*rows[t]),
  *                     grouped in n_sets = max(1, floor(that / assoc)) sets;
  *                     0 disables the cache (every row bypasses).
@@ -182,17 +187,20 @@ int emb_cache_get_stats(emb_cache_t h, int32_t table, int64_t* out, void* stream
 int emb_cache_check(emb_cache_t h, void* stream);
 
 /* Copy rows [row0, row0+n) of table `table` to host buffers, in the canonical
- * layout: codes uint8 [n][dim] (one code per byte), scale and bias FP32 [n]
- * (FP16 values widened exactly when sb_dtype is FP16), LFU counts int32 [n],
- * Adagrad accumulators FP32 [n].  A NULL buffer is skipped; counts and Adagrad
- * state read as 0 when the configuration has none.  Synchronizes `stream`. */
-int emb_cache_export_rows(emb_cache_t h, int32_t table, int64_t row0, int64_t n, uint8_t* codes, float* scale,
+ * layout: codes uint8 [n][dim] (one code per byte; for an FP16 table uint16
+ * [n][dim], the binary16 bit patterns), scale and bias FP32 [n] (FP16 values
+ * widened exactly when sb_dtype is FP16; 0 for an FP16 table), LFU counts int32
+ * [n], Adagrad accumulators FP32 [n].  A NULL buffer is skipped; counts and
+ * Adagrad state read as 0 when the configuration has none.  Synchronizes
+ * `stream`. */
+int emb_cache_export_rows(emb_cache_t h, int32_t table, int64_t row0, int64_t n, void* codes, float* scale,
                           float* bias, int32_t* lfu_count, float* adagrad, void* stream);
 
-/* Inverse of emb_cache_export_rows (host buffers in the same layout; codes
- * must be <= 2^precision-1, FP16 scale/bias must be FP16-representable).
+/* Inverse of emb_cache_export_rows (host buffers in the same layout; integer
+ * codes must be <= 2^precision-1, FP16 scale/bias must be FP16-representable;
+ * an FP16 table takes its codes alone, scale and bias may be NULL).
  * Synchronizes `stream`. */
-int emb_cache_import_rows(emb_cache_t h, int32_t table, int64_t row0, int64_t n, const uint8_t* codes,
+int emb_cache_import_rows(emb_cache_t h, int32_t table, int64_t row0, int64_t n, const void* codes,
                           const float* scale, const float* bias, const int32_t* lfu_count, const float* adagrad,
                           void* stream);
 

@@ -3,7 +3,8 @@
 // Lane layout of one embedding row of width D: a row is handled by a group of
 // LPR = D/8 consecutive lanes (2..32), and lane g of the group holds the 8
 // contiguous columns [8g, 8g+8).  So an FP32 row is two 16-byte loads per lane,
-// the INT4 codes of a lane are one dword (INT8: two), the 8 stochastic-rounding
+// the INT4 codes of a lane are one dword (INT8: two, INT2: a half-word, FP16
+// elements: four dwords), the 8 stochastic-rounding
 // uniforms of a lane are the 8 words of two Philox blocks, and a wave works on
 // 64/LPR rows at once.  The halving-tree sum pairs columns (j, j + h): lanes
 // g and g ^ (h/8) while h >= 8, then inside a lane.
@@ -24,10 +25,13 @@ struct Geo {
   static constexpr int GPW = 64 / LPR; // rows per wave
 };
 
+// A row record of the low-precision table: the codes (BITS 8, 4, 2) followed by the
+// row's (scale, bias), FP16 pair or FP32 pair; or, for BITS 16, the row's binary16
+// elements alone.
 template <int D, int BITS, bool SB16>
 struct Rec {
   static constexpr int CODE_BYTES = D * BITS / 8;
-  static constexpr int BYTES = CODE_BYTES + (SB16 ? 4 : 8);
+  static constexpr int BYTES = CODE_BYTES + (BITS == 16 ? 0 : SB16 ? 4 : 8);
 };
 
 // ---- lane exchange inside a row group ---------------------------------------------------
@@ -94,7 +98,15 @@ __device__ __forceinline__ void uniforms8(uint64_t seed, uint32_t step, uint32_t
   u[4] = u24(b.x); u[5] = u24(b.y); u[6] = u24(b.z); u[7] = u24(b.w);
 }
 
-__device__ __forceinline__ float f16_round(float x) { return __half2float(__float2half(x)); }
+// The compiler may fuse an FP32 multiply-add with a following conversion to FP16
+// (v_fma_mix*), rounding once instead of twice; the empty asm keeps the FP32 value
+// as an operand of its own so that the conversion rounds that value.
+__device__ __forceinline__ float as_f32_value(float x) {
+  asm volatile("" : "+v"(x));
+  return x;
+}
+
+__device__ __forceinline__ float f16_round(float x) { return __half2float(__float2half(as_f32_value(x))); }
 
 // Scale and bias words of a record, loaded raw so that a caller can issue further loads
 // before it converts them (decode_sb).
@@ -107,6 +119,11 @@ template <int D, int BITS, bool SB16>
 __device__ __forceinline__ SbWords<SB16> load_sb_words(const uint8_t* rec) {
   constexpr int CB = Rec<D, BITS, SB16>::CODE_BYTES;
   SbWords<SB16> r;
+  if constexpr (BITS == 16) {  // an FP16 table has no (s, b)
+    r.w[0] = 0u;
+    if constexpr (!SB16) r.w[1] = 0u;
+    return r;
+  }
   const uint32_t* p = reinterpret_cast<const uint32_t*>(rec + CB);
   r.w[0] = p[0];
   if constexpr (!SB16) r.w[1] = p[1];
@@ -129,23 +146,29 @@ __device__ __forceinline__ void load_sb(const uint8_t* rec, float& s, float& b) 
   decode_sb<SB16>(load_sb_words<D, BITS, SB16>(rec), s, b);
 }
 
-// Raw code words of lane g: INT4 one dword (8 nibbles, column 8g+i in nibble i),
-// INT8 two dwords (column 8g+i in byte i).
+// Raw code words of lane g: INT2 one half-word (column 8g+i in bits 2i..2i+1), INT4
+// one dword (column 8g+i in nibble i), INT8 two dwords (column 8g+i in byte i), FP16
+// four dwords (column 8g+i in half i%2 of dword i/2).
 template <int BITS>
 struct CodeWords {
-  uint32_t w[BITS == 8 ? 2 : 1];
+  static constexpr int N = BITS == 16 ? 4 : BITS == 8 ? 2 : 1;  // dwords per lane
+  uint32_t w[N];
 };
 
 template <int BITS, bool NT = false>
 __device__ __forceinline__ CodeWords<BITS> load_code_words(const uint8_t* rec, int g) {
   CodeWords<BITS> c;
-  const uint32_t* p = reinterpret_cast<const uint32_t*>(rec) + g * (BITS == 8 ? 2 : 1);
-  if constexpr (NT) {
-    c.w[0] = __builtin_nontemporal_load(p);
-    if constexpr (BITS == 8) c.w[1] = __builtin_nontemporal_load(p + 1);
+  if constexpr (BITS == 2) {
+    const uint16_t* p = reinterpret_cast<const uint16_t*>(rec) + g;
+    if constexpr (NT) c.w[0] = __builtin_nontemporal_load(p);
+    else c.w[0] = p[0];
   } else {
-    c.w[0] = p[0];
-    if constexpr (BITS == 8) c.w[1] = p[1];
+    const uint32_t* p = reinterpret_cast<const uint32_t*>(rec) + g * CodeWords<BITS>::N;
+#pragma unroll
+    for (int i = 0; i < CodeWords<BITS>::N; ++i) {
+      if constexpr (NT) c.w[i] = __builtin_nontemporal_load(p + i);
+      else c.w[i] = p[i];
+    }
   }
   return c;
 }
@@ -153,13 +176,22 @@ __device__ __forceinline__ CodeWords<BITS> load_code_words(const uint8_t* rec, i
 template <int BITS>
 __device__ __forceinline__ uint32_t code_of(const CodeWords<BITS>& c, int i) {
   if constexpr (BITS == 8) return (c.w[i >> 2] >> (8 * (i & 3))) & 0xFFu;
-  else return (c.w[0] >> (4 * i)) & 0xFu;
+  else if constexpr (BITS == 4) return (c.w[0] >> (4 * i)) & 0xFu;
+  else return (c.w[0] >> (2 * i)) & 0x3u;
 }
 
+// Up-conversion of lane g's 8 elements: q*s + b with one rounding (Alg. 1), or the
+// exact widening of binary16 elements (s, b unused).
 template <int BITS>
 __device__ __forceinline__ void dequant8(const CodeWords<BITS>& c, float s, float b, float (&x)[8]) {
+  if constexpr (BITS == 16) {
 #pragma unroll
-  for (int i = 0; i < 8; ++i) x[i] = __builtin_fmaf((float)code_of<BITS>(c, i), s, b);
+    for (int i = 0; i < 8; ++i)
+      x[i] = __half2float(__ushort_as_half((unsigned short)(c.w[i >> 1] >> (16 * (i & 1)))));
+  } else {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] = __builtin_fmaf((float)code_of<BITS>(c, i), s, b);
+  }
 }
 
 // fetch() of a non-resident row: q*s + b with one rounding (Alg. 1 dequantization).
@@ -202,13 +234,55 @@ __device__ __forceinline__ void store_frow8(float* row, int g, const float (&x)[
   p[1] = make_float4(x[4], x[5], x[6], x[7]);
 }
 
+// The binary16 value next to h in increasing (up) or decreasing order, h finite:
+// magnitudes are ordered like their bit patterns, the sign flips the direction, and
+// both zeros step to the smallest subnormal of the direction.
+__device__ __forceinline__ uint32_t f16_next(uint32_t h, bool up) {
+  const uint32_t sign = h & 0x8000u, mag = h & 0x7FFFu;
+  if (mag == 0) return up ? 0x0001u : 0x8001u;
+  return sign | (((sign == 0) == up) ? mag + 1u : mag - 1u);
+}
+
+// Down-conversion of x into binary16 bits (Sec. 3 "Rounding" with FP16 as the low
+// precision): nearest even (IEEE, overflow to infinity), or stochastic between the
+// consecutive finite values x- <= x <= x+, taking x+ when u < (x - x-)/(x+ - x-)
+// (exact: neighbours differ by a power of two); beyond 65504 stochastic rounding
+// saturates; a representable x or a NaN is kept.
+__device__ __forceinline__ uint32_t f16_bits_round(float x, bool sr, float u) {
+  x = as_f32_value(x);
+  const uint32_t h = (uint32_t)__half_as_ushort(__float2half_rn(x));
+  if (!sr || x != x) return h;
+  if (x > 65504.0f) return 0x7BFFu;
+  if (x < -65504.0f) return 0xFBFFu;
+  const float y = __half2float(__ushort_as_half((unsigned short)h));
+  if (y == x) return h;
+  const uint32_t lo_h = y < x ? h : f16_next(h, false), hi_h = y < x ? f16_next(h, true) : h;
+  const float lo = __half2float(__ushort_as_half((unsigned short)lo_h));
+  const float hi = __half2float(__ushort_as_half((unsigned short)hi_h));
+  return (u < (x - lo) / (hi - lo)) ? hi_h : lo_h;
+}
+
 // Down-conversion of one FP32 row into its low-precision record (Alg. 1 with the
-// Sec. 3 rounding knob).  b = min, s = (max - min)/(2^BITS - 1) (FP32, correctly
-// rounded; then rounded to FP16 when SB16); codes q = round((x - b)/s) clamped to
-// [0, 2^BITS - 1], all zero when s == 0.  A -0 extreme is taken as +0.
+// Sec. 3 rounding knob).  Integer codes: b = min, s = (max - min)/(2^BITS - 1)
+// (FP32, correctly rounded; then rounded to FP16 when SB16); codes
+// q = round((x - b)/s) clamped to [0, 2^BITS - 1], all zero when s == 0; a -0
+// extreme is taken as +0.  FP16 table: each element by f16_bits_round.  A record is
+// written once per step (nontemporal stores).
 template <int D, int BITS, bool SB16>
 __device__ __forceinline__ void quantize_store(const float (&x)[8], int g, uint8_t* rec, bool sr, uint64_t seed,
                                                uint32_t step, uint32_t table, uint32_t row) {
+  if constexpr (BITS == 16) {
+    float u[8];
+    if (sr) uniforms8(seed, step, table, row, g, u);
+    uint32_t* p = reinterpret_cast<uint32_t*>(rec) + 4 * g;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t lo = f16_bits_round(x[2 * i], sr, sr ? u[2 * i] : 0.0f);
+      const uint32_t hi = f16_bits_round(x[2 * i + 1], sr, sr ? u[2 * i + 1] : 0.0f);
+      __builtin_nontemporal_store(lo | (hi << 16), p + i);
+    }
+    return;
+  }
   constexpr int LPR = Geo<D>::LPR;
   constexpr int CB = Rec<D, BITS, SB16>::CODE_BYTES;
   constexpr float K = (float)((1 << BITS) - 1);
@@ -250,12 +324,16 @@ __device__ __forceinline__ void quantize_store(const float (&x)[8], int g, uint8
       if (i < 4) w0 |= q << (8 * i);
       else w1 |= q << (8 * (i - 4));
     } else {
-      w0 |= q << (4 * i);
+      w0 |= q << (BITS * i);
     }
   }
-  uint32_t* p = reinterpret_cast<uint32_t*>(rec) + g * (BITS == 8 ? 2 : 1);
-  __builtin_nontemporal_store(w0, p);  // a record is written once per step
-  if constexpr (BITS == 8) __builtin_nontemporal_store(w1, p + 1);
+  if constexpr (BITS == 2) {
+    __builtin_nontemporal_store((uint16_t)w0, reinterpret_cast<uint16_t*>(rec) + g);
+  } else {
+    uint32_t* p = reinterpret_cast<uint32_t*>(rec) + g * (BITS == 8 ? 2 : 1);
+    __builtin_nontemporal_store(w0, p);
+    if constexpr (BITS == 8) __builtin_nontemporal_store(w1, p + 1);
+  }
   if (g == 0) {
     uint32_t* ps = reinterpret_cast<uint32_t*>(rec + CB);
     if constexpr (SB16) {

@@ -5,15 +5,19 @@
 
 namespace embc {
 
-// Calls fn.template operator()<D, BITS, SB16>() for the runtime triple.
+// Calls fn.template operator()<D, BITS, SB16>() for the runtime triple (BITS 16 is an
+// FP16 table, which has no scale/bias: SB16 is false).
 template <typename Fn>
 hipError_t dispatch_row(int dim, int bits, int sb16, Fn&& fn) {
 #define EMBC_DISPATCH_DIM(DD)                                                            \
   case DD:                                                                               \
+    if (bits == 16) return fn.template operator()<DD, 16, false>();                      \
     if (bits == 8) return sb16 ? fn.template operator()<DD, 8, true>()                   \
                                : fn.template operator()<DD, 8, false>();                 \
     if (bits == 4) return sb16 ? fn.template operator()<DD, 4, true>()                   \
                                : fn.template operator()<DD, 4, false>();                 \
+    if (bits == 2) return sb16 ? fn.template operator()<DD, 2, true>()                   \
+                               : fn.template operator()<DD, 2, false>();                 \
     return hipErrorInvalidValue;
   switch (dim) {
     EMBC_DISPATCH_DIM(16)

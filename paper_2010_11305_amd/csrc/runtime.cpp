@@ -78,7 +78,8 @@ int plan_config(const emb_cache_config* c, Plan* p) {
   if (!c || !p) return EMB_EINVAL;
   if (c->num_tables < 1 || c->num_tables > 65535 || !c->rows) return EMB_EINVAL;
   if (c->dim != 16 && c->dim != 32 && c->dim != 64 && c->dim != 128 && c->dim != 256) return EMB_EINVAL;
-  if (c->precision != EMB_INT8 && c->precision != EMB_INT4) return EMB_EINVAL;
+  if (c->precision != EMB_FP16 && c->precision != EMB_INT8 && c->precision != EMB_INT4 && c->precision != EMB_INT2)
+    return EMB_EINVAL;
   if (c->sb_dtype != EMB_SB_FP32 && c->sb_dtype != EMB_SB_FP16) return EMB_EINVAL;
   if (!(c->cache_fraction >= 0.0) || !std::isfinite(c->cache_fraction)) return EMB_EINVAL;
   if (!is_pow2(c->assoc) || c->assoc > embc::kMaxAssoc) return EMB_EINVAL;
@@ -122,7 +123,8 @@ int plan_config(const emb_cache_config* c, Plan* p) {
   p->total_rows = rows;
   p->total_slots = slots;
   p->total_keys = keys;
-  p->rec_bytes = c->dim * c->precision / 8 + (c->sb_dtype == EMB_SB_FP16 ? 4 : 8);
+  // an FP16 table stores the elements alone; integer codes carry (s, b)
+  p->rec_bytes = c->dim * c->precision / 8 + (c->precision == EMB_FP16 ? 0 : c->sb_dtype == EMB_SB_FP16 ? 4 : 8);
 
   size_t o = 0;
   auto take = [&](size_t bytes) {
@@ -293,7 +295,7 @@ int emb_cache_create(const emb_cache_config* cfg, void* state, size_t state_byte
   d.T = cfg->num_tables;
   d.dim = cfg->dim;
   d.bits = cfg->precision;
-  d.sb16 = cfg->sb_dtype == EMB_SB_FP16;
+  d.sb16 = cfg->precision != EMB_FP16 && cfg->sb_dtype == EMB_SB_FP16;  // an FP16 table has no (s, b)
   d.assoc = cfg->assoc;
   d.rec_bytes = p.rec_bytes;
   d.policy = cfg->policy;
@@ -424,7 +426,7 @@ int emb_cache_check(emb_cache_t h, void* stream) {
   return EMB_OK;
 }
 
-int emb_cache_export_rows(emb_cache_t h, int32_t table, int64_t row0, int64_t n, uint8_t* codes, float* scale,
+int emb_cache_export_rows(emb_cache_t h, int32_t table, int64_t row0, int64_t n, void* codes_out, float* scale,
                           float* bias, int32_t* lfu_count, float* adagrad, void* stream) {
   if (!h || table < 0 || table >= h->cfg.num_tables || row0 < 0 || n < 0) return EMB_EINVAL;
   const TableDesc& td = h->plan.desc[table];
@@ -434,17 +436,24 @@ int emb_cache_export_rows(emb_cache_t h, int32_t table, int64_t row0, int64_t n,
   const int d = h->cfg.dim, RB = h->plan.rec_bytes, bits = h->cfg.precision;
   const int64_t g0 = td.row_base + row0;
   hipError_t e = hipSuccess;
-  if (codes || scale || bias) {
+  if (codes_out || scale || bias) {
     std::vector<uint8_t> buf((size_t)n * RB);
     e = hipMemcpyAsync(buf.data(), h->dev.rec + g0 * RB, buf.size(), hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) return EMB_EHIP;
     const int cb = d * bits / 8;
+    uint8_t* codes = static_cast<uint8_t*>(codes_out);
     for (int64_t i = 0; i < n; ++i) {
       const uint8_t* r = buf.data() + i * RB;
+      if (bits == EMB_FP16) {  // binary16 bit patterns as stored, no (s, b)
+        if (codes) std::memcpy(codes + i * d * 2, r, 2 * (size_t)d);
+        if (scale) scale[i] = 0.0f;
+        if (bias) bias[i] = 0.0f;
+        continue;
+      }
       if (codes) {
-        for (int j = 0; j < d; ++j)
-          codes[i * d + j] = bits == 8 ? r[j] : (uint8_t)((r[j >> 1] >> ((j & 1) * 4)) & 15);
+        const int per = 8 / bits, mask = (1 << bits) - 1;  // codes per byte, column j in bits (j % per) * bits
+        for (int j = 0; j < d; ++j) codes[i * d + j] = (uint8_t)((r[j / per] >> ((j % per) * bits)) & mask);
       }
       float sv, bv;
       if (h->cfg.sb_dtype == EMB_SB_FP16) {
@@ -473,7 +482,7 @@ int emb_cache_export_rows(emb_cache_t h, int32_t table, int64_t row0, int64_t n,
   return hip_status(e);
 }
 
-int emb_cache_import_rows(emb_cache_t h, int32_t table, int64_t row0, int64_t n, const uint8_t* codes,
+int emb_cache_import_rows(emb_cache_t h, int32_t table, int64_t row0, int64_t n, const void* codes_in,
                           const float* scale, const float* bias, const int32_t* lfu_count, const float* adagrad,
                           void* stream) {
   if (!h || table < 0 || table >= h->cfg.num_tables || row0 < 0 || n < 0) return EMB_EINVAL;
@@ -485,18 +494,23 @@ int emb_cache_import_rows(emb_cache_t h, int32_t table, int64_t row0, int64_t n,
   const int64_t g0 = td.row_base + row0;
   hipError_t e = hipSuccess;
   std::vector<uint8_t> buf;
-  if (codes || scale || bias) {
+  const uint8_t* codes = static_cast<const uint8_t*>(codes_in);
+  if (bits == EMB_FP16 && codes) {  // binary16 bit patterns as stored; scale and bias are not used
+    buf.assign((size_t)n * RB, 0);
+    for (int64_t i = 0; i < n; ++i) std::memcpy(buf.data() + i * RB, codes + i * d * 2, 2 * (size_t)d);
+    e = hipMemcpyAsync(h->dev.rec + g0 * RB, buf.data(), buf.size(), hipMemcpyHostToDevice, s);
+  } else if (bits != EMB_FP16 && (codes || scale || bias)) {
     if (!codes || !scale || !bias) return EMB_EINVAL;  // a record is written whole
     const int K = (1 << bits) - 1;
     const int cb = d * bits / 8;
+    const int per = 8 / bits;  // codes per byte, column j in bits (j % per) * bits
     buf.assign((size_t)n * RB, 0);
     for (int64_t i = 0; i < n; ++i) {
       uint8_t* r = buf.data() + i * RB;
       for (int j = 0; j < d; ++j) {
         const uint8_t q = codes[i * d + j];
         if (q > K) return EMB_EINVAL;
-        if (bits == 8) r[j] = q;
-        else r[j >> 1] |= (uint8_t)(q << ((j & 1) * 4));
+        r[j / per] |= (uint8_t)(q << ((j % per) * bits));
       }
       if (h->cfg.sb_dtype == EMB_SB_FP16) {
         const uint16_t hs = float_to_half_bits(scale[i]), hb = float_to_half_bits(bias[i]);

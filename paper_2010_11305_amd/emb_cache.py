@@ -169,6 +169,8 @@ class EmbCache:
         self.cfg = dict(cfg)
         self.T = len(cfg["rows"])
         self.dim = int(cfg["dim"])
+        # exported codes: binary16 bit patterns for an FP16 table, else one code per byte
+        self.code_dtype = np.uint16 if int(cfg["bits"]) == 16 else np.uint8
         self.device = torch.device(device or "cuda")
         self._c, self._keep = make_config(cfg, max_indices, max_batch)
         L = load()
@@ -263,7 +265,7 @@ class EmbCache:
 
     def export_rows(self, t: int, row0: int = 0, n: int | None = None) -> dict:
         n = int(self.cfg["rows"][t]) - row0 if n is None else n
-        codes = np.empty((n, self.dim), dtype=np.uint8)
+        codes = np.empty((n, self.dim), dtype=self.code_dtype)
         scale = np.empty(n, dtype=np.float32)
         bias = np.empty(n, dtype=np.float32)
         cnt = np.empty(n, dtype=np.int32)
@@ -274,8 +276,9 @@ class EmbCache:
 
     def import_rows(self, t: int, row0: int, codes, scale, bias, cnt=None, G=None):
         arrs = [np.ascontiguousarray(a, dtype=dt) if a is not None else None
-                for a, dt in zip([codes, scale, bias, cnt, G], [np.uint8, np.float32, np.float32, np.int32, np.float32])]
-        n = len(arrs[1])
+                for a, dt in zip([codes, scale, bias, cnt, G],
+                                 [self.code_dtype, np.float32, np.float32, np.int32, np.float32])]
+        n = len(next(a for a in arrs if a is not None))
         _check(load().emb_cache_import_rows(self._h, t, row0, n, *[_np(a) for a in arrs], self._stream()),
                "import_rows")
 

@@ -56,6 +56,17 @@ def test_query_sizes_named_configs(lib, name):
     assert s["workspace_bytes"] >= 16 * L
 
 
+@pytest.mark.parametrize("bits,sb16,d,rec", [
+    (16, False, 16, 32), (16, True, 128, 256), (8, False, 16, 24), (4, True, 128, 68), (2, False, 16, 12),
+    (2, True, 256, 68),
+])
+def test_row_record_bytes(lib, bits, sb16, d, rec):
+    """Record = codes (d*bits/8 bytes) + (s, b) (8 bytes FP32, 4 FP16); an FP16 table
+    stores its elements alone."""
+    s = ec.query_sizes(custom_cfg(bits=bits, sb_fp16=sb16, dim=d), 1024)
+    assert s["row_bytes"] == rec
+
+
 @pytest.mark.parametrize("name,over", [
     ("tiny", {}), ("tiny", {"assoc": 1}), ("tiny", {"cache_fraction": 0.0}), ("tiny", {"cache_fraction": 1.024, "assoc": 32}),
     ("kaggle_int8", {}), ("kaggle_int4", {}), ("industrial", {}), ("stress", {}),
@@ -77,7 +88,7 @@ def test_geometry_matches_oracle(lib, name, over):
 
 
 @pytest.mark.parametrize("bad", [
-    {"dim": 24}, {"dim": 512}, {"bits": 2}, {"assoc": 3}, {"assoc": 128}, {"assoc": 0}, {"cache_fraction": -0.1},
+    {"dim": 24}, {"dim": 512}, {"bits": 1}, {"bits": 32}, {"bits": 12}, {"assoc": 3}, {"assoc": 128}, {"assoc": 0}, {"cache_fraction": -0.1},
     {"cache_fraction": float("nan")}, {"rows": [0]}, {"rows": [2**31]}, {"rows": []}, {"policy": "fifo"},
     {"lfu_decay_interval": -1}, {"eps": -1.0}, {"lr": float("inf")},
 ])

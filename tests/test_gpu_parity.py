@@ -20,7 +20,8 @@ def torch():
     return t
 
 
-INIT_CASES = [(d, b, sb) for d in (16, 32, 64, 128, 256) for b in (8, 4) for sb in (False, True)]
+INIT_CASES = ([(d, b, sb) for d in (16, 32, 64, 128, 256) for b in (8, 4, 2) for sb in (False, True)]
+              + [(d, 16, False) for d in (16, 32, 64, 128, 256)])
 
 
 @pytest.mark.parametrize("dim,bits,sb16", INIT_CASES)
@@ -31,10 +32,11 @@ def test_init_uniform_parity(torch, dim, bits, sb16):
     compare_state(o, g, cfg)
 
 
-def test_forward_from_imported_state(torch):
+@pytest.mark.parametrize("over", [{}, {"bits": 16, "rounding": "stochastic"}, {"bits": 2, "sb_fp16": True}])
+def test_forward_from_imported_state(torch, over):
     """Oracle trains 4 steps; its state is imported into the GPU; pooled outputs match."""
-    cfg = configs.get("tiny")
-    log("forward from imported oracle state")
+    cfg = custom_cfg(**over)
+    log(f"forward from imported oracle state {over}")
     o, g = make_pair(cfg)
     for k in range(4):
         st = workload.make_step(cfg, k)
@@ -70,6 +72,18 @@ STEP_CASES = {
                              "rounding": "stochastic", "optimizer": "adagrad", "pooling": ("poisson", 30), "zipf": 1.2},
     "d256_int8_sr": {"dim": 256, "rounding": "stochastic", "assoc": 32, "cache_fraction": 0.1, "lr": 0.05},
     "hot_row": {"rows": [300], "zipf": 2.0, "batch": 600, "pooling": ("uniform", 1, 8), "assoc": 8},
+    "assoc64": {"assoc": 64, "cache_fraction": 0.3, "batch": 300, "pooling": ("uniform", 1, 12)},
+    "fp16_rne": {"bits": 16},
+    "fp16_sr_lfu_adagrad": {"bits": 16, "rounding": "stochastic", "policy": "lfu", "optimizer": "adagrad",
+                            "lfu_decay_interval": 3},
+    "fp16_direct_mapped_lfu": {"bits": 16, "assoc": 1, "policy": "lfu", "rounding": "stochastic"},
+    "d128_fp16_sr_lru16": {"dim": 128, "bits": 16, "rounding": "stochastic", "assoc": 16, "cache_fraction": 0.05,
+                           "pooling": ("poisson", 30), "zipf": 1.2},
+    "int2_rne": {"bits": 2},
+    "d64_int2_fp16sb_sr_adagrad": {"dim": 64, "bits": 2, "sb_fp16": True, "rounding": "stochastic",
+                                   "optimizer": "adagrad"},
+    "d256_int2_sr_assoc32": {"dim": 256, "bits": 2, "rounding": "stochastic", "assoc": 32, "cache_fraction": 0.1},
+    "int2_nocache_sr": {"bits": 2, "cache_fraction": 0.0, "rounding": "stochastic"},
     "multi_table": {"rows": [1000, 5, 64, 3000], "batch": 96, "assoc": 4, "cache_fraction": 0.05},
 }
 
