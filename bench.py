@@ -56,11 +56,18 @@ def measured_update_traffic():
         return None
 
 
+def record_bytes(cfg):
+    """rho: bytes of one row of the low-precision table (codes + (s,b), or FP16 elements)."""
+    if cfg["bits"] == 16:
+        return 2 * cfg["dim"]
+    return cfg["dim"] * cfg["bits"] // 8 + (4 if cfg["sb_fp16"] else 8)
+
+
 def describe(cfg):
     T, N = len(cfg["rows"]), cfg["rows"][0]
     pool = cfg["pooling"]
-    return (f"{cfg['name']}: {T} tables x {N} rows x d{cfg['dim']} INT{cfg['bits']} + "
-            f"{'FP16' if cfg['sb_fp16'] else 'FP32'} (s,b); FP32 cache {cfg['cache_fraction']:.0%} "
+    prec = "FP16" if cfg["bits"] == 16 else f"INT{cfg['bits']} + {'FP16' if cfg['sb_fp16'] else 'FP32'} (s,b)"
+    return (f"{cfg['name']}: {T} tables x {N} rows x d{cfg['dim']} {prec}; FP32 cache {cfg['cache_fraction']:.0%} "
             f"{cfg['assoc']}-way {cfg['policy'].upper()}; B={cfg['batch']} bags/table, pooling {pool}; "
             f"Zipf {cfg['zipf']}; {cfg['optimizer']} lr {cfg['lr']}; {cfg['rounding']} rounding")
 
@@ -77,7 +84,7 @@ def algorithmic_bytes(cfg, st, B, decay_step=False):
     """
     d = cfg["dim"]
     phi = 4 * d
-    rho = d * cfg["bits"] // 8 + (4 if cfg["sb_fp16"] else 8)
+    rho = record_bytes(cfg)
     L, U, Uh = st["bwd_lookups"], st["unique"], st["unique_hits"]
     Um = U - Uh
     Eh, Ubyp, Uins = st["hit_evictions"], st["bypasses"], st["inserts"]
@@ -106,7 +113,7 @@ def update_kernel_bytes(cfg, st):
     """
     d = cfg["dim"]
     phi = 4 * d
-    rho = d * cfg["bits"] // 8 + (4 if cfg["sb_fp16"] else 8)
+    rho = record_bytes(cfg)
     U, Uh, Eh = st["unique"], st["unique_hits"], st["hit_evictions"]
     Uins, Ubyp = st["inserts"], st["bypasses"]
     rows = U - Eh
@@ -121,7 +128,7 @@ def cpu_baseline(cfg, steps, budget_s):
     """The CPU oracle on one table of the workload (table 0), single thread."""
     import oracle  # test infrastructure: only this leg of the benchmark loads it
 
-    one = configs.get(cfg["name"], rows=[cfg["rows"][0]])
+    one = dict(cfg, rows=[cfg["rows"][0]])
     o = oracle.Oracle(one["rows"], one["dim"], one["bits"], one["sb_fp16"], one["cache_fraction"], one["assoc"],
                       one["policy"], one.get("lfu_decay_interval", 0), one["rounding"] == "stochastic",
                       one["optimizer"] == "adagrad", one["lr"], one["eps"], one["seed"])
@@ -152,6 +159,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="industrial")
+    ap.add_argument("--set", action="append", default=[], metavar="KEY=VALUE",
+                    help="override a field of the named workload (e.g. bits=16); int, float or text")
     ap.add_argument("--pool", type=int, default=3, help="distinct input batches cycled through")
     ap.add_argument("--stats-steps", type=int, default=3)
     ap.add_argument("--cpu-steps", type=int, default=20)
@@ -168,7 +177,17 @@ def main():
     import torch
     from paper_2010_11305_amd.emb_cache import EmbCache
 
-    cfg = configs.get(args.config)
+    over = {}
+    for kv in args.set:
+        k, v = kv.split("=", 1)
+        for conv in (int, float):
+            try:
+                v = conv(v)
+                break
+            except ValueError:
+                pass
+        over[k] = v
+    cfg = configs.get(args.config, **over)
     T, B, d = len(cfg["rows"]), cfg["batch"], cfg["dim"]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
