@@ -8,6 +8,10 @@ the CPU oracle and the HIP library are fed the arrays it returns.
   rejection-inversion (Hormann & Derflinger, 1996), then scattered over row ids
   by a seeded affine bijection row = (a*(rank-1) + c) mod N_t with gcd(a, N_t) = 1,
   so the hottest rows are not clustered in the low row ids or in one cache set.
+* Popularity drift (optional, cfg["drift"] = (period, fraction)): the offset c of
+  the bijection moves by fraction*N_t every `period` steps, so each popular row
+  stays popular for a phase of `period` steps and then gives way to another one
+  (the "data shift" of the paper's internal data, Sec. 5.2).
 * Bag lengths: uniform U{lo..hi}, fixed, or Poisson(mean), per (table, bag).
 * Offsets: int32 [T*B + 1], table-major (all bags of table 0, then table 1, ...).
 * Output gradients: N(0, sigma) FP32 of shape [B][T][d].
@@ -100,6 +104,10 @@ def table_indices(cfg: dict, step: int, table: int, n: int, sampler: ZipfSampler
     sampler = sampler or ZipfSampler(N, cfg["zipf"])
     ranks = sampler.sample(_rng(cfg["index_seed"], step, table, 2), n)
     a, c = affine_bijection(cfg["index_seed"], table, N)
+    drift = cfg.get("drift")
+    if drift:
+        period, fraction = drift
+        c = (c + (step // int(period)) * int(fraction * N)) % N
     return ((a * (ranks - 1) + c) % N).astype(np.int32)
 
 

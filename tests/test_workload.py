@@ -53,3 +53,22 @@ def test_industrial_single_table_slice():
     assert 0.9 * 30 * B < L < 1.1 * 30 * B
     u, c = np.unique(idx, return_counts=True)
     assert 0.05 < c.max() / L < 0.4          # Zipf 1.2 top row takes a large share
+
+
+def test_drift_moves_the_hot_rows_between_phases():
+    """With drift (period P, fraction f), the hottest rows are the same within a phase
+    and move by f*N row ids (through the bijection) at a phase boundary."""
+    cfg = configs.get("tiny", rows=[10000], batch=4096, pooling=("fixed", 1), zipf=1.2, drift=(5, 0.25))
+    top = []
+    for k in (0, 4, 5, 9, 10):
+        idx, _ = workload.make_indices(cfg, k)
+        v, c = np.unique(idx, return_counts=True)
+        top.append(set(v[np.argsort(-c)[:20]].tolist()))
+    assert len(top[0] & top[1]) >= 15 and len(top[2] & top[3]) >= 15      # same phase
+    assert len(top[0] & top[2]) <= 2 and len(top[2] & top[4]) <= 2        # next phase
+    # the hottest rank maps to a + c' mod N with c' moved by 2500 per phase
+    a, c = workload.affine_bijection(cfg["index_seed"], 0, 10000)
+    assert {c % 10000, (c + 2500) % 10000, (c + 5000) % 10000} <= top[0] | top[2] | top[4]
+    # without drift the stream is unchanged
+    base = configs.get("tiny", rows=[10000], batch=4096, pooling=("fixed", 1), zipf=1.2)
+    assert np.array_equal(workload.make_indices(base, 3)[0], workload.make_indices(dict(base, drift=None), 3)[0])
