@@ -159,6 +159,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="industrial")
+    ap.add_argument("--table", choices=("device", "host"), default="device",
+                    help="where the low-precision table lives (host: pinned host memory over the host link)")
     ap.add_argument("--set", action="append", default=[], metavar="KEY=VALUE",
                     help="override a field of the named workload (e.g. bits=16); int, float or text")
     ap.add_argument("--pool", type=int, default=3, help="distinct input batches cycled through")
@@ -211,7 +213,7 @@ def main():
     grads = [torch.randn((B, T, d), generator=gen, device=dev, dtype=torch.float32) * cfg["grad_sigma"]
              for _ in range(2)]
     max_idx = max(p[2] for p in pool)
-    emb = EmbCache(cfg, max_indices=max_idx)
+    emb = EmbCache(cfg, max_indices=max_idx, table=args.table)
     emb.init_uniform(cfg["init_lo"], cfg["init_hi"], cfg["init_seed"])
     out = torch.empty((B, T, d), dtype=torch.float32, device=dev)
     torch.cuda.synchronize()
@@ -291,7 +293,8 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": describe(cfg), "global_batch": B, "tables": T, "lookups_per_step": lookups / args.steps},
+        "config": {"workload": describe(cfg), "global_batch": B, "tables": T, "lookups_per_step": lookups / args.steps,
+                   "table_memory": args.table},
         "hbm_gbps_algorithmic": gbs,
         "hbm_frac_of_peak": gbs / HBM_PEAK_GBS,
         "bytes_per_step_algorithmic": step_bytes,

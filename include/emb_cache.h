@@ -122,6 +122,7 @@ typedef struct emb_cache_sizes {
   int64_t total_slots;    /* sum over tables of n_sets*assoc */
   int32_t row_bytes;      /* bytes of one low-precision row record (codes + scale + bias) */
   int32_t pad;
+  size_t table_bytes;     /* the low-precision table: the last table_bytes of state_bytes */
 } emb_cache_sizes;
 
 typedef struct emb_cache* emb_cache_t;
@@ -140,6 +141,17 @@ int emb_cache_table_geometry(const emb_cache_config* cfg, int32_t table, int64_t
  * all codes/scale/bias 0; sets step = 0.  Synchronizes `stream`. */
 int emb_cache_create(const emb_cache_config* cfg, void* state, size_t state_bytes, void* workspace,
                      size_t workspace_bytes, void* stream, emb_cache_t* out);
+
+/* As emb_cache_create, with the low-precision table in a buffer of its own:
+ * `table` (table_bytes >= the queried table_bytes, 256-byte aligned) is device
+ * memory, or pinned host memory from hipHostMalloc, which the kernels then reach
+ * over the host link -- the paper's table in unified memory with the FP32 cache
+ * in device memory (Sec. 5.3, Fig. 7).  `state` then needs only state_bytes -
+ * table_bytes.  Any other host memory is refused (EMB_EINVAL): a kernel could not
+ * reach it.  Synchronizes `stream`. */
+int emb_cache_create_with_table(const emb_cache_config* cfg, void* state, size_t state_bytes, void* table,
+                                size_t table_bytes, void* workspace, size_t workspace_bytes, void* stream,
+                                emb_cache_t* out);
 
 /* Release host metadata.  Does not touch device memory. */
 int emb_cache_destroy(emb_cache_t h);

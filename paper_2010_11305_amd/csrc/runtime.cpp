@@ -63,7 +63,7 @@ struct Plan {
   std::vector<TableDesc> desc;
   std::vector<int64_t> key_base;
   // state offsets
-  size_t o_rec, o_crow, o_tag, o_ts, o_cnt, o_G, o_desc, o_keyb, o_stats, o_err, state_bytes;
+  size_t o_rec, o_crow, o_tag, o_ts, o_cnt, o_G, o_desc, o_keyb, o_stats, o_err, state_bytes, table_bytes;
   // workspace offsets
   size_t o_kA, o_vA, o_kB, o_vB, o_ssmall, o_sst0, o_sst1, o_part, o_tcnt, o_tpre, o_uk, o_seg, o_setf, o_urow, o_utab, o_uslot,
       o_uact, o_udest, o_umeta, o_nch, o_cbase, o_uvrow, o_uvu, o_partial, o_span, o_ubig, o_brows, o_bbound, o_bpart, o_tabf, o_src, o_ctr, ws_bytes;
@@ -133,7 +133,6 @@ int plan_config(const emb_cache_config* c, Plan* p) {
     return at;
   };
   const bool lru = c->policy == EMB_LRU, lfu = c->policy == EMB_LFU;
-  p->o_rec = take((size_t)rows * p->rec_bytes);
   p->o_crow = take((size_t)slots * c->dim * 4);
   p->o_tag = take((size_t)slots * 4);
   p->o_ts = take(lru ? (size_t)slots * 4 : 0);
@@ -143,6 +142,9 @@ int plan_config(const emb_cache_config* c, Plan* p) {
   p->o_keyb = take(sizeof(int64_t) * (T + 1));
   p->o_stats = take(sizeof(unsigned long long) * T * embc::kNStat);
   p->o_err = take(kAlign);
+  // the low-precision table comes last: a caller may place it in a buffer of its own
+  p->o_rec = take((size_t)rows * p->rec_bytes);
+  p->table_bytes = o - p->o_rec;
   p->state_bytes = o;
 
   const size_t L = (size_t)c->max_indices;
@@ -239,6 +241,7 @@ int emb_cache_query_sizes(const emb_cache_config* cfg, emb_cache_sizes* out) {
   out->total_slots = p.total_slots;
   out->row_bytes = p.rec_bytes;
   out->pad = 0;
+  out->table_bytes = p.table_bytes;
   return EMB_OK;
 }
 
@@ -252,8 +255,52 @@ int emb_cache_table_geometry(const emb_cache_config* cfg, int32_t table, int64_t
   return EMB_OK;
 }
 
+namespace {
+
+// The device address of a caller's table buffer: device memory as it is, pinned host
+// memory (hipHostMalloc) through its device mapping; anything else is refused, since
+// a kernel could not reach it.
+int table_device_address(void* table, uint8_t** dev) {
+  hipPointerAttribute_t a{};
+  if (hipPointerGetAttributes(&a, table) != hipSuccess) {
+    (void)hipGetLastError();
+    return EMB_EINVAL;
+  }
+  if (a.type == hipMemoryTypeDevice) {
+    *dev = static_cast<uint8_t*>(table);
+    return EMB_OK;
+  }
+  if (a.type == hipMemoryTypeHost && a.devicePointer) {
+    *dev = static_cast<uint8_t*>(a.devicePointer);
+    return EMB_OK;
+  }
+  return EMB_EINVAL;
+}
+
+int create_impl(const emb_cache_config* cfg, void* state, size_t state_bytes, void* table, size_t table_bytes,
+                void* workspace, size_t workspace_bytes, void* stream, emb_cache_t* out);
+
+}  // namespace
+
 int emb_cache_create(const emb_cache_config* cfg, void* state, size_t state_bytes, void* workspace,
                      size_t workspace_bytes, void* stream, emb_cache_t* out) {
+  return create_impl(cfg, state, state_bytes, nullptr, 0, workspace, workspace_bytes, stream, out);
+}
+
+int emb_cache_create_with_table(const emb_cache_config* cfg, void* state, size_t state_bytes, void* table,
+                                size_t table_bytes, void* workspace, size_t workspace_bytes, void* stream,
+                                emb_cache_t* out) {
+  if (!table) {
+    if (out) *out = nullptr;
+    return EMB_EINVAL;
+  }
+  return create_impl(cfg, state, state_bytes, table, table_bytes, workspace, workspace_bytes, stream, out);
+}
+
+namespace {
+
+int create_impl(const emb_cache_config* cfg, void* state, size_t state_bytes, void* table, size_t table_bytes,
+                void* workspace, size_t workspace_bytes, void* stream, emb_cache_t* out) {
   if (!out) return EMB_EINVAL;
   *out = nullptr;
   emb_cache* h = new (std::nothrow) emb_cache();
@@ -265,13 +312,20 @@ int emb_cache_create(const emb_cache_config* cfg, void* state, size_t state_byte
   }
   const Plan& p = h->plan;
   if (!state || !workspace || (reinterpret_cast<uintptr_t>(state) % kAlign) ||
-      (reinterpret_cast<uintptr_t>(workspace) % kAlign)) {
+      (reinterpret_cast<uintptr_t>(workspace) % kAlign) || (reinterpret_cast<uintptr_t>(table) % kAlign)) {
     delete h;
     return EMB_EINVAL;
   }
-  if (state_bytes < p.state_bytes || workspace_bytes < p.ws_bytes) {
+  // with a table buffer of its own, the state buffer holds everything before the table
+  const size_t need_state = table ? p.o_rec : p.state_bytes;
+  if (state_bytes < need_state || workspace_bytes < p.ws_bytes || (table && table_bytes < p.table_bytes)) {
     delete h;
     return EMB_ENOMEM;
+  }
+  uint8_t* table_dev = nullptr;
+  if (table && table_device_address(table, &table_dev) != EMB_OK) {
+    delete h;
+    return EMB_EINVAL;
   }
   h->cfg = *cfg;
   h->rows.assign(cfg->rows, cfg->rows + cfg->num_tables);
@@ -282,7 +336,7 @@ int emb_cache_create(const emb_cache_config* cfg, void* state, size_t state_byte
 
   uint8_t* sb = static_cast<uint8_t*>(state);
   embc::Dev& d = h->dev;
-  d.rec = sb + p.o_rec;
+  d.rec = table ? table_dev : sb + p.o_rec;
   d.crow = reinterpret_cast<float*>(sb + p.o_crow);
   d.tag = reinterpret_cast<int32_t*>(sb + p.o_tag);
   d.ts = cfg->policy == EMB_LRU ? reinterpret_cast<int32_t*>(sb + p.o_ts) : nullptr;
@@ -363,6 +417,8 @@ int emb_cache_create(const emb_cache_config* cfg, void* state, size_t state_byte
   return EMB_OK;
 }
 
+}  // namespace
+
 int emb_cache_destroy(emb_cache_t h) {
   delete h;
   return EMB_OK;
@@ -438,7 +494,7 @@ int emb_cache_export_rows(emb_cache_t h, int32_t table, int64_t row0, int64_t n,
   hipError_t e = hipSuccess;
   if (codes_out || scale || bias) {
     std::vector<uint8_t> buf((size_t)n * RB);
-    e = hipMemcpyAsync(buf.data(), h->dev.rec + g0 * RB, buf.size(), hipMemcpyDeviceToHost, s);
+    e = hipMemcpyAsync(buf.data(), h->dev.rec + g0 * RB, buf.size(), hipMemcpyDefault, s);  // device or pinned host table
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) return EMB_EHIP;
     const int cb = d * bits / 8;
@@ -498,7 +554,7 @@ int emb_cache_import_rows(emb_cache_t h, int32_t table, int64_t row0, int64_t n,
   if (bits == EMB_FP16 && codes) {  // binary16 bit patterns as stored; scale and bias are not used
     buf.assign((size_t)n * RB, 0);
     for (int64_t i = 0; i < n; ++i) std::memcpy(buf.data() + i * RB, codes + i * d * 2, 2 * (size_t)d);
-    e = hipMemcpyAsync(h->dev.rec + g0 * RB, buf.data(), buf.size(), hipMemcpyHostToDevice, s);
+    e = hipMemcpyAsync(h->dev.rec + g0 * RB, buf.data(), buf.size(), hipMemcpyDefault, s);
   } else if (bits != EMB_FP16 && (codes || scale || bias)) {
     if (!codes || !scale || !bias) return EMB_EINVAL;  // a record is written whole
     const int K = (1 << bits) - 1;
@@ -522,7 +578,7 @@ int emb_cache_import_rows(emb_cache_t h, int32_t table, int64_t row0, int64_t n,
         std::memcpy(r + cb + 4, &bias[i], 4);
       }
     }
-    e = hipMemcpyAsync(h->dev.rec + g0 * RB, buf.data(), buf.size(), hipMemcpyHostToDevice, s);
+    e = hipMemcpyAsync(h->dev.rec + g0 * RB, buf.data(), buf.size(), hipMemcpyDefault, s);
   }
   if (e == hipSuccess && lfu_count && h->dev.cnt)
     e = hipMemcpyAsync(h->dev.cnt + g0, lfu_count, 4 * (size_t)n, hipMemcpyHostToDevice, s);

@@ -58,6 +58,7 @@ class Sizes(ctypes.Structure):
         ("total_slots", ctypes.c_int64),
         ("row_bytes", ctypes.c_int32),
         ("pad", ctypes.c_int32),
+        ("table_bytes", ctypes.c_size_t),
     ]
 
 
@@ -78,6 +79,8 @@ def load():
         "emb_cache_query_sizes": [c.POINTER(Config), c.POINTER(Sizes)],
         "emb_cache_table_geometry": [c.POINTER(Config), i32, c.POINTER(i64), c.POINTER(i64)],
         "emb_cache_create": [c.POINTER(Config), P, c.c_size_t, P, c.c_size_t, P, c.POINTER(P)],
+        "emb_cache_create_with_table": [c.POINTER(Config), P, c.c_size_t, P, c.c_size_t, P, c.c_size_t, P,
+                                        c.POINTER(P)],
         "emb_cache_destroy": [P],
         "emb_cache_init_uniform": [P, f32, f32, u64, P],
         "emb_cache_forward": [P, P, i64, P, i32, P, P],
@@ -144,7 +147,7 @@ def query_sizes(cfg: dict, max_indices: int, max_batch: int | None = None) -> di
     _check(load().emb_cache_query_sizes(ctypes.byref(c), ctypes.byref(s)), "emb_cache_query_sizes")
     del keep
     return {"state_bytes": s.state_bytes, "workspace_bytes": s.workspace_bytes, "total_rows": s.total_rows,
-            "total_slots": s.total_slots, "row_bytes": s.row_bytes}
+            "total_slots": s.total_slots, "row_bytes": s.row_bytes, "table_bytes": s.table_bytes}
 
 
 def _np(a):
@@ -160,9 +163,13 @@ class EmbCache:
 
     forward(indices, offsets, batch) -> pooled [batch][T][dim] FP32 (torch, device)
     backward_update(indices, offsets, batch, grad_out)
+
+    table="host" puts the low-precision table in pinned host memory (torch
+    pin_memory, i.e. hipHostMalloc) that the kernels reach over the host link; the
+    FP32 cache and everything else stay in device memory.
     """
 
-    def __init__(self, cfg: dict, max_indices: int, max_batch: int | None = None, device=None):
+    def __init__(self, cfg: dict, max_indices: int, max_batch: int | None = None, device=None, table="device"):
         import torch
 
         self.torch = torch
@@ -177,11 +184,27 @@ class EmbCache:
         s = Sizes()
         _check(L.emb_cache_query_sizes(ctypes.byref(self._c), ctypes.byref(s)), "emb_cache_query_sizes")
         self.sizes = s
-        self.state = torch.empty(max(int(s.state_bytes), 256), dtype=torch.uint8, device=self.device)
         self.workspace = torch.empty(max(int(s.workspace_bytes), 256), dtype=torch.uint8, device=self.device)
         h = ctypes.c_void_p()
-        _check(L.emb_cache_create(ctypes.byref(self._c), _dptr(self.state), s.state_bytes, _dptr(self.workspace),
-                                  s.workspace_bytes, self._stream(), ctypes.byref(h)), "emb_cache_create")
+        if table == "device":
+            self.state = torch.empty(max(int(s.state_bytes), 256), dtype=torch.uint8, device=self.device)
+            self.table = None
+            _check(L.emb_cache_create(ctypes.byref(self._c), _dptr(self.state), s.state_bytes,
+                                      _dptr(self.workspace), s.workspace_bytes, self._stream(), ctypes.byref(h)),
+                   "emb_cache_create")
+        elif table == "host":
+            core = int(s.state_bytes - s.table_bytes)
+            self.state = torch.empty(max(core, 256), dtype=torch.uint8, device=self.device)
+            # 256 bytes of slack so that the table can start on a 256-byte boundary
+            self._table_mem = torch.empty(int(s.table_bytes) + 256, dtype=torch.uint8, pin_memory=True)
+            skip = (-self._table_mem.data_ptr()) % 256
+            self.table = self._table_mem[skip:skip + int(s.table_bytes)]
+            _check(L.emb_cache_create_with_table(ctypes.byref(self._c), _dptr(self.state), core,
+                                                 ctypes.c_void_p(self.table.data_ptr()), s.table_bytes,
+                                                 _dptr(self.workspace), s.workspace_bytes, self._stream(),
+                                                 ctypes.byref(h)), "emb_cache_create_with_table")
+        else:
+            raise ValueError(f"table must be 'device' or 'host', not {table!r}")
         self._h = h
         self.n_sets, self.slots = [], []
         for t in range(self.T):

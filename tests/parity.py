@@ -64,13 +64,13 @@ def to_dev(st, torch):
             torch.from_numpy(st["grad"]).cuda())
 
 
-def make_pair(cfg, max_indices=None):
+def make_pair(cfg, max_indices=None, table="device"):
     from paper_2010_11305_amd.emb_cache import EmbCache
     o = oracle_from_cfg(cfg)
     o.init_uniform(cfg["init_lo"], cfg["init_hi"], cfg["init_seed"])
     if max_indices is None:
         max_indices = max(1, int(workload.make_indices(cfg, 0)[0].size * 2 + 64))
-    g = EmbCache(cfg, max_indices=max_indices)
+    g = EmbCache(cfg, max_indices=max_indices, table=table)
     g.init_uniform(cfg["init_lo"], cfg["init_hi"], cfg["init_seed"])
     return o, g
 

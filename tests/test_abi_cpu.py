@@ -52,6 +52,8 @@ def test_query_sizes_named_configs(lib, name):
     N = sum(cfg["rows"])
     rec = cfg["dim"] * cfg["bits"] // 8 + (4 if cfg["sb_fp16"] else 8)
     assert s["row_bytes"] == rec and s["total_rows"] == N
+    # the table is the last part of the state, padded to 256 bytes
+    assert N * rec <= s["table_bytes"] < N * rec + 256 and s["table_bytes"] < s["state_bytes"]
     assert s["state_bytes"] >= N * rec + s["total_slots"] * (4 * cfg["dim"] + 4)
     assert s["workspace_bytes"] >= 16 * L
 
@@ -139,3 +141,11 @@ def test_null_handle_rejected(lib):
     assert lib.emb_cache_backward_update(None, None, 0, None, 0, None, None) == ec.EMB_EINVAL
     assert lib.emb_cache_check(None, None) == ec.EMB_EINVAL
     assert lib.emb_cache_destroy(None) == 0
+
+
+def test_create_with_table_rejects_null_table(lib):
+    c, keep = ec.make_config(custom_cfg(), 1024)
+    h = ctypes.c_void_p(1)
+    st = lib.emb_cache_create_with_table(ctypes.byref(c), ctypes.c_void_p(256), 1 << 20, None, 1 << 20,
+                                         ctypes.c_void_p(256), 1 << 20, None, ctypes.byref(h))
+    assert st == ec.EMB_EINVAL and not h.value

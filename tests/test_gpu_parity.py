@@ -102,6 +102,23 @@ def test_step_parity(torch, case):
         assert s["inserts"] + s["unique_hits"] > 0
 
 
+HOST_TABLE_CASES = ["tiny", "tiny_int4_fp16_lfu_adagrad", "fp16_sr_lfu_adagrad", "d128_int4_fp16_lru16",
+                    "tiny_nocache", "d64_int2_fp16sb_sr_adagrad"]
+
+
+@pytest.mark.parametrize("case", HOST_TABLE_CASES)
+def test_step_parity_host_table(torch, case):
+    """The low-precision table in pinned host memory (reached over the host link), the
+    cache in device memory: the same bits as the oracle."""
+    cfg = custom_cfg(**STEP_CASES[case])
+    log(f"host-table step parity {case}")
+    o, g = make_pair(cfg, table="host")
+    assert g.table is not None and g.table.is_pinned()
+    for k in range(6):
+        step_both(o, g, cfg, workload.make_step(cfg, k), torch)
+        compare_state(o, g, cfg)
+
+
 def _bags_of(rows, per_bag, rng):
     rows = np.array(rows, dtype=np.int32)
     rng.shuffle(rows)
