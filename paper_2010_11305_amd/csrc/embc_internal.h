@@ -128,6 +128,7 @@ enum : int {
   kCScanTotal = 6,  // scratch total of the last scan
   kCBadOffsets = 7, // offsets of this step failed validation
   kCBig = 8,        // big rows
+  kCHitEv = 9,      // inserts displacing a resident updated this step
   kNCounters = 16
 };
 
@@ -137,10 +138,18 @@ hipError_t launch_reset_state(const Dev& d, hipStream_t s);
 hipError_t launch_init_uniform(const Dev& d, float lo, float hi, uint64_t init_seed, hipStream_t s);
 hipError_t launch_forward(const Dev& d, const Work& w, const int32_t* idx, int64_t L, const int32_t* off,
                           int32_t B, float* out, hipStream_t s);
+// A second stream of the handle and two events: the replacement decisions and the
+// write-back of displaced residents run there while the merged gradients are summed
+// on the caller's stream.
+struct SideStream {
+  hipStream_t s = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+};
+
 // update_events: nullptr, or two events recorded on `s` around the row-update kernel.
 hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int64_t L, const int32_t* off,
                            int32_t B, const float* grad, uint64_t step, int key_bits, bool decay,
-                           const hipEvent_t* update_events, hipStream_t s);
+                           const hipEvent_t* update_events, const SideStream& side, hipStream_t s);
 
 size_t sort_status_words(int64_t n);
 constexpr size_t kSortSmallWords = 2 * kMaxPasses * 256 + 64;

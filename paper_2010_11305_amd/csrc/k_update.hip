@@ -735,6 +735,7 @@ __global__ __launch_bounds__(256) void k_policy(Dev dv, Work w, uint32_t step) {
     }
     const uint32_t n_valid = (uint32_t)__popcll(__ballot(lane < n_ins && my_old >= 0));
     const uint32_t n_hitev = (uint32_t)__popcll(__ballot(lane < n_ins && my_hu >= 0));
+    if (lane == 0 && n_hitev) atomicAdd(&w.ctr[kCHitEv], (unsigned long long)n_hitev);
     if (lane == 0) {
       ps.ins += (uint32_t)n_ins;
       ps.byp += (uint32_t)(M - n_ins);
@@ -747,9 +748,14 @@ __global__ __launch_bounds__(256) void k_policy(Dev dv, Work w, uint32_t step) {
 }
 
 // ---- displaced residents -> T -----------------------------------------------------------------
-template <int D, int BITS, bool SB16>
+// UPDATED = false: residents not updated this step (their FP32 way is quantized as it
+// is; no merged gradient needed, so this runs beside the gradient sums);
+// UPDATED = true: residents updated this step and then displaced (LFU or direct-mapped;
+// their merged gradient is applied first), after the gradient sums.
+template <int D, int BITS, bool SB16, bool UPDATED>
 __global__ __launch_bounds__(256) void k_evict(Dev dv, Work w, const uint32_t* __restrict__ sval,
                                                const float* __restrict__ grad, uint32_t step) {
+  if (UPDATED && w.ctr[kCHitEv] == 0) return;
   constexpr int LPR = Geo<D>::LPR;
   constexpr int GPB = 256 / LPR;
   constexpr int RB = Rec<D, BITS, SB16>::BYTES;
@@ -769,11 +775,11 @@ __global__ __launch_bounds__(256) void k_evict(Dev dv, Work w, const uint32_t* _
       const int32_t dst = w.udest[u];
       const int32_t vrow = w.uvic_row[u];
       const int32_t vu = w.uvic_u[u];
-      if (act != kActInsert || vrow < 0) continue;
+      if (act != kActInsert || vrow < 0 || (vu >= 0) != UPDATED) continue;
       const int64_t vgrow = td.row_base + vrow;
       float xv[8];
       load_frow8_nt(dv.crow + (int64_t)dst * D, g, xv);
-      if (vu >= 0) {
+      if (UPDATED) {
         // the displaced resident was updated this step (LFU): its new value goes to T
         const float Gv = load_G(dv, vgrow);
         float gv[8];
@@ -885,7 +891,7 @@ __global__ __launch_bounds__(256) void k_update(Dev dv, Work w, const uint32_t* 
 // ---- one training step ----------------------------------------------------------------------
 hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int64_t L, const int32_t* off, int32_t B,
                            const float* grad, uint64_t step64, int key_bits, bool decay,
-                           const hipEvent_t* update_events, hipStream_t s) {
+                           const hipEvent_t* update_events, const SideStream& side, hipStream_t s) {
   const uint32_t step = (uint32_t)step64;
   k_bwd_begin<<<1, 256, 0, s>>>(d, w.ctr, L);
   if (decay && d.cnt) k_decay<<<grid_for(d.total_rows), 256, 0, s>>>(d.cnt, d.total_rows);
@@ -919,15 +925,28 @@ hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int6
   if (nblk > w.max_nblk) return hipErrorInvalidValue;
   if (nblk > 0) k_block_bounds<<<grid(k_block_bounds), 256, 0, s>>>(w, sv, nb_shift, nblk);
   return dispatch_row(d.dim, d.bits, d.sb16, [&]<int D, int BITS, bool SB16>() -> hipError_t {
+    // replacement decisions and the write-back of residents displaced without an update
+    // on the side stream, the merged gradients on `s`; joined before the updates
+    const bool cached = d.total_slots > 0;
+    if (cached) {
+      hipError_t e2 = hipEventRecord(side.fork, s);
+      if (e2 == hipSuccess) e2 = hipStreamWaitEvent(side.s, side.fork, 0);
+      if (e2 != hipSuccess) return e2;
+      k_policy<<<grid(k_policy), 256, 0, side.s>>>(d, w, step);
+      k_evict<D, BITS, SB16, false><<<grid(k_evict<D, BITS, SB16, false>), 256, 0, side.s>>>(d, w, sv, grad, step);
+      e2 = hipEventRecord(side.join, side.s);
+      if (e2 != hipSuccess) return e2;
+    }
     k_partials<D><<<grid(k_partials<D>), 256, 0, s>>>(d, w, sv, grad);
     if (nblk > 0) {
       k_block_partials<D><<<resident_grid(reinterpret_cast<const void*>(k_block_partials<D>), kBlockThreads),
                             kBlockThreads, 0, s>>>(d, w, sv, grad, B, nblk);
       k_block_fold<D><<<grid(k_block_fold<D>), 256, 0, s>>>(w, nblk);
     }
-    if (d.total_slots > 0) {
-      k_policy<<<grid(k_policy), 256, 0, s>>>(d, w, step);
-      k_evict<D, BITS, SB16><<<grid(k_evict<D, BITS, SB16>), 256, 0, s>>>(d, w, sv, grad, step);
+    if (cached) {
+      const hipError_t e2 = hipStreamWaitEvent(s, side.join, 0);
+      if (e2 != hipSuccess) return e2;
+      k_evict<D, BITS, SB16, true><<<grid(k_evict<D, BITS, SB16, true>), 256, 0, s>>>(d, w, sv, grad, step);
     }
     k_pack_meta<<<grid(k_pack_meta), 256, 0, s>>>(w, sv);
     if (update_events) {

@@ -206,8 +206,12 @@ struct emb_cache {
   bool timing = false;
   std::vector<hipEvent_t> tev;
   uint64_t timed = 0;
+  embc::SideStream side;  // default priority, non-blocking; events without timing
   ~emb_cache() {
     for (hipEvent_t e : tev) (void)hipEventDestroy(e);
+    if (side.fork) (void)hipEventDestroy(side.fork);
+    if (side.join) (void)hipEventDestroy(side.join);
+    if (side.s) (void)hipStreamDestroy(side.s);
   }
 };
 
@@ -406,6 +410,9 @@ int create_impl(const emb_cache_config* cfg, void* state, size_t state_bytes, vo
   if (e == hipSuccess)
     e = hipMemcpyAsync(sb + p.o_keyb, p.key_base.data(), sizeof(int64_t) * p.key_base.size(), hipMemcpyHostToDevice,
                        s);
+  if (e == hipSuccess) e = hipStreamCreateWithFlags(&h->side.s, hipStreamNonBlocking);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&h->side.fork, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&h->side.join, hipEventDisableTiming);
   if (e == hipSuccess) e = embc::launch_reset_state(d, s);
   if (e == hipSuccess) e = hipStreamSynchronize(s);
   if (e != hipSuccess) {
@@ -447,7 +454,7 @@ int emb_cache_backward_update(emb_cache_t h, const int32_t* indices, int64_t num
   const hipEvent_t* tev = nullptr;
   if (h->timing) tev = &h->tev[2 * (h->timed % emb_cache::kTimedCalls)];
   const hipError_t e = embc::launch_backward(h->dev, h->work, indices, num_indices, offsets, batch, grad_out,
-                                             h->step, h->key_bits, decay, tev, S(stream));
+                                             h->step, h->key_bits, decay, tev, h->side, S(stream));
   if (e != hipSuccess) return EMB_EHIP;
   if (h->timing) h->timed += 1;
   h->step += 1;
