@@ -345,6 +345,13 @@ __device__ __forceinline__ void quantize_store(const float (&x)[8], int g, uint8
   }
 }
 
+// n / d and n % d for a DivConst (exact for every 32-bit n).
+__device__ __forceinline__ uint32_t div_by(uint32_t n, const DivConst& c) {
+  const uint32_t t = __umulhi(c.m, n);
+  return (t + ((n - t) >> c.s1)) >> c.s2;
+}
+__device__ __forceinline__ uint32_t mod_by(uint32_t n, const DivConst& c) { return n - div_by(n, c) * c.d; }
+
 // Table of a sort key (binary search over key_base[0..T]).
 __device__ __forceinline__ int table_of_key(const int64_t* key_base, int T, uint32_t key) {
   int lo = 0, hi = T;  // key_base[lo] <= key < key_base[hi]
@@ -359,7 +366,7 @@ __device__ __forceinline__ int table_of_key(const int64_t* key_base, int T, uint
 // compared with int4 loads when assoc is a multiple of 4).
 __device__ __forceinline__ int32_t probe_slot(const Dev& dv, const TableDesc& td, int32_t r) {
   if (td.n_sets == 0) return -1;
-  const int64_t set = (int64_t)((uint32_t)r % (uint32_t)td.n_sets);
+  const int64_t set = (int64_t)mod_by((uint32_t)r, td.by_sets);
   const int64_t base = td.slot_base + set * dv.assoc;
   const int32_t* tg = dv.tag + base;
   if ((dv.assoc & 3) == 0) {

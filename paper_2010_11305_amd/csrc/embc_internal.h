@@ -42,6 +42,16 @@ constexpr int kMaxPasses = 4;  // 8-bit digits of a 32-bit sort key
 // Per-table geometry.  Sort keys are set-major: key = key_base + set*Q + row/n_sets,
 // with set = row % n_sets and Q = ceil(N/n_sets), so that one sort groups the
 // lookups by row, the rows by set, and the rows of a set in ascending order.
+// Unsigned 32-bit division by a constant 1 <= d < 2^31 as one high multiply, a
+// subtract, an add and two shifts (Granlund and Montgomery, "Division by invariant
+// integers using multiplication", PLDI 1994, Sec. 4): with l = ceil(log2 d),
+// m = floor(2^32 (2^l - d) / d) + 1, t = mulhi(m, n):
+// n / d = (t + ((n - t) >> s1)) >> s2, s1 = min(l, 1), s2 = max(l - 1, 0), exact for
+// every 32-bit n.
+struct DivConst {
+  uint32_t d = 1, m = 1, s1 = 0, s2 = 0;
+};
+
 struct TableDesc {
   int64_t N;
   int64_t row_base;
@@ -49,6 +59,8 @@ struct TableDesc {
   int64_t slot_base;
   int64_t Q;          // key stride of a set; N when there is no cache
   int64_t key_base;
+  DivConst by_sets;   // division by n_sets (by 1 when there is no cache)
+  DivConst by_Q;      // division by Q
 };
 
 // Device view of the state, passed by value to every kernel.

@@ -129,7 +129,7 @@ __global__ __launch_bounds__(256) void k_fwd_probe(Dev dv, const int32_t* __rest
         valid[q] = r[q] >= 0 && (int64_t)r[q] < td.N;
         found[q] = -1;
         if (valid[q] && td.n_sets > 0) {
-          const int64_t set = (int64_t)((uint32_t)r[q] % (uint32_t)td.n_sets);
+          const int64_t set = (int64_t)mod_by((uint32_t)r[q], td.by_sets);
           const int32_t* tg = tags + set * A;
           int32_t tw[W];
           if constexpr (W % 4 == 0) {

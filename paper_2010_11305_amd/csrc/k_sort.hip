@@ -52,6 +52,7 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_reduce(const T* __restric
                                                               const unsigned long long* dev_n, T* part) {
   __shared__ T lds4[4];
   if (dev_n) n = min(n, (int64_t)*dev_n);
+  if ((int64_t)blockIdx.x * kScanTile >= n) return;  // a tile past the values (whole block)
   const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
   T s = 0;
 #pragma unroll
@@ -62,9 +63,13 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_reduce(const T* __restric
   if (threadIdx.x == 0) part[blockIdx.x] = tot;
 }
 
+// The tiles past the device-side count (dev_n) hold no values: only the first
+// ceil(min(n, dev_n) / kScanTile) partials are scanned.
 template <typename T>
-__global__ __launch_bounds__(kScanThreads) void k_scan_top(T* part, int64_t nb, T* total_out) {
+__global__ __launch_bounds__(kScanThreads) void k_scan_top(T* part, int64_t nb, int64_t n,
+                                                           const unsigned long long* dev_n, T* total_out) {
   __shared__ T lds4[4];
+  if (dev_n) nb = min(nb, (min(n, (int64_t)*dev_n) + kScanTile - 1) / kScanTile);
   T carry = 0;
   for (int64_t b0 = 0; b0 < nb; b0 += kScanThreads) {
     const int64_t i = b0 + threadIdx.x;
@@ -82,6 +87,7 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_down(const T* __restrict_
                                                             const unsigned long long* dev_n, const T* part) {
   __shared__ T lds4[4];
   if (dev_n) n = min(n, (int64_t)*dev_n);
+  if ((int64_t)blockIdx.x * kScanTile >= n) return;  // a tile past the values (whole block)
   const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
   T v[kScanItems];
   T s = 0;
@@ -103,12 +109,12 @@ template <typename T>
 hipError_t scan_exclusive(const T* in, T* out, int64_t n, const unsigned long long* dev_n, T* part, T* total,
                           hipStream_t s) {
   if (n <= 0) {
-    if (total) k_scan_top<T><<<1, kScanThreads, 0, s>>>(part, 0, total);
+    if (total) k_scan_top<T><<<1, kScanThreads, 0, s>>>(part, 0, 0, nullptr, total);
     return hipGetLastError();
   }
   const int64_t nb = (n + kScanTile - 1) / kScanTile;
   k_scan_reduce<T><<<(unsigned)nb, kScanThreads, 0, s>>>(in, n, dev_n, part);
-  k_scan_top<T><<<1, kScanThreads, 0, s>>>(part, nb, total);
+  k_scan_top<T><<<1, kScanThreads, 0, s>>>(part, nb, n, dev_n, total);
   k_scan_down<T><<<(unsigned)nb, kScanThreads, 0, s>>>(in, out, n, dev_n, part);
   return hipGetLastError();
 }
@@ -400,8 +406,8 @@ __global__ __launch_bounds__(256) void k_expand(Dev dv, const int32_t* __restric
       uint32_t key = kKeyInvalid;
       if (r >= 0 && (int64_t)r < td.N) {
         if (td.n_sets > 0) {
-          const uint32_t set = (uint32_t)r % (uint32_t)td.n_sets;
-          const uint32_t q = (uint32_t)r / (uint32_t)td.n_sets;
+          const uint32_t q = div_by((uint32_t)r, td.by_sets);
+          const uint32_t set = (uint32_t)r - q * (uint32_t)td.n_sets;
           key = (uint32_t)(td.key_base + (int64_t)set * td.Q + q);
         } else {
           key = (uint32_t)(td.key_base + r);
@@ -465,13 +471,14 @@ size_t uniq_tile_words(int64_t n) { return (size_t)((n + kUqTile - 1) / kUqTile 
 // Table of the keys seen by one thread, with the key range and set stride of that table.
 struct TabCursor {
   int t = -1;
-  int64_t kb = 0, kb_next = 0, Q = 1;
+  int64_t kb = 0, kb_next = 0;
+  DivConst byQ;
   bool cached = false;
   __device__ void load(const Dev& dv) {
     kb = dv.key_base[t];
     kb_next = dv.key_base[t + 1];
     const TableDesc& td = dv.desc[t];
-    Q = td.Q;
+    byQ = td.by_Q;
     cached = td.n_sets > 0;
   }
   // position on the table of a valid key (keys only increase after the first call)
@@ -485,7 +492,7 @@ struct TabCursor {
       load(dv);
     }
   }
-  __device__ uint32_t set_of(uint32_t key) const { return (uint32_t)((int64_t)key - kb) / (uint32_t)Q; }
+  __device__ uint32_t set_of(uint32_t key) const { return div_by((uint32_t)((int64_t)key - kb), byQ); }
 };
 
 // Walks the thread's keys; calls on_start(i, key, is_set_start) for every row start.

@@ -83,7 +83,10 @@ __global__ __launch_bounds__(256) void k_probe(Dev dv, Work w, uint32_t step) {
       const TableDesc td = dv.desc[t];
       const int64_t local = (int64_t)key - td.key_base;
       int64_t r = local;
-      if (td.n_sets > 0) r = (local % td.Q) * td.n_sets + local / td.Q;
+      if (td.n_sets > 0) {
+        const uint32_t sq = div_by((uint32_t)local, td.by_Q);  // local = set * Q + q
+        r = (int64_t)((uint32_t)local - sq * (uint32_t)td.Q) * td.n_sets + sq;
+      }
       nocache = td.n_sets == 0;
       const int64_t grow = td.row_base + r;
       const uint32_t count = w.seg[u + 1] - w.seg[u];

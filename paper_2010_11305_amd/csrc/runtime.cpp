@@ -44,6 +44,22 @@ unsigned resident_grid(const void* kernel, int threads) {
 
 namespace {
 
+// Magic numbers of DivConst for 1 <= d < 2^31.
+embc::DivConst div_const(uint32_t d) {
+  embc::DivConst c;
+  uint32_t l = 0;
+  while (l < 32 && (1ull << l) < d) ++l;  // ceil(log2 d)
+  c.d = d;
+  c.m = (uint32_t)(((1ull << 32) * ((1ull << l) - d)) / d + 1);
+  c.s1 = l < 1 ? l : 1;
+  c.s2 = l > 1 ? l - 1 : 0;
+  return c;
+}
+
+}  // namespace
+
+namespace {
+
 constexpr size_t kAlign = 256;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
@@ -111,6 +127,8 @@ int plan_config(const emb_cache_config* c, Plan* p) {
     d.n_sets = n_sets;
     d.slot_base = slots;
     d.Q = n_sets ? (N + n_sets - 1) / n_sets : N;
+    d.by_sets = div_const(n_sets ? (uint32_t)n_sets : 1u);
+    d.by_Q = div_const((uint32_t)d.Q);
     d.key_base = keys;
     p->key_base[t] = keys;
     rows += N;

@@ -85,6 +85,10 @@ STEP_CASES = {
     "d256_int2_sr_assoc32": {"dim": 256, "bits": 2, "rounding": "stochastic", "assoc": 32, "cache_fraction": 0.1},
     "int2_nocache_sr": {"bits": 2, "cache_fraction": 0.0, "rounding": "stochastic"},
     "multi_table": {"rows": [1000, 5, 64, 3000], "batch": 96, "assoc": 4, "cache_fraction": 0.05},
+    "odd_tables": {"rows": [1, 2, 3, 7, 97, 641, 1001, 4093, 5000, 65537, 100003, 2], "batch": 200, "assoc": 8,
+                   "cache_fraction": 0.07, "pooling": ("uniform", 1, 6)},
+    "odd_tables_lfu_dm": {"rows": [3, 17, 999, 12289, 3], "batch": 150, "assoc": 1, "policy": "lfu",
+                          "cache_fraction": 0.3},
 }
 
 
