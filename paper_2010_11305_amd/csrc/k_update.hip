@@ -760,36 +760,57 @@ __global__ __launch_bounds__(256) void k_evict(Dev dv, Work w, const uint32_t* _
                                                const float* __restrict__ grad, uint32_t step) {
   if (UPDATED && w.ctr[kCHitEv] == 0) return;
   constexpr int LPR = Geo<D>::LPR;
-  constexpr int GPB = 256 / LPR;
+  constexpr int GPW = 64 / LPR;  // row groups per wave
   constexpr int RB = Rec<D, BITS, SB16>::BYTES;
-  const int g = threadIdx.x & (LPR - 1);
-  const int64_t nU = (int64_t)w.ctr[kCUnique];
+  const int lane = threadIdx.x & 63;
+  const int g = lane & (LPR - 1), grp = lane / LPR;
   const bool sr = dv.rounding != 0;
   const XcdSplit xs(dv.T, true);
-  const int64_t gx = xs.unit * GPB + threadIdx.x / LPR, gstride = xs.units * GPB;
+  // each wave takes windows of 64 consecutive unique rows: one coalesced load of each
+  // row's decision, a ballot of the rows that displace a resident, then those rows
+  // GPW at a time (one per row group), so no group idles on rows without a victim
+  const int64_t wv = xs.unit * (blockDim.x / 64) + threadIdx.x / 64, wstride = xs.units * (blockDim.x / 64);
   for (int seg = xs.xcd; seg < xs.segments(dv.T); seg += kXcds) {
     const int t = seg / xs.parts;
     int64_t tlo, thi, lo, hi;
     table_rows(w, t, tlo, thi);
     part_range(tlo, thi, seg % xs.parts, xs.parts, lo, hi);
     const TableDesc td = dv.desc[t];
-    for (int64_t u = lo + gx; u < hi; u += gstride) {
-      const int32_t act = w.uact[u];
-      const int32_t dst = w.udest[u];
-      const int32_t vrow = w.uvic_row[u];
-      const int32_t vu = w.uvic_u[u];
-      if (act != kActInsert || vrow < 0 || (vu >= 0) != UPDATED) continue;
-      const int64_t vgrow = td.row_base + vrow;
-      float xv[8];
-      load_frow8_nt(dv.crow + (int64_t)dst * D, g, xv);
-      if (UPDATED) {
-        // the displaced resident was updated this step (LFU): its new value goes to T
-        const float Gv = load_G(dv, vgrow);
-        float gv[8];
-        merged_grad<D>(w, sval, grad_rows<D>(grad, t, dv.T), vu, g, gv);
-        apply_optimizer<D>(dv, xv, gv, vgrow, g, Gv);
+    if (td.n_sets == 0) continue;
+    for (int64_t w0 = lo + wv * 64; w0 < hi; w0 += wstride * 64) {
+      const int64_t u = w0 + lane;
+      int32_t dst = 0, vrow = -1, vu = -1;
+      bool take = false;
+      if (u < hi) {
+        const int32_t act = w.uact[u];
+        dst = w.udest[u];
+        vrow = w.uvic_row[u];
+        vu = w.uvic_u[u];
+        take = act == kActInsert && vrow >= 0 && (vu >= 0) == UPDATED;
       }
-      quantize_store<D, BITS, SB16>(xv, g, dv.rec + vgrow * RB, sr, dv.seed, step, (uint32_t)t, (uint32_t)vrow);
+      uint64_t mask = __ballot(take);
+      while (mask) {
+        // the grp-th set bit of mask is this group's row (none when fewer remain)
+        uint64_t m = mask;
+        for (int k = 0; k < grp && m; ++k) m &= m - 1;
+        const int src = m ? __builtin_ctzll(m) : 0;
+        const bool mine = m != 0;
+        for (int k = 0; k < GPW && mask; ++k) mask &= mask - 1;
+        const int32_t e_dst = __shfl(dst, src), e_vrow = __shfl(vrow, src), e_vu = __shfl(vu, src);
+        if (!mine) continue;
+        const int64_t vgrow = td.row_base + e_vrow;
+        float xv[8];
+        load_frow8_nt(dv.crow + (int64_t)e_dst * D, g, xv);
+        if (UPDATED) {
+          // the displaced resident was updated this step (LFU): its new value goes to T
+          const float Gv = load_G(dv, vgrow);
+          float gv[8];
+          merged_grad<D>(w, sval, grad_rows<D>(grad, t, dv.T), e_vu, g, gv);
+          apply_optimizer<D>(dv, xv, gv, vgrow, g, Gv);
+        }
+        quantize_store<D, BITS, SB16>(xv, g, dv.rec + vgrow * RB, sr, dv.seed, step, (uint32_t)t,
+                                      (uint32_t)e_vrow);
+      }
     }
   }
 }
