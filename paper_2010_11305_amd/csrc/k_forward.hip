@@ -196,8 +196,10 @@ __global__ __launch_bounds__(256) void k_fwd_gather(Dev dv, const int32_t* __res
     part_range(0, B, seg % xs.parts, xs.parts, blo, bhi);
     const TableDesc td = dv.desc[t];
     const uint8_t* rec0 = dv.rec + td.row_base * RB;
-    // codes outside this table's slots and rows are skipped (only malformed offsets produce them)
-    const int64_t slot_lo = td.slot_base, slot_hi = td.slot_base + td.n_sets * dv.assoc;
+    // codes outside this table's slots and rows are skipped (only malformed offsets
+    // produce them); slots, rows and positions are below 2^31 (32-bit arithmetic)
+    const int32_t slot_lo = (int32_t)td.slot_base, slot_hi = (int32_t)(td.slot_base + td.n_sets * dv.assoc);
+    const int32_t nrows = (int32_t)td.N;
     if (blo + gx >= bhi) continue;
     // the offsets of the group's next bag are loaded one bag ahead, the codes of the
     // next LPR positions one chunk ahead (indices clamped so that the loads are
@@ -210,10 +212,13 @@ __global__ __launch_bounds__(256) void k_fwd_gather(Dev dv, const int32_t* __res
       const int64_t nb = min<int64_t>(b + gstride, bhi - 1);
       o0 = offt[nb];
       o1 = offt[nb + 1];
+      // the sum starts from -0, the identity of IEEE addition (adding the first term
+      // gives exactly that term, as in the seeded left-to-right sum); a bag without a
+      // valid lookup gives +0
       float acc[8];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) acc[i] = 0.0f;
-      bool first = true;
+      for (int i = 0; i < 8; ++i) acc[i] = -0.0f;
+      bool any = false;
       int32_t code_next = p0 + g < p1 ? src[p0 + g] : -1;
       for (int64_t pc = p0; pc < p1; pc += LPR) {
         const int n = (int)min<int64_t>(LPR, p1 - pc);
@@ -230,7 +235,7 @@ __global__ __launch_bounds__(256) void k_fwd_gather(Dev dv, const int32_t* __res
             kind[q] = 0;
             if (j + q < n) {
               if (cq >= slot_lo && cq < slot_hi) kind[q] = 1;
-              else if (cq <= -2 && (int64_t)(-2 - cq) < td.N) kind[q] = 2;
+              else if (cq <= -2 && -2 - cq < nrows) kind[q] = 2;
             }
             if (kind[q] == 1) {
               load_frow8(dv.crow + (int64_t)cq * D, g, raw[q]);
@@ -248,16 +253,15 @@ __global__ __launch_bounds__(256) void k_fwd_gather(Dev dv, const int32_t* __res
               decode_sb<SB16>(sbw[q], sq, bq);
               dequant8<BITS>(cw[q], sq, bq, raw[q]);
             }
-            if (first) {
 #pragma unroll
-              for (int i = 0; i < 8; ++i) acc[i] = raw[q][i];
-              first = false;
-            } else {
-#pragma unroll
-              for (int i = 0; i < 8; ++i) acc[i] = acc[i] + raw[q][i];
-            }
+            for (int i = 0; i < 8; ++i) acc[i] = acc[i] + raw[q][i];
+            any = true;
           }
         }
+      }
+      if (!any) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[i] = 0.0f;
       }
       store_frow8_nt(out + ((int64_t)b * dv.T + t) * D, g, acc);
     }
