@@ -182,7 +182,10 @@ template <int D>
 __device__ __forceinline__ void chunk_sum(const uint32_t* __restrict__ sval, int64_t i0, int64_t i1, GradRows<D> gr,
                                           int g, float (&acc)[8]) {
   constexpr int LPR = Geo<D>::LPR, CPL = 8, U = kChunkUnroll;
-  bool first = true;
+  // the sum starts from -0, the identity of IEEE addition: adding the first term gives
+  // exactly that term, as in the seeded left-to-right sum (the chunk is not empty)
+#pragma unroll
+  for (int k = 0; k < CPL; ++k) acc[k] = -0.0f;
   uint32_t pv = 0xFFFFFFFFu;  // bag of the last occurrence added (none yet)
   float last[CPL];
 #pragma unroll
@@ -209,14 +212,8 @@ __device__ __forceinline__ void chunk_sum(const uint32_t* __restrict__ sval, int
 #pragma unroll
             for (int k = 0; k < CPL; ++k) x[q][k] = last[k];
           }
-          if (first) {
 #pragma unroll
-            for (int k = 0; k < CPL; ++k) acc[k] = x[q][k];
-            first = false;
-          } else {
-#pragma unroll
-            for (int k = 0; k < CPL; ++k) acc[k] = acc[k] + x[q][k];
-          }
+          for (int k = 0; k < CPL; ++k) acc[k] = acc[k] + x[q][k];
 #pragma unroll
           for (int k = 0; k < CPL; ++k) last[k] = x[q][k];
           pv = v[q];
