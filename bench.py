@@ -258,6 +258,7 @@ def main():
     # algorithmic bytes from the statistics of further steps of the same stream
     fwd_b, bwd_b, upd_b, n_st = 0, 0, 0, 0
     hit_lk, all_lk = 0, 0
+    counts = {}
     for k in range(args.stats_steps):
         step(args.warmup + args.steps + k)
         for t in range(T):
@@ -268,6 +269,8 @@ def main():
             upd_b += update_kernel_bytes(cfg, st)
             hit_lk += st["hit_lookups"]
             all_lk += st["lookups"]
+            for key in ("unique", "unique_hits", "inserts", "bypasses", "evictions", "hit_evictions"):
+                counts[key] = counts.get(key, 0) + st[key]
         n_st += 1
     fwd_b /= n_st
     bwd_b /= n_st
@@ -303,6 +306,7 @@ def main():
         "fwd_ms_p90": float(np.percentile(fwd_ms, 90)),
         "bwd_ms_p90": float(np.percentile(bwd_ms, 90)),
         "hit_rate_lookups": hit_lk / max(all_lk, 1),
+        "rows_per_step": {k: v / max(n_st, 1) for k, v in counts.items()},
         "status": status,
         "roofline": {"bound": "hbm", "kernel": "k_update (merged gradient, fetch, row-wise Adagrad, write-back)",
                      "achieved": upd_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": upd_gbs / HBM_PEAK_GBS,

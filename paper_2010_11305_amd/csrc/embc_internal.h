@@ -99,6 +99,7 @@ struct Work {
   uint32_t* valsB;
   uint32_t* sort_small;  // radix sort: digit counts, their prefix sums, tile tickets
   uint32_t* sort_status[2];  // radix sort look-back status words
+  uint32_t* sort_seg;    // radix sort, segmented mode: segment starts, first tiles, per-table digit counts
   unsigned long long* part;  // scan partials
   unsigned long long* tile_cnt;  // unique rows and touched sets per tile of sorted keys, packed (sets << 32 | rows)
   unsigned long long* tile_pre;  // their exclusive prefix sums
@@ -160,10 +161,11 @@ struct SideStream {
 
 // update_events: nullptr, or two events recorded on `s` around the row-update kernel.
 hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int64_t L, const int32_t* off,
-                           int32_t B, const float* grad, uint64_t step, int key_bits, bool decay,
+                           int32_t B, const float* grad, uint64_t step, int key_bits, int seg_passes, bool decay,
                            const hipEvent_t* update_events, const SideStream& side, hipStream_t s);
 
-size_t sort_status_words(int64_t n);
+size_t sort_status_words(int64_t n, int T);
+size_t sort_seg_words(int T);
 constexpr size_t kSortSmallWords = 2 * kMaxPasses * 256 + 64;
 size_t scan_partial_words(int64_t n);
 size_t uniq_tile_words(int64_t n);

@@ -14,7 +14,15 @@ struct SortScratch {
   uint32_t* ghist;      // [kMaxPasses][256] digit counts
   uint32_t* gbase;      // [kMaxPasses][256] their exclusive prefix sums
   uint32_t* tickets;    // [kMaxPasses] tile tickets
-  uint32_t* status[2];  // [sort_status_words(n)] look-back status words, alternating by pass
+  uint32_t* status[2];  // [sort_status_words(n, T)] look-back status words, alternating by pass
+};
+
+// Scratch of the segmented mode (sort_seg_words(T) words).
+struct SegSort {
+  uint32_t* pos = nullptr;    // [T+1] first position of each table's lookups; pos[T] = n
+  uint32_t* tbase = nullptr;  // [T+1] first tile of each table's segment; tbase[T] = tiles
+  uint32_t* hist = nullptr;   // [T][kMaxPasses][256] local-key digit counts per table
+  uint32_t* base = nullptr;   // [T][kMaxPasses][256] where each table's digit runs start
 };
 
 // Stable LSD radix sort of n < 2^30 (key, value) pairs over `passes` (<= kMaxPasses)
@@ -22,6 +30,15 @@ struct SortScratch {
 // result is.  A look-back that waits too long sets kErrSort in *err.
 hipError_t sort_pairs(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32_t* vB, int64_t n, int passes,
                       const SortScratch& ss, int32_t* err, int* in_B, hipStream_t s);
+
+// The same order from `passes` (< kMaxPasses) digit passes over each table's segment
+// of the stream (lookups of table t at [off[t*B], off[(t+1)*B])), sorted by the local
+// key; every table's key range must be below 2^(8*passes) and every valid key's top
+// byte below 255.  One more pass and a copy run only when some key is kKeyInvalid.
+hipError_t sort_pairs_segmented(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32_t* vB, int64_t n, int passes,
+                                const int32_t* off, int32_t B, int T, const int64_t* key_base,
+                                const unsigned long long* ctr, const SortScratch& ss, const SegSort& sg, int32_t* err,
+                                int* in_B, hipStream_t s);
 
 // Offsets must be non-decreasing and inside [0, L]; otherwise set the error flag and
 // ctr[kCBadOffsets].

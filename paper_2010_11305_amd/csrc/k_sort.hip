@@ -151,18 +151,49 @@ __device__ __forceinline__ uint64_t match_digit(uint32_t d, bool valid) {
 // tile.  Tiles are numbered in the order their workgroups start, so every tile a
 // look-back waits for is already running; the wait is bounded all the same (after
 // kSortSpinLimit polls the step is flagged as failed and the tile goes on).
+//
+// Segmented mode.  The lookups arrive grouped by table (bag t*B + b belongs to table
+// t), so the keys of table t fill the positions [P_t, P_t+1) and every valid key there
+// lies in table t's key range.  Sorting each segment by the local key (key minus the
+// table's key base) gives the global order in fewer passes when every table's key
+// range is far smaller than the sum of them (100 tables of 5M rows: 3 passes instead
+// of 4).  Tiles never straddle a segment (each segment starts a new tile), a look-back
+// ends at the segment's first tile, and digit runs start at P_t.  A skipped lookup
+// (kKeyInvalid) takes digit 255 in every pass, above every valid local key, so it ends
+// its table's segment; when there is any, one more stable pass on the top byte of the
+// global key (255 only for kKeyInvalid) moves them behind every valid key, and the
+// pairs are copied back so that the result stays in the same buffer.
 constexpr uint32_t kStAgg = 1u << 30;
 constexpr uint32_t kStPre = 2u << 30;
 constexpr uint32_t kStCount = (1u << 30) - 1;
 constexpr uint32_t kSortSpinLimit = 1u << 20;
 
-size_t sort_status_words(int64_t n) { return 256 * (size_t)((n + kRadixTile - 1) / kRadixTile + 1); }
+size_t sort_status_words(int64_t n, int T) {
+  return 256 * (size_t)((n + kRadixTile - 1) / kRadixTile + T + 1);
+}
+size_t sort_seg_words(int T) { return 2 * (size_t)T * kMaxPasses * 256 + 2 * (size_t)(T + 1) + 64; }
 
 __device__ __forceinline__ uint32_t status_load(const uint32_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ void status_store(uint32_t* p, uint32_t v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Segment of tile `tile` (< tbase[T]): the largest t with tbase[t] <= tile.  Empty
+// segments share their successor's first tile and are never returned.
+__device__ __forceinline__ int seg_of_tile(const uint32_t* tbase, int T, uint32_t tile) {
+  int lo = 0, hi = T;  // tbase[lo] <= tile < tbase[hi]
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (tbase[mid] <= tile) lo = mid; else hi = mid;
+  }
+  return lo;
+}
+
+// Digit of a key in a pass of the segmented mode: the local key's, or 255 when skipped.
+__device__ __forceinline__ uint32_t seg_digit(uint32_t key, uint32_t kb, int shift) {
+  return key == kKeyInvalid ? 255u : ((key - kb) >> shift) & 255u;
 }
 
 // ghist [kMaxPasses][256] and the pass tickets must be zero on entry (k_sort_begin).
@@ -215,13 +246,127 @@ __global__ __launch_bounds__(256) void k_sort_scan(const uint32_t* __restrict__ 
   }
 }
 
+// Segment starts P_t (t = 0..T; P_0 = 0 and P_T = n, so positions outside every bag,
+// which hold skipped keys, join the first or the last segment) and the first tile of
+// each segment (tbase[T] = number of tiles).  With malformed offsets every key is
+// skipped and the whole stream is one segment.  Also clears the per-table histograms.
+__global__ __launch_bounds__(256) void k_seg_setup(const int32_t* __restrict__ off, int32_t B, int T, int64_t n,
+                                                   const unsigned long long* __restrict__ ctr, SegSort sg) {
+  __shared__ uint32_t lds4[4];
+  const bool bad = ctr[kCBadOffsets] != 0;
+  const auto start = [&](int t) -> int64_t {
+    if (t <= 0) return 0;
+    if (t >= T || bad) return n;
+    return min<int64_t>(max<int64_t>(off[(int64_t)t * B], 0), n);
+  };
+  uint32_t run = 0;
+  for (int t0 = 0; t0 <= T; t0 += 256) {
+    const int t = t0 + (int)threadIdx.x;
+    uint32_t tiles = 0;
+    int64_t p = 0;
+    if (t <= T) {
+      p = start(t);
+      if (t < T) tiles = (uint32_t)((start(t + 1) - p + kRadixTile - 1) / kRadixTile);
+    }
+    uint32_t tot;
+    const uint32_t ex = block_exclusive_scan<uint32_t>(tiles, lds4, tot);
+    if (t <= T) {
+      sg.pos[t] = (uint32_t)p;
+      sg.tbase[t] = run + ex;
+    }
+    run += tot;
+  }
+  const int64_t hw = (int64_t)T * kMaxPasses * 256;
+  for (int64_t i = threadIdx.x; i < hw; i += 256) sg.hist[i] = 0;
+}
+
+// Per-table histograms of the local-key digits of every segmented pass, and the global
+// histogram of the top byte of the key (for the pass that moves skipped keys last), in
+// one read of the keys; each block takes kSegHistTiles consecutive tiles and adds its
+// counts when the table changes.  Also clears the status words of the first pass.
+constexpr int kSegHistTiles = 8;
+
+__global__ __launch_bounds__(256) void k_seg_hist(const uint32_t* __restrict__ keys, int64_t n, int passes,
+                                                  const int64_t* __restrict__ key_base, int T, SegSort sg,
+                                                  uint32_t* __restrict__ top_hist, uint32_t* __restrict__ status,
+                                                  int64_t status_words) {
+  __shared__ uint32_t h[kRadixWaves][kMaxPasses + 1][256];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  for (int i = threadIdx.x; i < kRadixWaves * (kMaxPasses + 1) * 256; i += 256) (&h[0][0][0])[i] = 0;
+  __syncthreads();
+  const uint32_t ntiles = sg.tbase[T];
+  int cur = -1;  // table whose counts the LDS holds
+  const auto flush = [&](int t) {
+    __syncthreads();
+    for (int p = 0; p <= passes; ++p) {
+      uint32_t c = 0;
+#pragma unroll
+      for (int w = 0; w < kRadixWaves; ++w) {
+        c += h[w][p][threadIdx.x];
+        h[w][p][threadIdx.x] = 0;
+      }
+      if (c) atomicAdd(p < passes ? &sg.hist[((int64_t)t * kMaxPasses + p) * 256 + threadIdx.x]
+                                  : &top_hist[threadIdx.x], c);
+    }
+    __syncthreads();
+  };
+  for (uint32_t tile = blockIdx.x * kSegHistTiles; tile < min<uint32_t>(ntiles, (blockIdx.x + 1) * kSegHistTiles);
+       ++tile) {
+    const int t = seg_of_tile(sg.tbase, T, tile);
+    if (t != cur) {
+      if (cur >= 0) flush(cur);
+      cur = t;
+    }
+    const int64_t lo = sg.pos[t] + (int64_t)(tile - sg.tbase[t]) * kRadixTile;
+    const int64_t hi = min<int64_t>(sg.pos[t + 1], lo + kRadixTile);
+    const uint32_t kb = (uint32_t)key_base[t];
+    for (int64_t i0 = lo + wv * 64; i0 < hi; i0 += 256) {
+      const int64_t i = i0 + lane;
+      const bool valid = i < hi;
+      const uint32_t k = valid ? keys[i] : 0u;
+      for (int p = 0; p <= passes; ++p) {
+        const uint32_t d = p < passes ? seg_digit(k, kb, 8 * p) : k >> 24;
+        const uint32_t d0 = __shfl(d, 0);
+        const uint64_t same = __ballot(valid && d == d0);
+        if (lane == 0) atomicAdd(&h[wv][p][d0], (uint32_t)__popcll(same));
+        if (valid && d != d0) atomicAdd(&h[wv][p][d], 1u);
+      }
+    }
+  }
+  if (cur >= 0) flush(cur);
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < status_words; i += stride) status[i] = 0;
+}
+
+// base[t][p][d] = P_t + number of table t's keys whose pass-p digit is below d (one
+// block per table); block 0 also scans the top-byte histogram.
+__global__ __launch_bounds__(256) void k_seg_scan(SegSort sg, int passes, const uint32_t* __restrict__ top_hist,
+                                                  uint32_t* __restrict__ top_base) {
+  __shared__ uint32_t lds4[4];
+  const int t = blockIdx.x;
+  for (int p = 0; p < passes; ++p) {
+    const int64_t i = ((int64_t)t * kMaxPasses + p) * 256 + threadIdx.x;
+    uint32_t tot;
+    sg.base[i] = sg.pos[t] + block_exclusive_scan<uint32_t>(sg.hist[i], lds4, tot);
+  }
+  if (t == 0) {
+    uint32_t tot;
+    top_base[threadIdx.x] = block_exclusive_scan<uint32_t>(top_hist[threadIdx.x], lds4, tot);
+  }
+}
+
+// One radix pass.  SEG: tiles of the segmented mode (sg, pass).  Otherwise tiles of the
+// whole stream; a non-null only_if skips the pass (and the copy below) unless *only_if.
+template <bool SEG>
 __global__ __launch_bounds__(kRadixThreads) void k_sort_pass(const uint32_t* __restrict__ kin,
                                                              const uint32_t* __restrict__ vin,
                                                              uint32_t* __restrict__ kout, uint32_t* __restrict__ vout,
                                                              int64_t n, int shift, const uint32_t* __restrict__ gbase,
                                                              uint32_t* __restrict__ status, uint32_t* __restrict__ ticket,
                                                              uint32_t* __restrict__ next_status,
-                                                             int64_t status_words, int32_t* __restrict__ err) {
+                                                             int64_t status_words, int32_t* __restrict__ err,
+                                                             SegSort sg, const int64_t* __restrict__ key_base, int T,
+                                                             int pass, const uint32_t* __restrict__ only_if) {
   __shared__ uint32_t wcnt[kRadixWaves][256];
   __shared__ uint32_t dpre[256];
   __shared__ uint32_t goff[256];
@@ -234,95 +379,128 @@ __global__ __launch_bounds__(kRadixThreads) void k_sort_pass(const uint32_t* __r
   if (threadIdx.x == 0) tile_s = atomicAdd(ticket, 1u);
   __syncthreads();
   const int64_t tile = tile_s;
-  const int64_t tile0 = tile * kRadixTile;
-  const int64_t base = tile0 + (int64_t)wv * 64 * kRadixItems;
-  uint32_t k[kRadixItems], v[kRadixItems], rank[kRadixItems];
-#pragma unroll
-  for (int i = 0; i < kRadixItems; ++i) {
-    const int64_t p = base + i * 64 + lane;
-    const bool valid = p < n;
-    k[i] = valid ? kin[p] : 0xFFFFFFFFu;
-    v[i] = valid ? vin[p] : 0u;
-  }
-#pragma unroll
-  for (int i = 0; i < kRadixItems; ++i) {
-    const int64_t p = base + i * 64 + lane;
-    const bool valid = p < n;
-    const uint32_t d = (k[i] >> shift) & 255u;
-    const uint64_t peers = match_digit(d, valid);
-    const uint32_t before = (uint32_t)__popcll(peers & lanemask_lt());
-    uint32_t old = 0;
-    if (valid) old = wcnt[wv][d];
-    __builtin_amdgcn_wave_barrier();
-    if (valid && before == 0) wcnt[wv][d] = old + (uint32_t)__popcll(peers);
-    __builtin_amdgcn_wave_barrier();
-    rank[i] = old + before;
-  }
-  __syncthreads();
-  {
-    const int d = threadIdx.x;
-    uint32_t run = 0;
-#pragma unroll
-    for (int w = 0; w < kRadixWaves; ++w) {
-      const uint32_t c = wcnt[w][d];
-      wcnt[w][d] = run;
-      run += c;
+  // the tile's table and position range (block-uniform)
+  bool work = true;
+  int t = 0;
+  int64_t tfirst = 0, lo = tile * kRadixTile, hi = min<int64_t>(n, lo + kRadixTile);
+  uint32_t kb = 0;
+  if (SEG) {
+    work = tile < (int64_t)sg.tbase[T];
+    if (work) {
+      t = seg_of_tile(sg.tbase, T, (uint32_t)tile);
+      tfirst = sg.tbase[t];
+      lo = sg.pos[t] + (tile - tfirst) * kRadixTile;
+      hi = min<int64_t>(sg.pos[t + 1], lo + kRadixTile);
+      kb = (uint32_t)key_base[t];
     }
-    uint32_t* st = status + tile * 256 + d;
-    uint32_t excl = 0;
-    if (tile == 0) {
-      status_store(st, kStPre | run);
-    } else {
-      status_store(st, kStAgg | run);
-      int64_t j = tile - 1;
-      uint32_t polls = 0;
-      for (;;) {
-        const uint32_t w = status_load(status + j * 256 + d);
-        const uint32_t state = w & ~kStCount;
-        if (state == 0) {
-          if (++polls > kSortSpinLimit) {
-            atomicOr(err, kErrSort);
-            break;
-          }
-          __builtin_amdgcn_s_sleep(1);
-          continue;
-        }
-        excl += w & kStCount;
-        if (state == kStPre || j == 0) break;
-        --j;
+  } else {
+    work = lo < n && (only_if == nullptr || *only_if != 0);
+  }
+  const auto digit = [&](uint32_t key) -> uint32_t {
+    return SEG ? seg_digit(key, kb, shift) : (key >> shift) & 255u;
+  };
+  if (work) {
+    const int64_t base = lo + (int64_t)wv * 64 * kRadixItems;
+    uint32_t k[kRadixItems], v[kRadixItems], rank[kRadixItems];
+#pragma unroll
+    for (int i = 0; i < kRadixItems; ++i) {
+      const int64_t p = base + i * 64 + lane;
+      const bool valid = p < hi;
+      k[i] = valid ? kin[p] : 0xFFFFFFFFu;
+      v[i] = valid ? vin[p] : 0u;
+    }
+#pragma unroll
+    for (int i = 0; i < kRadixItems; ++i) {
+      const int64_t p = base + i * 64 + lane;
+      const bool valid = p < hi;
+      const uint32_t d = digit(k[i]);
+      const uint64_t peers = match_digit(d, valid);
+      const uint32_t before = (uint32_t)__popcll(peers & lanemask_lt());
+      uint32_t old = 0;
+      if (valid) old = wcnt[wv][d];
+      __builtin_amdgcn_wave_barrier();
+      if (valid && before == 0) wcnt[wv][d] = old + (uint32_t)__popcll(peers);
+      __builtin_amdgcn_wave_barrier();
+      rank[i] = old + before;
+    }
+    __syncthreads();
+    {
+      const int d = threadIdx.x;
+      uint32_t run = 0;
+#pragma unroll
+      for (int w = 0; w < kRadixWaves; ++w) {
+        const uint32_t c = wcnt[w][d];
+        wcnt[w][d] = run;
+        run += c;
       }
-      status_store(st, kStPre | (excl + run));
+      uint32_t* st = status + tile * 256 + d;
+      uint32_t excl = 0;
+      if (tile == tfirst) {
+        status_store(st, kStPre | run);
+      } else {
+        status_store(st, kStAgg | run);
+        int64_t j = tile - 1;
+        uint32_t polls = 0;
+        for (;;) {
+          const uint32_t w = status_load(status + j * 256 + d);
+          const uint32_t state = w & ~kStCount;
+          if (state == 0) {
+            if (++polls > kSortSpinLimit) {
+              atomicOr(err, kErrSort);
+              break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+            continue;
+          }
+          excl += w & kStCount;
+          if (state == kStPre || j == tfirst) break;
+          --j;
+        }
+        status_store(st, kStPre | (excl + run));
+      }
+      uint32_t tot;
+      dpre[d] = block_exclusive_scan<uint32_t>(run, lds4, tot);
+      goff[d] = (SEG ? sg.base[((int64_t)t * kMaxPasses + pass) * 256 + d] : gbase[d]) + excl;
     }
-    uint32_t tot;
-    dpre[d] = block_exclusive_scan<uint32_t>(run, lds4, tot);
-    goff[d] = gbase[d] + excl;
-  }
-  __syncthreads();
+    __syncthreads();
 #pragma unroll
-  for (int i = 0; i < kRadixItems; ++i) {
-    const int64_t p = base + i * 64 + lane;
-    if (p < n) {
-      const uint32_t d = (k[i] >> shift) & 255u;
-      const uint32_t pos = dpre[d] + wcnt[wv][d] + rank[i];
-      skey[pos] = k[i];
-      sval[pos] = v[i];
+    for (int i = 0; i < kRadixItems; ++i) {
+      const int64_t p = base + i * 64 + lane;
+      if (p < hi) {
+        const uint32_t d = digit(k[i]);
+        const uint32_t pos = dpre[d] + wcnt[wv][d] + rank[i];
+        skey[pos] = k[i];
+        sval[pos] = v[i];
+      }
     }
-  }
-  __syncthreads();
-  const int cnt = (int)min((int64_t)kRadixTile, n - tile0);
-  for (int j = threadIdx.x; j < cnt; j += kRadixThreads) {
-    const uint32_t key = skey[j];
-    const uint32_t d = (key >> shift) & 255u;
-    const uint32_t g = goff[d] + (uint32_t)j - dpre[d];
-    if ((int64_t)g < n) {  // always, unless a look-back gave up
-      kout[g] = key;
-      vout[g] = sval[j];
+    __syncthreads();
+    const int cnt = (int)(hi - lo);
+    for (int j = threadIdx.x; j < cnt; j += kRadixThreads) {
+      const uint32_t key = skey[j];
+      const uint32_t d = digit(key);
+      const uint32_t g = goff[d] + (uint32_t)j - dpre[d];
+      if ((int64_t)g < n) {  // always, unless a look-back gave up
+        kout[g] = key;
+        vout[g] = sval[j];
+      }
     }
   }
   // the other status buffer (the previous pass's, finished) is cleared for the next pass
   if (next_status) {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < status_words; i += stride) next_status[i] = 0;
+  }
+}
+
+// (src) -> (dst) pairs when *only_if is non-zero.
+__global__ __launch_bounds__(256) void k_copy_pairs(const uint32_t* __restrict__ ks, const uint32_t* __restrict__ vs,
+                                                    uint32_t* __restrict__ kd, uint32_t* __restrict__ vd, int64_t n,
+                                                    const uint32_t* __restrict__ only_if) {
+  if (*only_if == 0) return;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+    kd[i] = ks[i];
+    vd[i] = vs[i];
   }
 }
 
@@ -342,10 +520,54 @@ hipError_t sort_pairs(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32_t* vB, in
     uint32_t* ko = *in_B ? kA : kB;
     uint32_t* vo = *in_B ? vA : vB;
     uint32_t* next = pass + 1 < passes ? ss.status[(pass + 1) & 1] : nullptr;
-    k_sort_pass<<<(unsigned)nb, kRadixThreads, 0, s>>>(ki, vi, ko, vo, n, 8 * pass, ss.gbase + 256 * pass,
-                                                       ss.status[pass & 1], ss.tickets + pass, next, sw, err);
+    k_sort_pass<false><<<(unsigned)nb, kRadixThreads, 0, s>>>(ki, vi, ko, vo, n, 8 * pass, ss.gbase + 256 * pass,
+                                                              ss.status[pass & 1], ss.tickets + pass, next, sw, err,
+                                                              SegSort{}, nullptr, 0, pass, nullptr);
     *in_B = !*in_B;
   }
+  return hipGetLastError();
+}
+
+hipError_t sort_pairs_segmented(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32_t* vB, int64_t n, int passes,
+                                const int32_t* off, int32_t B, int T, const int64_t* key_base,
+                                const unsigned long long* ctr, const SortScratch& ss, const SegSort& sg, int32_t* err,
+                                int* in_B, hipStream_t s) {
+  *in_B = 0;
+  if (n <= 0) return hipSuccess;
+  if (passes < 1 || passes >= kMaxPasses || n > (int64_t)kStCount || T < 1) return hipErrorInvalidValue;
+  const int64_t nb_max = (n + kRadixTile - 1) / kRadixTile + T;  // every segment adds at most one partial tile
+  const int64_t sw = 256 * nb_max;
+  uint32_t* top_hist = ss.ghist;
+  uint32_t* top_base = ss.gbase;
+  k_sort_begin<<<1, 256, 0, s>>>(ss.ghist, ss.tickets);
+  k_seg_setup<<<1, 256, 0, s>>>(off, B, T, n, ctr, sg);
+  k_seg_hist<<<(unsigned)((nb_max + kSegHistTiles - 1) / kSegHistTiles), 256, 0, s>>>(
+      kA, n, passes, key_base, T, sg, top_hist, ss.status[0], sw);
+  k_seg_scan<<<(unsigned)T, 256, 0, s>>>(sg, passes, top_hist, top_base);
+  for (int pass = 0; pass < passes; ++pass) {
+    const uint32_t* ki = *in_B ? kB : kA;
+    const uint32_t* vi = *in_B ? vB : vA;
+    uint32_t* ko = *in_B ? kA : kB;
+    uint32_t* vo = *in_B ? vA : vB;
+    // the last segmented pass clears the status words of the pass for skipped keys
+    uint32_t* next = ss.status[(pass + 1) & 1];
+    k_sort_pass<true><<<(unsigned)nb_max, kRadixThreads, 0, s>>>(ki, vi, ko, vo, n, 8 * pass, nullptr,
+                                                                 ss.status[pass & 1], ss.tickets + pass, next, sw,
+                                                                 err, sg, key_base, T, pass, nullptr);
+    *in_B = !*in_B;
+  }
+  // skipped keys (top byte 255) behind every valid key, then back into the same buffer;
+  // both kernels return at once when there is none
+  uint32_t* kr = *in_B ? kB : kA;
+  uint32_t* vr = *in_B ? vB : vA;
+  uint32_t* ko = *in_B ? kA : kB;
+  uint32_t* vo = *in_B ? vA : vB;
+  const uint32_t* any_skipped = top_hist + 255;
+  const int64_t nb = (n + kRadixTile - 1) / kRadixTile;
+  k_sort_pass<false><<<(unsigned)nb, kRadixThreads, 0, s>>>(kr, vr, ko, vo, n, 24, top_base,
+                                                            ss.status[passes & 1], ss.tickets + passes, nullptr,
+                                                            256 * nb, err, SegSort{}, nullptr, 0, 0, any_skipped);
+  k_copy_pairs<<<grid_for(n, 2048), 256, 0, s>>>(ko, vo, kr, vr, n, any_skipped);
   return hipGetLastError();
 }
 

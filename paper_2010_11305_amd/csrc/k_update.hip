@@ -911,7 +911,7 @@ __global__ __launch_bounds__(256) void k_update(Dev dv, Work w, const uint32_t* 
 
 // ---- one training step ----------------------------------------------------------------------
 hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int64_t L, const int32_t* off, int32_t B,
-                           const float* grad, uint64_t step64, int key_bits, bool decay,
+                           const float* grad, uint64_t step64, int key_bits, int seg_passes, bool decay,
                            const hipEvent_t* update_events, const SideStream& side, hipStream_t s) {
   const uint32_t step = (uint32_t)step64;
   k_bwd_begin<<<1, 256, 0, s>>>(d, w.ctr, L);
@@ -922,7 +922,14 @@ hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int6
   int in_B = 0;
   const SortScratch ss{w.sort_small, w.sort_small + kMaxPasses * 256, w.sort_small + 2 * kMaxPasses * 256,
                        {w.sort_status[0], w.sort_status[1]}};
-  e = sort_pairs(w.keysA, w.valsA, w.keysB, w.valsB, L, passes, ss, d.err, &in_B, s);
+  if (seg_passes > 0 && seg_passes < passes) {
+    const size_t TT = (size_t)d.T * kMaxPasses * 256;
+    const SegSort sg{w.sort_seg, w.sort_seg + (d.T + 1), w.sort_seg + 2 * (d.T + 1), w.sort_seg + 2 * (d.T + 1) + TT};
+    e = sort_pairs_segmented(w.keysA, w.valsA, w.keysB, w.valsB, L, seg_passes, off, B, d.T, d.key_base, w.ctr, ss,
+                             sg, d.err, &in_B, s);
+  } else {
+    e = sort_pairs(w.keysA, w.valsA, w.keysB, w.valsB, L, passes, ss, d.err, &in_B, s);
+  }
   if (e != hipSuccess) return e;
   const uint32_t* sk = in_B ? w.keysB : w.keysA;
   const uint32_t* sv = in_B ? w.valsB : w.valsA;

@@ -81,7 +81,7 @@ struct Plan {
   // state offsets
   size_t o_rec, o_crow, o_tag, o_ts, o_cnt, o_G, o_desc, o_keyb, o_stats, o_err, state_bytes, table_bytes;
   // workspace offsets
-  size_t o_kA, o_vA, o_kB, o_vB, o_ssmall, o_sst0, o_sst1, o_part, o_tcnt, o_tpre, o_uk, o_seg, o_setf, o_urow, o_utab, o_uslot,
+  size_t o_kA, o_vA, o_kB, o_vB, o_ssmall, o_sst0, o_sst1, o_sseg, o_part, o_tcnt, o_tpre, o_uk, o_seg, o_setf, o_urow, o_utab, o_uslot,
       o_uact, o_udest, o_umeta, o_nch, o_cbase, o_uvrow, o_uvu, o_partial, o_span, o_ubig, o_brows, o_bbound, o_bpart, o_tabf, o_src, o_ctr, ws_bytes;
   int64_t max_partials = 0;
   int64_t max_big = 0;
@@ -172,8 +172,9 @@ int plan_config(const emb_cache_config* c, Plan* p) {
   p->o_kB = take(4 * L);
   p->o_vB = take(4 * L);
   p->o_ssmall = take(4 * embc::kSortSmallWords);
-  p->o_sst0 = take(4 * embc::sort_status_words((int64_t)L));
-  p->o_sst1 = take(4 * embc::sort_status_words((int64_t)L));
+  p->o_sst0 = take(4 * embc::sort_status_words((int64_t)L, T));
+  p->o_sst1 = take(4 * embc::sort_status_words((int64_t)L, T));
+  p->o_sseg = take(4 * embc::sort_seg_words(T));
   p->o_part = take(8 * embc::scan_partial_words((int64_t)L + 256 * 64));
   p->o_tcnt = take(8 * embc::uniq_tile_words((int64_t)L));
   p->o_tpre = take(8 * embc::uniq_tile_words((int64_t)L));
@@ -219,6 +220,7 @@ struct emb_cache {
   embc::Work work;
   uint64_t step = 0;
   int key_bits = 1;
+  int seg_passes = 0;  // digit passes of the per-table sort, 0 = sort the whole key
   // measurement: event pairs around the row-update kernel of the last kTimedCalls calls
   static constexpr int kTimedCalls = 64;
   bool timing = false;
@@ -355,6 +357,15 @@ int create_impl(const emb_cache_config* cfg, void* state, size_t state_bytes, vo
   // every valid key is below 2^key_bits - 1, the skipped-lookup key truncated to key_bits
   h->key_bits = bit_length((uint64_t)p.total_keys);
   if (h->key_bits < 1) h->key_bits = 1;
+  // the lookups come grouped by table: sorting each table's segment by its local key
+  // takes fewer passes when every table's key range is much smaller than their sum
+  // (valid keys must keep a top byte below 255, that of the skipped-lookup key)
+  {
+    int64_t max_range = 1;
+    for (int t = 0; t < cfg->num_tables; ++t) max_range = std::max(max_range, p.key_base[t + 1] - p.key_base[t]);
+    const int seg = (bit_length((uint64_t)max_range) + 7) / 8;
+    h->seg_passes = (seg < (h->key_bits + 7) / 8 && p.total_keys <= 0xFF000000LL) ? seg : 0;
+  }
 
   uint8_t* sb = static_cast<uint8_t*>(state);
   embc::Dev& d = h->dev;
@@ -392,6 +403,7 @@ int create_impl(const emb_cache_config* cfg, void* state, size_t state_bytes, vo
   w.sort_small = reinterpret_cast<uint32_t*>(wb + p.o_ssmall);
   w.sort_status[0] = reinterpret_cast<uint32_t*>(wb + p.o_sst0);
   w.sort_status[1] = reinterpret_cast<uint32_t*>(wb + p.o_sst1);
+  w.sort_seg = reinterpret_cast<uint32_t*>(wb + p.o_sseg);
   w.part = reinterpret_cast<unsigned long long*>(wb + p.o_part);
   w.tile_cnt = reinterpret_cast<unsigned long long*>(wb + p.o_tcnt);
   w.tile_pre = reinterpret_cast<unsigned long long*>(wb + p.o_tpre);
@@ -472,7 +484,7 @@ int emb_cache_backward_update(emb_cache_t h, const int32_t* indices, int64_t num
   const hipEvent_t* tev = nullptr;
   if (h->timing) tev = &h->tev[2 * (h->timed % emb_cache::kTimedCalls)];
   const hipError_t e = embc::launch_backward(h->dev, h->work, indices, num_indices, offsets, batch, grad_out,
-                                             h->step, h->key_bits, decay, tev, h->side, S(stream));
+                                             h->step, h->key_bits, h->seg_passes, decay, tev, h->side, S(stream));
   if (e != hipSuccess) return EMB_EHIP;
   if (h->timing) h->timed += 1;
   h->step += 1;

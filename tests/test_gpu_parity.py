@@ -89,7 +89,31 @@ STEP_CASES = {
                    "cache_fraction": 0.07, "pooling": ("uniform", 1, 6)},
     "odd_tables_lfu_dm": {"rows": [3, 17, 999, 12289, 3], "batch": 150, "assoc": 1, "policy": "lfu",
                           "cache_fraction": 0.3},
+    # tables whose key ranges fit 16 bits while their sum needs 18: the per-table sort
+    # (2 digit passes per segment, several tiles per table, a 5-row table in one tile)
+    "seg_tables": {"rows": [40000, 5, 60001, 300, 50000, 30000], "batch": 512, "assoc": 8, "cache_fraction": 0.05,
+                   "pooling": ("poisson", 12), "zipf": 1.1},
+    "seg_tables_lfu_sr_adagrad": {"rows": [40000, 5, 60001, 300, 50000, 30000], "batch": 512, "assoc": 4,
+                                  "cache_fraction": 0.02, "policy": "lfu", "rounding": "stochastic",
+                                  "optimizer": "adagrad", "bits": 4, "sb_fp16": True, "dim": 32,
+                                  "pooling": ("poisson", 12), "zipf": 1.1},
+    # 360 small tables: every segment's keys fit one digit pass, their sum needs two
+    "seg_tables_small": {"rows": [200, 250, 17, 240, 1, 199] * 60, "batch": 40, "assoc": 2, "cache_fraction": 0.05,
+                         "pooling": ("uniform", 0, 5)},
 }
+
+
+def sort_passes(cfg):
+    """Digit passes of the sort of the whole key, and of the per-table sort (the
+    library picks the latter when it takes fewer passes)."""
+    ranges = []
+    for n in cfg["rows"]:
+        sets = int(np.floor(cfg["cache_fraction"] * n)) // cfg["assoc"] if cfg["cache_fraction"] > 0 else 0
+        if cfg["cache_fraction"] > 0:
+            sets = max(sets, 1)
+        ranges.append(sets * -(-n // sets) if sets else n)
+    total = sum(ranges)
+    return (int(total).bit_length() + 7) // 8, (int(max(ranges)).bit_length() + 7) // 8
 
 
 @pytest.mark.parametrize("case", list(STEP_CASES))
@@ -172,6 +196,43 @@ def test_kaggle_int4_full_size(torch):
         step_both(o, g, cfg, workload.make_step(cfg, k), torch)
     log("kaggle_int4: comparing state")
     compare_state(o, g, cfg)
+
+
+def test_seg_cases_take_the_per_table_sort():
+    for case in ("seg_tables", "seg_tables_lfu_sr_adagrad", "seg_tables_small"):
+        whole, seg = sort_passes(custom_cfg(**STEP_CASES[case]))
+        assert seg < whole, case
+    whole, seg = sort_passes(configs.get("industrial"))
+    assert (whole, seg) == (4, 3)
+
+
+def test_per_table_sort_with_skipped_lookups(torch):
+    """Per-table sort with skipped lookups inside bags (negative and out-of-range rows),
+    positions before the first and after the last bag, and tables without lookups."""
+    from paper_2010_11305_amd.emb_cache import EMB_EINDEX
+    cfg = custom_cfg(**dict(STEP_CASES["seg_tables"], batch=64))
+    assert sort_passes(cfg)[1] < sort_passes(cfg)[0]
+    rng = np.random.default_rng(11)
+    T, B = len(cfg["rows"]), cfg["batch"]
+    o, g = make_pair(cfg, max_indices=8192)
+    for k in range(4):
+        idx, off = [int(v) for v in rng.integers(-3, 10, size=3)], [3]
+        for t in range(T):
+            n_t = cfg["rows"][t]
+            for b in range(B):
+                m = 0 if (t == 3 or (t == 1 and k % 2)) else int(rng.integers(0, 9))
+                r = np.minimum(rng.zipf(1.2, size=m) - 1, n_t - 1)
+                bad = rng.random(m) < 0.1
+                r[bad] = rng.choice([-1, n_t, n_t + 7, -(2 ** 31)], size=int(bad.sum()))
+                idx += [int(v) for v in r]
+                off.append(len(idx))
+        idx += [5, -1]
+        st = {"indices": np.array(idx, dtype=np.int32), "offsets": np.array(off, dtype=np.int32), "batch": B,
+              "grad": rng.standard_normal((B, T, cfg["dim"])).astype(np.float32)}
+        log(f"per-table sort with skipped lookups: step {k}, {len(idx)} positions")
+        step_both(o, g, cfg, st, torch)
+        compare_state(o, g, cfg)
+        assert g.check() == EMB_EINDEX
 
 
 def test_invalid_indices_and_empty_bags(torch):
