@@ -357,6 +357,12 @@ __global__ __launch_bounds__(256) void k_seg_scan(SegSort sg, int passes, const 
 
 // One radix pass.  SEG: tiles of the segmented mode (sg, pass).  Otherwise tiles of the
 // whole stream; a non-null only_if skips the pass (and the copy below) unless *only_if.
+// With `once`, a workgroup handles the one tile its ticket names (grid = tiles: a new
+// workgroup's loads overlap the scatter of a finishing one).  Otherwise the grid is at
+// most what the device holds at once and every workgroup takes tiles from the ticket
+// until none is left (the pass that only runs when some key was skipped: when none
+// was, it ends after one read of the flag per workgroup).  Either way a look-back only
+// waits on tiles whose workgroups took their ticket earlier and are running.
 template <bool SEG>
 __global__ __launch_bounds__(kRadixThreads) void k_sort_pass(const uint32_t* __restrict__ kin,
                                                              const uint32_t* __restrict__ vin,
@@ -366,7 +372,8 @@ __global__ __launch_bounds__(kRadixThreads) void k_sort_pass(const uint32_t* __r
                                                              uint32_t* __restrict__ next_status,
                                                              int64_t status_words, int32_t* __restrict__ err,
                                                              SegSort sg, const int64_t* __restrict__ key_base, int T,
-                                                             int pass, const uint32_t* __restrict__ only_if) {
+                                                             int pass, const uint32_t* __restrict__ only_if,
+                                                             bool once) {
   __shared__ uint32_t wcnt[kRadixWaves][256];
   __shared__ uint32_t dpre[256];
   __shared__ uint32_t goff[256];
@@ -375,31 +382,28 @@ __global__ __launch_bounds__(kRadixThreads) void k_sort_pass(const uint32_t* __r
   __shared__ uint32_t lds4[4];
   __shared__ uint32_t tile_s;
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  for (int i = threadIdx.x; i < kRadixWaves * 256; i += kRadixThreads) (&wcnt[0][0])[i] = 0;
-  if (threadIdx.x == 0) tile_s = atomicAdd(ticket, 1u);
-  __syncthreads();
-  const int64_t tile = tile_s;
-  // the tile's table and position range (block-uniform)
-  bool work = true;
-  int t = 0;
-  int64_t tfirst = 0, lo = tile * kRadixTile, hi = min<int64_t>(n, lo + kRadixTile);
-  uint32_t kb = 0;
-  if (SEG) {
-    work = tile < (int64_t)sg.tbase[T];
-    if (work) {
+  const int64_t ntiles = SEG ? (int64_t)sg.tbase[T]
+                             : (only_if == nullptr || *only_if != 0) ? (n + kRadixTile - 1) / kRadixTile : 0;
+  for (;;) {
+    for (int i = threadIdx.x; i < kRadixWaves * 256; i += kRadixThreads) (&wcnt[0][0])[i] = 0;
+    if (threadIdx.x == 0) tile_s = ntiles > 0 ? atomicAdd(ticket, 1u) : 0xFFFFFFFFu;
+    __syncthreads();
+    const int64_t tile = tile_s;
+    if (tile >= ntiles) break;  // block-uniform
+    // the tile's table and position range
+    int t = 0;
+    int64_t tfirst = 0, lo = tile * kRadixTile, hi = min<int64_t>(n, lo + kRadixTile);
+    uint32_t kb = 0;
+    if (SEG) {
       t = seg_of_tile(sg.tbase, T, (uint32_t)tile);
       tfirst = sg.tbase[t];
       lo = sg.pos[t] + (tile - tfirst) * kRadixTile;
       hi = min<int64_t>(sg.pos[t + 1], lo + kRadixTile);
       kb = (uint32_t)key_base[t];
     }
-  } else {
-    work = lo < n && (only_if == nullptr || *only_if != 0);
-  }
-  const auto digit = [&](uint32_t key) -> uint32_t {
-    return SEG ? seg_digit(key, kb, shift) : (key >> shift) & 255u;
-  };
-  if (work) {
+    const auto digit = [&](uint32_t key) -> uint32_t {
+      return SEG ? seg_digit(key, kb, shift) : (key >> shift) & 255u;
+    };
     const int64_t base = lo + (int64_t)wv * 64 * kRadixItems;
     uint32_t k[kRadixItems], v[kRadixItems], rank[kRadixItems];
 #pragma unroll
@@ -484,6 +488,8 @@ __global__ __launch_bounds__(kRadixThreads) void k_sort_pass(const uint32_t* __r
         vout[g] = sval[j];
       }
     }
+    if (once) break;
+    __syncthreads();  // LDS is reused by the next tile
   }
   // the other status buffer (the previous pass's, finished) is cleared for the next pass
   if (next_status) {
@@ -504,6 +510,13 @@ __global__ __launch_bounds__(256) void k_copy_pairs(const uint32_t* __restrict__
   }
 }
 
+// workgroups of a pass that loops over `tiles` tiles: no more than the device holds at once
+template <bool SEG>
+unsigned pass_grid(int64_t tiles) {
+  const int64_t r = resident_grid(reinterpret_cast<const void*>(k_sort_pass<SEG>), kRadixThreads);
+  return (unsigned)std::max<int64_t>(1, std::min<int64_t>(tiles, r));
+}
+
 hipError_t sort_pairs(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32_t* vB, int64_t n, int passes,
                       const SortScratch& ss, int32_t* err, int* in_B, hipStream_t s) {
   *in_B = 0;
@@ -522,7 +535,7 @@ hipError_t sort_pairs(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32_t* vB, in
     uint32_t* next = pass + 1 < passes ? ss.status[(pass + 1) & 1] : nullptr;
     k_sort_pass<false><<<(unsigned)nb, kRadixThreads, 0, s>>>(ki, vi, ko, vo, n, 8 * pass, ss.gbase + 256 * pass,
                                                               ss.status[pass & 1], ss.tickets + pass, next, sw, err,
-                                                              SegSort{}, nullptr, 0, pass, nullptr);
+                                                              SegSort{}, nullptr, 0, pass, nullptr, true);
     *in_B = !*in_B;
   }
   return hipGetLastError();
@@ -553,7 +566,7 @@ hipError_t sort_pairs_segmented(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32
     uint32_t* next = ss.status[(pass + 1) & 1];
     k_sort_pass<true><<<(unsigned)nb_max, kRadixThreads, 0, s>>>(ki, vi, ko, vo, n, 8 * pass, nullptr,
                                                                  ss.status[pass & 1], ss.tickets + pass, next, sw,
-                                                                 err, sg, key_base, T, pass, nullptr);
+                                                                 err, sg, key_base, T, pass, nullptr, true);
     *in_B = !*in_B;
   }
   // skipped keys (top byte 255) behind every valid key, then back into the same buffer;
@@ -564,9 +577,10 @@ hipError_t sort_pairs_segmented(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32
   uint32_t* vo = *in_B ? vA : vB;
   const uint32_t* any_skipped = top_hist + 255;
   const int64_t nb = (n + kRadixTile - 1) / kRadixTile;
-  k_sort_pass<false><<<(unsigned)nb, kRadixThreads, 0, s>>>(kr, vr, ko, vo, n, 24, top_base,
+  k_sort_pass<false><<<pass_grid<false>(nb), kRadixThreads, 0, s>>>(kr, vr, ko, vo, n, 24, top_base,
                                                             ss.status[passes & 1], ss.tickets + passes, nullptr,
-                                                            256 * nb, err, SegSort{}, nullptr, 0, 0, any_skipped);
+                                                            256 * nb, err, SegSort{}, nullptr, 0, 0, any_skipped,
+                                                            false);
   k_copy_pairs<<<grid_for(n, 2048), 256, 0, s>>>(ko, vo, kr, vr, n, any_skipped);
   return hipGetLastError();
 }
