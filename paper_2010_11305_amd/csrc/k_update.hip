@@ -3,8 +3,9 @@
 // After the sort (k_sort.hip) the lookups are grouped by row, the rows by set:
 //   k_probe     per unique row: residency (slot or miss), LRU stamp / LFU count update
 //   k_partials  chunk sums (64 lookups each) of the merged gradient of rows with 65..512 lookups
-//   k_policy    per touched set, one wave (one lane per way): which missed rows enter the
-//               cache and which resident each of them displaces (decisions only)
+//   k_policy    per touched set, a group of G >= assoc lanes (one lane per way; 64/G sets
+//               per wave): which missed rows enter the cache and which resident each of
+//               them displaces (decisions only)
 //   k_block_partials  per (table, bag block): the block's gradient rows staged in LDS
 //               once, the block sums of every row with > 512 lookups; k_block_fold
 //               folds them per row (chunk sums are folded by the kernel that uses them)
@@ -597,19 +598,29 @@ struct PolicyStats {
   }
 };
 
+// G lanes per set (G >= assoc): a wave decides 64/G sets at once, each group of G
+// lanes on its own run of consecutive sets.  Every cross-lane step (ballot, shuffle,
+// LDS slot) stays inside the group, and every branch below is uniform over a group.
+template <int G>
 __global__ __launch_bounds__(256) void k_policy(Dev dv, Work w, uint32_t step) {
   __shared__ PolicyLds lds_all[4];
   PolicyLds& L = lds_all[threadIdx.x >> 6];
+  constexpr int NG = 64 / G;
   const int lane = threadIdx.x & 63;
+  const int gb = lane & ~(G - 1);  // the group's first lane
+  const int l = lane & (G - 1);    // lane within the group
+  const uint64_t gmask = G == 64 ? ~0ull : (((1ull << G) - 1) << gb);
+  const uint64_t below = lanemask_lt() & gmask;
   const int A = dv.assoc;
   const bool lru = dv.policy == 0;
   const int64_t nS = (int64_t)w.ctr[kCSets];
   const int64_t wave0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
-  // contiguous runs of sets per wave, so that the table (and its statistics) rarely changes
-  const int64_t per = (nS + nwaves - 1) / nwaves;
-  const int64_t k0 = wave0 * per, k1 = min<int64_t>(k0 + per, nS);
-  PolicyStats ps;  // meaningful in lane 0
+  // contiguous runs of sets per group, so that the table (and its statistics) rarely changes
+  const int64_t ngroups = nwaves * NG, grp = wave0 * NG + lane / G;
+  const int64_t per = (nS + ngroups - 1) / ngroups;
+  const int64_t k0 = grp * per, k1 = min<int64_t>(k0 + per, nS);
+  PolicyStats ps;  // meaningful in the group's lane 0
   for (int64_t k = k0; k < k1; ++k) {
     const int64_t u0 = w.set_first[k], u1 = w.set_first[k + 1];
     const int t = w.utab[u0];
@@ -621,29 +632,29 @@ __global__ __launch_bounds__(256) void k_policy(Dev dv, Work w, uint32_t step) {
     L.hitu[lane] = -1;
     __builtin_amdgcn_wave_barrier();
     int64_t M = 0;
-    for (int64_t c = u0; c < u1; c += 64) {
-      const int64_t u = c + lane;
+    for (int64_t c = u0; c < u1; c += G) {
+      const int64_t u = c + l;
       bool miss = false;
       if (u < u1) {
         const int32_t sl = w.uslot[u];
-        if (sl >= 0) L.hitu[sl - sbase] = (int32_t)u;
+        if (sl >= 0) L.hitu[gb + (sl - sbase)] = (int32_t)u;
         else miss = true;
       }
-      M += __popcll(__ballot(miss));
+      M += __popcll(__ballot(miss) & gmask);
     }
     __builtin_amdgcn_wave_barrier();
     if (M == 0) continue;
     if (t != ps.t) {
-      if (lane == 0) ps.flush(dv.stats);
+      if (l == 0) ps.flush(dv.stats);
       ps.t = t;
     }
 
     // ways, their tags and priorities (empty = lowest)
     int32_t tg = -1;
     long long vpv = LLONG_MAX;
-    if (lane < A) {
-      tg = dv.tag[sbase + lane];
-      vpv = tg < 0 ? LLONG_MIN : (lru ? (long long)dv.ts[sbase + lane] : (long long)dv.cnt[td.row_base + tg]);
+    if (l < A) {
+      tg = dv.tag[sbase + l];
+      vpv = tg < 0 ? LLONG_MIN : (lru ? (long long)dv.ts[sbase + l] : (long long)dv.cnt[td.row_base + tg]);
     }
     // lane k < n_ins: the k-th insert (unique row my_u) takes way my_way, displacing my_old
     // (-1 if the way was empty); my_hu is my_old's unique row if it was updated this step
@@ -654,89 +665,90 @@ __global__ __launch_bounds__(256) void k_policy(Dev dv, Work w, uint32_t step) {
     if (A == 1 && lru) {
       // direct-mapped LRU: no priority test; the largest missed row ends in the way
       int64_t win = -1;
-      for (int64_t c = u0; c < u1; c += 64) {
-        const int64_t u = c + lane;
+      for (int64_t c = u0; c < u1; c += G) {
+        const int64_t u = c + l;
         const bool miss = u < u1 && w.uslot[u] < 0;
-        const uint64_t m = __ballot(miss);
-        if (m) win = c + 63 - __clzll((unsigned long long)m);
+        const uint64_t m = __ballot(miss) & gmask;
+        if (m) win = c + (63 - __clzll((unsigned long long)m)) - gb;
       }
       n_ins = 1;
       my_u = (int32_t)win;
-      my_old = __shfl(tg, 0);
-      my_hu = my_old >= 0 ? L.hitu[0] : -1;
+      my_old = __shfl(tg, gb);
+      my_hu = my_old >= 0 ? L.hitu[gb] : -1;
     } else {
-      // victims ranked by (priority asc, way asc); every lane runs the shuffles
+      // victims ranked by (priority asc, way asc); every lane of the group runs the shuffles
       int vr = 0;
       for (int j = 0; j < A; ++j) {
-        const long long pj = __shfl(vpv, j);
-        vr += (pj < vpv || (pj == vpv && j < lane)) ? 1 : 0;
+        const long long pj = __shfl(vpv, gb + j);
+        vr += (pj < vpv || (pj == vpv && j < l)) ? 1 : 0;
       }
-      if (lane < A) {
-        L.vic_way[vr] = lane;
-        L.vic_pv[vr] = vpv;
+      if (l < A) {
+        L.vic_way[gb + vr] = l;
+        L.vic_pv[gb + vr] = vpv;
       }
       // candidates ranked by (priority desc, row asc); only ranks < A matter
       const int64_t K = M < A ? M : A;
       if (lru) {
         int64_t seen = 0;
-        for (int64_t c = u0; c < u1 && seen < K; c += 64) {
-          const int64_t u = c + lane;
+        for (int64_t c = u0; c < u1 && seen < K; c += G) {
+          const int64_t u = c + l;
           const bool miss = u < u1 && w.uslot[u] < 0;
-          const uint64_t m = __ballot(miss);
-          const int64_t rank = seen + __popcll(m & lanemask_lt());
+          const uint64_t m = __ballot(miss) & gmask;
+          const int64_t rank = seen + __popcll(m & below);
           if (miss && rank < K) {
-            L.cand_u[rank] = (int32_t)u;
-            L.cand_pv[rank] = (long long)step;
+            L.cand_u[gb + rank] = (int32_t)u;
+            L.cand_pv[gb + rank] = (long long)step;
           }
           seen += __popcll(m);
         }
       } else {
-        for (int64_t c = u0; c < u1; c += 64) {
-          const int64_t u = c + lane;
+        for (int64_t c = u0; c < u1; c += G) {
+          const int64_t u = c + l;
           const bool miss = u < u1 && w.uslot[u] < 0;
           const long long mypv = miss ? (long long)dv.cnt[w.urow[u]] : 0;
           const int32_t myrow = u < u1 ? w.urow[u] : 0;
           int64_t rank = 0;
-          for (int64_t c2 = u0; c2 < u1; c2 += 64) {
-            const int64_t u2 = c2 + lane;
+          for (int64_t c2 = u0; c2 < u1; c2 += G) {
+            const int64_t u2 = c2 + l;
             const bool miss2 = u2 < u1 && w.uslot[u2] < 0;
             const long long pv2 = miss2 ? (long long)dv.cnt[w.urow[u2]] : 0;
             const int32_t row2 = u2 < u1 ? w.urow[u2] : 0;
-            for (int j = 0; j < 64; ++j) {
-              const long long pj = __shfl(pv2, j);
-              const int32_t rj = __shfl(row2, j);
-              const int mj = __shfl((int)miss2, j);
+#pragma unroll 4
+            for (int j = 0; j < G; ++j) {
+              const long long pj = __shfl(pv2, gb + j);
+              const int32_t rj = __shfl(row2, gb + j);
+              const int mj = __shfl((int)miss2, gb + j);
               if (mj && (pj > mypv || (pj == mypv && rj < myrow))) ++rank;
             }
           }
           if (miss && rank < K) {
-            L.cand_u[rank] = (int32_t)u;
-            L.cand_pv[rank] = mypv;
+            L.cand_u[gb + rank] = (int32_t)u;
+            L.cand_pv[gb + rank] = mypv;
           }
         }
       }
       __builtin_amdgcn_wave_barrier();
       // the k-th candidate takes the k-th victim while strictly higher; stop at the first failure
-      const bool ok = lane < K && L.cand_pv[lane] > L.vic_pv[lane];
-      const uint64_t fail = __ballot(lane < K && !ok);
-      n_ins = fail ? __ffsll((unsigned long long)fail) - 1 : (int)K;
-      my_way = lane < n_ins ? L.vic_way[lane] : 0;
-      my_old = __shfl(tg, my_way);
-      my_u = lane < n_ins ? L.cand_u[lane] : -1;
-      my_hu = (lane < n_ins && my_old >= 0) ? L.hitu[my_way] : -1;
+      const bool ok = l < K && L.cand_pv[gb + l] > L.vic_pv[gb + l];
+      const uint64_t fail = __ballot(l < K && !ok) & gmask;
+      n_ins = fail ? __ffsll((unsigned long long)fail) - 1 - gb : (int)K;
+      my_way = l < n_ins ? L.vic_way[gb + l] : 0;
+      my_old = __shfl(tg, gb + my_way);
+      my_u = l < n_ins ? L.cand_u[gb + l] : -1;
+      my_hu = (l < n_ins && my_old >= 0) ? L.hitu[gb + my_way] : -1;
       __builtin_amdgcn_wave_barrier();
     }
-    if (lane < n_ins) {
+    if (l < n_ins) {
       w.uact[my_u] = kActInsert;
       w.udest[my_u] = (int32_t)(sbase + my_way);
       w.uvic_row[my_u] = my_old;
       w.uvic_u[my_u] = my_hu;
       if (my_hu >= 0) w.uact[my_hu] = kActDone;  // handled by the row that displaces it
     }
-    const uint32_t n_valid = (uint32_t)__popcll(__ballot(lane < n_ins && my_old >= 0));
-    const uint32_t n_hitev = (uint32_t)__popcll(__ballot(lane < n_ins && my_hu >= 0));
-    if (lane == 0 && n_hitev) atomicAdd(&w.ctr[kCHitEv], (unsigned long long)n_hitev);
-    if (lane == 0) {
+    const uint32_t n_valid = (uint32_t)__popcll(__ballot(l < n_ins && my_old >= 0) & gmask);
+    const uint32_t n_hitev = (uint32_t)__popcll(__ballot(l < n_ins && my_hu >= 0) & gmask);
+    if (l == 0 && n_hitev) atomicAdd(&w.ctr[kCHitEv], (unsigned long long)n_hitev);
+    if (l == 0) {
       ps.ins += (uint32_t)n_ins;
       ps.byp += (uint32_t)(M - n_ins);
       ps.ev += n_valid;
@@ -744,7 +756,7 @@ __global__ __launch_bounds__(256) void k_policy(Dev dv, Work w, uint32_t step) {
       ps.he += n_hitev;
     }
   }
-  if (lane == 0) ps.flush(dv.stats);
+  if (l == 0) ps.flush(dv.stats);
 }
 
 // ---- displaced residents -> T -----------------------------------------------------------------
@@ -960,7 +972,9 @@ hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int6
       hipError_t e2 = hipEventRecord(side.fork, s);
       if (e2 == hipSuccess) e2 = hipStreamWaitEvent(side.s, side.fork, 0);
       if (e2 != hipSuccess) return e2;
-      k_policy<<<grid(k_policy), 256, 0, side.s>>>(d, w, step);
+      if (d.assoc <= 16) k_policy<16><<<grid(k_policy<16>), 256, 0, side.s>>>(d, w, step);
+      else if (d.assoc <= 32) k_policy<32><<<grid(k_policy<32>), 256, 0, side.s>>>(d, w, step);
+      else k_policy<64><<<grid(k_policy<64>), 256, 0, side.s>>>(d, w, step);
       k_evict<D, BITS, SB16, false><<<grid(k_evict<D, BITS, SB16, false>), 256, 0, side.s>>>(d, w, sv, grad, step);
       e2 = hipEventRecord(side.join, side.s);
       if (e2 != hipSuccess) return e2;
