@@ -357,13 +357,13 @@ __global__ __launch_bounds__(256) void k_seg_scan(SegSort sg, int passes, const 
 
 // One radix pass.  SEG: tiles of the segmented mode (sg, pass).  Otherwise tiles of the
 // whole stream; a non-null only_if skips the pass (and the copy below) unless *only_if.
-// With `once`, a workgroup handles the one tile its ticket names (grid = tiles: a new
-// workgroup's loads overlap the scatter of a finishing one).  Otherwise the grid is at
+// Without LOOP, a workgroup handles the one tile its ticket names (grid = tiles: a new
+// workgroup's loads overlap the scatter of a finishing one).  With LOOP the grid is at
 // most what the device holds at once and every workgroup takes tiles from the ticket
 // until none is left (the pass that only runs when some key was skipped: when none
 // was, it ends after one read of the flag per workgroup).  Either way a look-back only
 // waits on tiles whose workgroups took their ticket earlier and are running.
-template <bool SEG>
+template <bool SEG, bool LOOP>
 __global__ __launch_bounds__(kRadixThreads) void k_sort_pass(const uint32_t* __restrict__ kin,
                                                              const uint32_t* __restrict__ vin,
                                                              uint32_t* __restrict__ kout, uint32_t* __restrict__ vout,
@@ -372,8 +372,7 @@ __global__ __launch_bounds__(kRadixThreads) void k_sort_pass(const uint32_t* __r
                                                              uint32_t* __restrict__ next_status,
                                                              int64_t status_words, int32_t* __restrict__ err,
                                                              SegSort sg, const int64_t* __restrict__ key_base, int T,
-                                                             int pass, const uint32_t* __restrict__ only_if,
-                                                             bool once) {
+                                                             int pass, const uint32_t* __restrict__ only_if) {
   __shared__ uint32_t wcnt[kRadixWaves][256];
   __shared__ uint32_t dpre[256];
   __shared__ uint32_t goff[256];
@@ -488,7 +487,7 @@ __global__ __launch_bounds__(kRadixThreads) void k_sort_pass(const uint32_t* __r
         vout[g] = sval[j];
       }
     }
-    if (once) break;
+    if constexpr (!LOOP) break;
     __syncthreads();  // LDS is reused by the next tile
   }
   // the other status buffer (the previous pass's, finished) is cleared for the next pass
@@ -513,7 +512,7 @@ __global__ __launch_bounds__(256) void k_copy_pairs(const uint32_t* __restrict__
 // workgroups of a pass that loops over `tiles` tiles: no more than the device holds at once
 template <bool SEG>
 unsigned pass_grid(int64_t tiles) {
-  const int64_t r = resident_grid(reinterpret_cast<const void*>(k_sort_pass<SEG>), kRadixThreads);
+  const int64_t r = resident_grid(reinterpret_cast<const void*>(k_sort_pass<SEG, true>), kRadixThreads);
   return (unsigned)std::max<int64_t>(1, std::min<int64_t>(tiles, r));
 }
 
@@ -533,9 +532,9 @@ hipError_t sort_pairs(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32_t* vB, in
     uint32_t* ko = *in_B ? kA : kB;
     uint32_t* vo = *in_B ? vA : vB;
     uint32_t* next = pass + 1 < passes ? ss.status[(pass + 1) & 1] : nullptr;
-    k_sort_pass<false><<<(unsigned)nb, kRadixThreads, 0, s>>>(ki, vi, ko, vo, n, 8 * pass, ss.gbase + 256 * pass,
+    k_sort_pass<false, false><<<(unsigned)nb, kRadixThreads, 0, s>>>(ki, vi, ko, vo, n, 8 * pass, ss.gbase + 256 * pass,
                                                               ss.status[pass & 1], ss.tickets + pass, next, sw, err,
-                                                              SegSort{}, nullptr, 0, pass, nullptr, true);
+                                                              SegSort{}, nullptr, 0, pass, nullptr);
     *in_B = !*in_B;
   }
   return hipGetLastError();
@@ -564,9 +563,9 @@ hipError_t sort_pairs_segmented(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32
     uint32_t* vo = *in_B ? vA : vB;
     // the last segmented pass clears the status words of the pass for skipped keys
     uint32_t* next = ss.status[(pass + 1) & 1];
-    k_sort_pass<true><<<(unsigned)nb_max, kRadixThreads, 0, s>>>(ki, vi, ko, vo, n, 8 * pass, nullptr,
+    k_sort_pass<true, false><<<(unsigned)nb_max, kRadixThreads, 0, s>>>(ki, vi, ko, vo, n, 8 * pass, nullptr,
                                                                  ss.status[pass & 1], ss.tickets + pass, next, sw,
-                                                                 err, sg, key_base, T, pass, nullptr, true);
+                                                                 err, sg, key_base, T, pass, nullptr);
     *in_B = !*in_B;
   }
   // skipped keys (top byte 255) behind every valid key, then back into the same buffer;
@@ -577,10 +576,9 @@ hipError_t sort_pairs_segmented(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32
   uint32_t* vo = *in_B ? vA : vB;
   const uint32_t* any_skipped = top_hist + 255;
   const int64_t nb = (n + kRadixTile - 1) / kRadixTile;
-  k_sort_pass<false><<<pass_grid<false>(nb), kRadixThreads, 0, s>>>(kr, vr, ko, vo, n, 24, top_base,
+  k_sort_pass<false, true><<<pass_grid<false>(nb), kRadixThreads, 0, s>>>(kr, vr, ko, vo, n, 24, top_base,
                                                             ss.status[passes & 1], ss.tickets + passes, nullptr,
-                                                            256 * nb, err, SegSort{}, nullptr, 0, 0, any_skipped,
-                                                            false);
+                                                            256 * nb, err, SegSort{}, nullptr, 0, 0, any_skipped);
   k_copy_pairs<<<grid_for(n, 2048), 256, 0, s>>>(ko, vo, kr, vr, n, any_skipped);
   return hipGetLastError();
 }
