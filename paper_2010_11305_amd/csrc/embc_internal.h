@@ -27,6 +27,9 @@ constexpr uint32_t kKeyInvalid = 0xFFFFFFFFu;  // sort key of a skipped lookup (
 constexpr int kSumChunk = 64;
 constexpr uint32_t kBlockAbove = 512;
 constexpr int kBlockFloats = 32768;
+// A bag block is staged in LDS in kStages runs of kBlockFloats/kStages floats.
+constexpr int kStages = 2;
+constexpr int64_t bound_stride(int64_t max_nblk) { return kStages * max_nblk + 1; }
 constexpr int kMaxAssoc = 64;
 
 enum : int32_t { kActHitStay = 0, kActHitEvict = 1, kActInsert = 2, kActBypass = 3 };
@@ -120,7 +123,7 @@ struct Work {
   uint2* chunk_span;     // [L/32 + 2] occurrences [x, y) of the sorted stream summed by each chunk
   uint32_t* ubig;        // [L] 1 for a row with more than kBlockAbove lookups, then its exclusive prefix
   int32_t* big_rows;     // [max_big] unique row of each such row ("big row"), in unique-row order
-  uint32_t* bbound;      // [max_big][max_nblk + 1] first occurrence of each bag block of a big row
+  uint32_t* bbound;      // [max_big][bound_stride(max_nblk)] first occurrence of each stage of a big row
   float* bpart;          // [max_big][max_nblk][dim] block sums of the big rows
   int64_t max_big;
   int32_t max_nblk;

@@ -255,7 +255,7 @@ __device__ __forceinline__ void fold_chunks(const float* __restrict__ partial, i
 template <int D>
 __device__ __forceinline__ void fold_blocks(const Work& w, int64_t h, int nblk, int g, float (&acc)[8]) {
   constexpr int U = 4;
-  const uint32_t* bb = w.bbound + h * (int64_t)(w.max_nblk + 1);
+  const uint32_t* bb = w.bbound + h * (int64_t)bound_stride(w.max_nblk);
   const float* bp = w.bpart + h * (int64_t)w.max_nblk * D;
   bool first = true;
   uint32_t prev = bb[0];
@@ -265,7 +265,7 @@ __device__ __forceinline__ void fold_blocks(const Work& w, int64_t h, int nblk, 
 #pragma unroll
     for (int q = 0; q < U; ++q) {
       const int k = min(k0 + q, nblk - 1);
-      nx[q] = bb[k + 1];
+      nx[q] = bb[(k + 1) * kStages];
       load_frow8(bp + (int64_t)k * D, g, x[q]);
     }
 #pragma unroll
@@ -309,21 +309,23 @@ __device__ __forceinline__ void merged_grad(const Work& w, const uint32_t* __res
   else sum_occ<D>(sval, s0, s1, gr, g, acc);
 }
 
-// bbound[h][k] = first occurrence of big row h whose bag lies in block k or after
-// (k = 0 .. nblk; bbound[h][nblk] = the end of its occurrences): one thread per
-// (row, block) binary-searches the row's occurrences, whose bags ascend.
-__global__ __launch_bounds__(256) void k_block_bounds(Work w, const uint32_t* __restrict__ sval, int nb_shift,
+// bbound[h][j] = first occurrence of big row h whose bag lies in stage j (the j-th run
+// of NB/kStages bags) or after (j = 0 .. kStages*nblk; the last = the end of its
+// occurrences): one thread per (row, stage) binary-searches the row's occurrences,
+// whose bags ascend.  Bag block k is stages kStages*k .. kStages*k + kStages - 1.
+__global__ __launch_bounds__(256) void k_block_bounds(Work w, const uint32_t* __restrict__ sval, int stage_shift,
                                                       int nblk) {
   const int64_t nbig = (int64_t)w.ctr[kCBig];
-  const int64_t n = nbig * (nblk + 1);
+  const int ns = kStages * nblk;
+  const int64_t n = nbig * (ns + 1);
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += stride) {
-    const int64_t h = e / (nblk + 1);
-    const int k = (int)(e - h * (nblk + 1));
+    const int64_t h = e / (ns + 1);
+    const int j = (int)(e - h * (ns + 1));
     const int64_t u = w.big_rows[h];
-    uint32_t a = w.seg[u], b = w.seg[u + 1];  // first occurrence with bag >= k*NB lies in [a, b]
-    if (k < nblk) {
-      const uint32_t key = (uint32_t)k << nb_shift;
+    uint32_t a = w.seg[u], b = w.seg[u + 1];  // first occurrence with bag >= j*NS lies in [a, b]
+    if (j < ns) {
+      const uint32_t key = (uint32_t)j << stage_shift;
       while (a < b) {
         const uint32_t m = a + (b - a) / 2;
         if (sval[m] < key) a = m + 1; else b = m;
@@ -331,43 +333,58 @@ __global__ __launch_bounds__(256) void k_block_bounds(Work w, const uint32_t* __
     } else {
       a = b;
     }
-    w.bbound[h * (int64_t)(w.max_nblk + 1) + k] = a;
+    w.bbound[h * (int64_t)bound_stride(w.max_nblk) + j] = a;
   }
 }
 
 // Block sums of the big rows: per (table t, bag block k), the gradient rows of the
-// block's NB bags are staged in LDS (128 KiB) once; then one group of GL = min(64, d)
-// lanes per big row of t (CL = d/GL columns per lane; rows taken longest first) sums
-// the row's occurrences in the block left to right (seeded with the first).  The bags of 4*GL occurrences are
-// loaded at a time (4 per lane) and U staged rows are read at a time.
-// Tables split over the XCDs.
-constexpr int kBlockThreads = 1024;
+// block's NB bags are staged in LDS a stage of NB/kStages bags (64 KiB) at a time, so
+// that two workgroups share a CU (while one waits on a long sum the other works); one
+// group of GL = min(64, d) lanes per big row of t with occurrences in the stage (CL =
+// d/GL columns per lane; rows taken longest first) adds them left to right to the
+// row's block sum, which starts from -0 (the identity of IEEE addition) in the block's
+// first stage with occurrences and is carried between stages in the row's block slot.
+// The bags of 4*GL occurrences are loaded at a time (4 per lane) and U staged rows are
+// read at a time.  Tables split over the XCDs; a workgroup takes every units-th
+// (segment, block) pair of its XCD.
+constexpr int kBlockThreads = 512;
 
 template <int D>
 __global__ __launch_bounds__(kBlockThreads) void k_block_partials(Dev dv, Work w, const uint32_t* __restrict__ sval,
                                                                   const float* __restrict__ grad, int32_t B,
                                                                   int nblk) {
   constexpr int NB = kBlockFloats / D;
+  constexpr int NS = NB / kStages;  // bags per stage
+  constexpr int SF = kBlockFloats / kStages;  // floats per stage
   constexpr int GL = D < 64 ? D : 64;  // lanes per row group
   constexpr int CL = D / GL;           // columns per lane (1, 2 or 4)
-  constexpr int GPB = kBlockThreads / GL;
   constexpr int U = 16;
-  constexpr int PER = kBlockFloats / 4 / kBlockThreads;  // float4 staged per thread
-  __shared__ float4 stage[kBlockFloats / 4];
+  constexpr int PER = SF / 4 / kBlockThreads;  // float4 staged per thread
+  __shared__ float4 stage[SF / 4];
   __shared__ uint32_t lrow[kBlockThreads], lr0[kBlockThreads], lr1[kBlockThreads], cnt_s[4];
   const float* sf = reinterpret_cast<const float*>(stage);
   const int l = threadIdx.x & (GL - 1);
   const XcdSplit xs(dv.T, true);
-  for (int seg = xs.xcd; seg < xs.segments(dv.T); seg += kXcds) {
+  const int64_t stride_b = bound_stride(w.max_nblk);
+  // (segment, block) pairs of this XCD: segment xs.xcd + kXcds*i holds blocks
+  // [klo, khi) of its table, at most kcap of them
+  const int64_t kcap = (nblk + xs.parts - 1) / xs.parts;
+  const int64_t nseg_x = (xs.segments(dv.T) - xs.xcd + kXcds - 1) / kXcds;
+  for (int64_t job = xs.unit; job < nseg_x * kcap; job += xs.units) {
+    const int seg = xs.xcd + kXcds * (int)(job / kcap);
     const int t = seg / xs.parts;
     const int64_t h0 = w.ubig[w.tab_first[t]], h1 = w.ubig[w.tab_first[t + 1]];
     if (h0 == h1) continue;
     int64_t klo, khi;
     part_range(0, nblk, seg % xs.parts, xs.parts, klo, khi);
-    for (int64_t k = klo + xs.unit; k < khi; k += xs.units) {
-      const int64_t bag0 = k * NB;
-      const int nrows = (int)min<int64_t>(NB, (int64_t)B - bag0);
-      __syncthreads();  // the previous block's sums are done with `stage`
+    const int64_t k = klo + job % kcap;
+    if (k >= khi) continue;
+    for (int hs = 0; hs < kStages; ++hs) {
+      const int64_t js = k * kStages + hs;  // stage index
+      const int64_t bag0 = js * NS;
+      if (bag0 >= B) break;
+      const int nrows = (int)min<int64_t>(NS, (int64_t)B - bag0);
+      __syncthreads();  // the previous stage's sums are done with `stage`
       {
         float4 v[PER];
 #pragma unroll
@@ -380,31 +397,32 @@ __global__ __launch_bounds__(kBlockThreads) void k_block_partials(Dev dv, Work w
         for (int q = 0; q < PER; ++q) stage[q * kBlockThreads + threadIdx.x] = v[q];
       }
       __syncthreads();
-      // the table's big rows, kBlockThreads at a time: their ranges in this block are
+      // the table's big rows, kBlockThreads at a time: their ranges in this stage are
       // listed in LDS with the rows of more than 4*GL occurrences first, and the row
       // groups take list entries in order (the longest sums start first)
       for (int64_t hc = h0; hc < h1; hc += kBlockThreads) {
         const int nr = (int)min<int64_t>(kBlockThreads, h1 - hc);
         if (threadIdx.x == 0) {
-          cnt_s[0] = 0;  // rows with more than 4*GL occurrences in the block
+          cnt_s[0] = 0;  // rows with more than 4*GL occurrences in the stage
           cnt_s[1] = 0;  // list positions taken by those rows
           cnt_s[2] = 0;  // list positions taken by the others (after them)
           cnt_s[3] = 0;  // next list entry for a row group
         }
         __syncthreads();
         uint32_t r0 = 0, r1 = 0;
-        bool heavy = false;
+        bool heavy = false, carry = false;
         if ((int)threadIdx.x < nr) {
-          const uint32_t* bb = w.bbound + (hc + threadIdx.x) * (int64_t)(w.max_nblk + 1);
-          r0 = bb[k];
-          r1 = bb[k + 1];
+          const uint32_t* bb = w.bbound + (hc + threadIdx.x) * stride_b;
+          r0 = bb[js];
+          r1 = bb[js + 1];
+          carry = bb[k * kStages] < r0;  // occurrences in an earlier stage of the block
           heavy = r1 - r0 > 4u * GL;
           if (heavy) atomicAdd(&cnt_s[0], 1u);
         }
         __syncthreads();
         if ((int)threadIdx.x < nr) {
           const uint32_t pos = heavy ? atomicAdd(&cnt_s[1], 1u) : cnt_s[0] + atomicAdd(&cnt_s[2], 1u);
-          lrow[pos] = (uint32_t)threadIdx.x;
+          lrow[pos] = (uint32_t)threadIdx.x | (carry ? 0x80000000u : 0u);
           lr0[pos] = r0;
           lr1[pos] = r1;
         }
@@ -414,14 +432,16 @@ __global__ __launch_bounds__(kBlockThreads) void k_block_partials(Dev dv, Work w
           if (l == 0) e = atomicAdd(&cnt_s[3], 1u);
           e = __shfl(e, 0, GL);
           if ((int)e >= nr) break;
-          const int64_t h = hc + lrow[e];
+          const uint32_t le = lrow[e];
+          const int64_t h = hc + (le & 0x7FFFFFFFu);
           const uint32_t i0 = lr0[e], i1 = lr1[e];
           if (i0 >= i1) continue;
-          // the sum starts from -0, the identity of IEEE addition: adding the first
-          // term gives exactly that term, as in the seeded left-to-right sum
+          // the block sum goes on from the earlier stages' terms, or starts from -0,
+          // the identity of IEEE addition: adding the first term gives exactly that term
+          float* o = w.bpart + (h * (int64_t)w.max_nblk + k) * D + l * CL;
           float acc[CL];
 #pragma unroll
-          for (int c = 0; c < CL; ++c) acc[c] = -0.0f;
+          for (int c = 0; c < CL; ++c) acc[c] = (le >> 31) ? o[c] : -0.0f;
           // runs of 4*GL occurrences: lane l holds the bags (relative to the block) of
           // occurrences 4l .. 4l+3 of the run; occurrence j of the run is component j%4
           // of lane j/4.  Every occurrence in [i0, i1) lies in the block; indices past
@@ -459,11 +479,10 @@ __global__ __launch_bounds__(kBlockThreads) void k_block_partials(Dev dv, Work w
             for (; j + U <= n; j += U) batch(j, U);  // full batches: no per-term test
             if (j < n) batch(j, n - j);
           }
-          float* o = w.bpart + (h * (int64_t)w.max_nblk + k) * D + l * CL;
 #pragma unroll
           for (int c = 0; c < CL; ++c) o[c] = acc[c];
         }
-        __syncthreads();  // every group is done with the list before it is rebuilt
+        __syncthreads();  // every group is done with the list (and its sums) before it is rebuilt
       }
     }
   }
@@ -961,9 +980,10 @@ hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int6
   k_chunk_spans<<<grid(k_chunk_spans), 256, 0, s>>>(w);
   // bag blocks of NB = kBlockFloats/d bags (a power of two) for the big rows
   const int nb_shift = __builtin_ctz((unsigned)(kBlockFloats / d.dim));
+  const int stage_shift = nb_shift - __builtin_ctz((unsigned)kStages);
   const int nblk = (int)(((int64_t)B + (kBlockFloats / d.dim) - 1) / (kBlockFloats / d.dim));
   if (nblk > w.max_nblk) return hipErrorInvalidValue;
-  if (nblk > 0) k_block_bounds<<<grid(k_block_bounds), 256, 0, s>>>(w, sv, nb_shift, nblk);
+  if (nblk > 0) k_block_bounds<<<grid(k_block_bounds), 256, 0, s>>>(w, sv, stage_shift, nblk);
   return dispatch_row(d.dim, d.bits, d.sb16, [&]<int D, int BITS, bool SB16>() -> hipError_t {
     // replacement decisions and the write-back of residents displaced without an update
     // on the side stream, the merged gradients on `s`; joined before the updates

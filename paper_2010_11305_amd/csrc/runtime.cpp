@@ -201,7 +201,7 @@ int plan_config(const emb_cache_config* c, Plan* p) {
     p->max_nblk = (int32_t)((c->max_batch + nb - 1) / nb);
   }
   p->o_brows = take(4 * (size_t)p->max_big);
-  p->o_bbound = take(4 * (size_t)p->max_big * (size_t)(p->max_nblk + 1));
+  p->o_bbound = take(4 * (size_t)p->max_big * (size_t)embc::bound_stride(p->max_nblk));
   p->o_bpart = take(4 * (size_t)p->max_big * (size_t)p->max_nblk * (size_t)c->dim);
   p->o_tabf = take(4 * (size_t)(T + 1));
   p->o_src = take(4 * L);
