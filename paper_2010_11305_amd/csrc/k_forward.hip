@@ -116,37 +116,62 @@ __global__ __launch_bounds__(256) void k_fwd_probe(Dev dv, const int32_t* __rest
     part_range(a, b, seg % xs.parts, xs.parts, lo, hi);
     const int32_t* tags = dv.tag + td.slot_base + sub * W;
     uint32_t ok = 0, hit = 0, bad = 0;
+    // the index loads run one iteration ahead of the tag loads, and every load is
+    // unconditional (a position past hi re-reads position lo, an invalid row probes
+    // set 0), so an iteration's tags are waited for with the next indices in flight
+    int32_t rn[PU];
+    if (lo + ptid < hi) {
+#pragma unroll
+      for (int q = 0; q < PU; ++q) {
+        const int64_t p = lo + ptid + q * pstride;
+        rn[q] = idx[p < hi ? p : lo];
+      }
+    }
     for (int64_t p0 = lo + ptid; p0 < hi; p0 += pstride * PU) {
       int32_t r[PU], found[PU];
       bool valid[PU];
+      int32_t tw[PU][W];
 #pragma unroll
       for (int q = 0; q < PU; ++q) {
-        const int64_t p = p0 + q * pstride;
-        r[q] = p < hi ? idx[p] : -1;
-      }
-#pragma unroll
-      for (int q = 0; q < PU; ++q) {
-        valid[q] = r[q] >= 0 && (int64_t)r[q] < td.N;
+        r[q] = rn[q];
+        valid[q] = p0 + q * pstride < hi && r[q] >= 0 && (int64_t)r[q] < td.N;
         found[q] = -1;
-        if (valid[q] && td.n_sets > 0) {
-          const int64_t set = (int64_t)mod_by((uint32_t)r[q], td.by_sets);
+      }
+      if (td.n_sets > 0) {
+#pragma unroll
+        for (int q = 0; q < PU; ++q) {
+          const int64_t set = valid[q] ? (int64_t)mod_by((uint32_t)r[q], td.by_sets) : 0;
           const int32_t* tg = tags + set * A;
-          int32_t tw[W];
           if constexpr (W % 4 == 0) {
 #pragma unroll
             for (int k = 0; k < W; k += 4) {
               const int4 v = *reinterpret_cast<const int4*>(tg + k);
-              tw[k] = v.x; tw[k + 1] = v.y; tw[k + 2] = v.z; tw[k + 3] = v.w;
+              tw[q][k] = v.x; tw[q][k + 1] = v.y; tw[q][k + 2] = v.z; tw[q][k + 3] = v.w;
             }
           } else if constexpr (W == 2) {
             const int2 v = *reinterpret_cast<const int2*>(tg);
-            tw[0] = v.x; tw[1] = v.y;
+            tw[q][0] = v.x; tw[q][1] = v.y;
           } else {
-            tw[0] = tg[0];
+            tw[q][0] = tg[0];
           }
+        }
+      }
+      // the next iteration's indices
+      {
+        const int64_t pn = p0 + pstride * PU;
+#pragma unroll
+        for (int q = 0; q < PU; ++q) {
+          const int64_t p = pn + q * pstride;
+          rn[q] = idx[p < hi ? p : lo];
+        }
+      }
+      if (td.n_sets > 0) {
+#pragma unroll
+        for (int q = 0; q < PU; ++q) {
+          const int64_t set = valid[q] ? (int64_t)mod_by((uint32_t)r[q], td.by_sets) : 0;
 #pragma unroll
           for (int k = 0; k < W; ++k)
-            if (tw[k] == r[q]) found[q] = (int32_t)(td.slot_base + set * A + sub * W + k);
+            if (valid[q] && tw[q][k] == r[q]) found[q] = (int32_t)(td.slot_base + set * A + sub * W + k);
         }
       }
 #pragma unroll
