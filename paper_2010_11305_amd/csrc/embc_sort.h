@@ -33,8 +33,8 @@ hipError_t sort_pairs(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32_t* vB, in
 
 // The same order from `passes` (< kMaxPasses) digit passes over each table's segment
 // of the stream (lookups of table t at [off[t*B], off[(t+1)*B])), sorted by the local
-// key; every table's key range must be below 2^(8*passes) and every valid key's top
-// byte below 255.  One more pass and a copy run only when some key is kKeyInvalid.
+// key; every table's key range must be below 2^(8*passes).  One more pass and a copy
+// run only when some key is kKeyInvalid.
 hipError_t sort_pairs_segmented(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32_t* vB, int64_t n, int passes,
                                 const int32_t* off, int32_t B, int T, const int64_t* key_base,
                                 const unsigned long long* ctr, const SortScratch& ss, const SegSort& sg, int32_t* err,

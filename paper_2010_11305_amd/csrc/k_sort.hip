@@ -160,9 +160,9 @@ __device__ __forceinline__ uint64_t match_digit(uint32_t d, bool valid) {
 // of 4).  Tiles never straddle a segment (each segment starts a new tile), a look-back
 // ends at the segment's first tile, and digit runs start at P_t.  A skipped lookup
 // (kKeyInvalid) takes digit 255 in every pass, above every valid local key, so it ends
-// its table's segment; when there is any, one more stable pass on the top byte of the
-// global key (255 only for kKeyInvalid) moves them behind every valid key, and the
-// pairs are copied back so that the result stays in the same buffer.
+// its table's segment; when there is any, one more stable pass (digit 1 for a skipped
+// key, 0 for the others) moves them behind every valid key, and the pairs are copied
+// back so that the result stays in the same buffer.
 constexpr uint32_t kStAgg = 1u << 30;
 constexpr uint32_t kStPre = 2u << 30;
 constexpr uint32_t kStCount = (1u << 30) - 1;
@@ -280,33 +280,34 @@ __global__ __launch_bounds__(256) void k_seg_setup(const int32_t* __restrict__ o
   for (int64_t i = threadIdx.x; i < hw; i += 256) sg.hist[i] = 0;
 }
 
-// Per-table histograms of the local-key digits of every segmented pass, and the global
-// histogram of the top byte of the key (for the pass that moves skipped keys last), in
-// one read of the keys; each block takes kSegHistTiles consecutive tiles and adds its
-// counts when the table changes.  Also clears the status words of the first pass.
+// Per-table histograms of the local-key digits of every segmented pass, and the number
+// of skipped keys (n_skipped[0], for the pass that moves them last), in one read of the
+// keys; each block takes kSegHistTiles consecutive tiles and adds its counts when the
+// table changes.  Also clears the status words of the first pass.
 constexpr int kSegHistTiles = 8;
 
 __global__ __launch_bounds__(256) void k_seg_hist(const uint32_t* __restrict__ keys, int64_t n, int passes,
                                                   const int64_t* __restrict__ key_base, int T, SegSort sg,
-                                                  uint32_t* __restrict__ top_hist, uint32_t* __restrict__ status,
+                                                  uint32_t* __restrict__ n_skipped, uint32_t* __restrict__ status,
                                                   int64_t status_words) {
-  __shared__ uint32_t h[kRadixWaves][kMaxPasses + 1][256];
+  __shared__ uint32_t h[kRadixWaves][kMaxPasses][256];
+  __shared__ uint32_t skipped_s;
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  for (int i = threadIdx.x; i < kRadixWaves * (kMaxPasses + 1) * 256; i += 256) (&h[0][0][0])[i] = 0;
+  for (int i = threadIdx.x; i < kRadixWaves * kMaxPasses * 256; i += 256) (&h[0][0][0])[i] = 0;
+  if (threadIdx.x == 0) skipped_s = 0;
   __syncthreads();
   const uint32_t ntiles = sg.tbase[T];
   int cur = -1;  // table whose counts the LDS holds
   const auto flush = [&](int t) {
     __syncthreads();
-    for (int p = 0; p <= passes; ++p) {
+    for (int p = 0; p < passes; ++p) {
       uint32_t c = 0;
 #pragma unroll
       for (int w = 0; w < kRadixWaves; ++w) {
         c += h[w][p][threadIdx.x];
         h[w][p][threadIdx.x] = 0;
       }
-      if (c) atomicAdd(p < passes ? &sg.hist[((int64_t)t * kMaxPasses + p) * 256 + threadIdx.x]
-                                  : &top_hist[threadIdx.x], c);
+      if (c) atomicAdd(&sg.hist[((int64_t)t * kMaxPasses + p) * 256 + threadIdx.x], c);
     }
     __syncthreads();
   };
@@ -324,8 +325,10 @@ __global__ __launch_bounds__(256) void k_seg_hist(const uint32_t* __restrict__ k
       const int64_t i = i0 + lane;
       const bool valid = i < hi;
       const uint32_t k = valid ? keys[i] : 0u;
-      for (int p = 0; p <= passes; ++p) {
-        const uint32_t d = p < passes ? seg_digit(k, kb, 8 * p) : k >> 24;
+      const uint32_t nsk = (uint32_t)__popcll(__ballot(valid && k == kKeyInvalid));
+      if (lane == 0 && nsk) atomicAdd(&skipped_s, nsk);
+      for (int p = 0; p < passes; ++p) {
+        const uint32_t d = seg_digit(k, kb, 8 * p);
         const uint32_t d0 = __shfl(d, 0);
         const uint64_t same = __ballot(valid && d == d0);
         if (lane == 0) atomicAdd(&h[wv][p][d0], (uint32_t)__popcll(same));
@@ -334,14 +337,17 @@ __global__ __launch_bounds__(256) void k_seg_hist(const uint32_t* __restrict__ k
     }
   }
   if (cur >= 0) flush(cur);
+  if (threadIdx.x == 0 && skipped_s) atomicAdd(n_skipped, skipped_s);
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < status_words; i += stride) status[i] = 0;
 }
 
 // base[t][p][d] = P_t + number of table t's keys whose pass-p digit is below d (one
-// block per table); block 0 also scans the top-byte histogram.
-__global__ __launch_bounds__(256) void k_seg_scan(SegSort sg, int passes, const uint32_t* __restrict__ top_hist,
-                                                  uint32_t* __restrict__ top_base) {
+// block per table); block 0 also writes the bases of the pass that moves skipped keys
+// last: valid keys from 0, skipped ones from n - n_skipped.
+__global__ __launch_bounds__(256) void k_seg_scan(SegSort sg, int passes, int64_t n,
+                                                  const uint32_t* __restrict__ n_skipped,
+                                                  uint32_t* __restrict__ skip_base) {
   __shared__ uint32_t lds4[4];
   const int t = blockIdx.x;
   for (int p = 0; p < passes; ++p) {
@@ -349,21 +355,22 @@ __global__ __launch_bounds__(256) void k_seg_scan(SegSort sg, int passes, const 
     uint32_t tot;
     sg.base[i] = sg.pos[t] + block_exclusive_scan<uint32_t>(sg.hist[i], lds4, tot);
   }
-  if (t == 0) {
-    uint32_t tot;
-    top_base[threadIdx.x] = block_exclusive_scan<uint32_t>(top_hist[threadIdx.x], lds4, tot);
-  }
+  if (t == 0 && threadIdx.x < 2) skip_base[threadIdx.x] = threadIdx.x == 0 ? 0u : (uint32_t)(n - n_skipped[0]);
 }
 
-// One radix pass.  SEG: tiles of the segmented mode (sg, pass).  Otherwise tiles of the
-// whole stream; a non-null only_if skips the pass (and the copy below) unless *only_if.
+// One radix pass.  kModeSeg: tiles of the segmented mode (sg, pass), digits of the local
+// key.  Otherwise tiles of the whole stream, with the key's digit at `shift`
+// (kModeWhole) or 1 for a skipped key and 0 for the others (kModeSkipped); a non-null
+// only_if skips the pass (and the copy below) unless *only_if.
 // Without LOOP, a workgroup handles the one tile its ticket names (grid = tiles: a new
 // workgroup's loads overlap the scatter of a finishing one).  With LOOP the grid is at
 // most what the device holds at once and every workgroup takes tiles from the ticket
 // until none is left (the pass that only runs when some key was skipped: when none
 // was, it ends after one read of the flag per workgroup).  Either way a look-back only
 // waits on tiles whose workgroups took their ticket earlier and are running.
-template <bool SEG, bool LOOP>
+constexpr int kModeWhole = 0, kModeSeg = 1, kModeSkipped = 2;
+
+template <int MODE, bool LOOP>
 __global__ __launch_bounds__(kRadixThreads) void k_sort_pass(const uint32_t* __restrict__ kin,
                                                              const uint32_t* __restrict__ vin,
                                                              uint32_t* __restrict__ kout, uint32_t* __restrict__ vout,
@@ -381,6 +388,7 @@ __global__ __launch_bounds__(kRadixThreads) void k_sort_pass(const uint32_t* __r
   __shared__ uint32_t lds4[4];
   __shared__ uint32_t tile_s;
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  constexpr bool SEG = MODE == kModeSeg;
   const int64_t ntiles = SEG ? (int64_t)sg.tbase[T]
                              : (only_if == nullptr || *only_if != 0) ? (n + kRadixTile - 1) / kRadixTile : 0;
   for (;;) {
@@ -401,7 +409,9 @@ __global__ __launch_bounds__(kRadixThreads) void k_sort_pass(const uint32_t* __r
       kb = (uint32_t)key_base[t];
     }
     const auto digit = [&](uint32_t key) -> uint32_t {
-      return SEG ? seg_digit(key, kb, shift) : (key >> shift) & 255u;
+      if constexpr (MODE == kModeSeg) return seg_digit(key, kb, shift);
+      else if constexpr (MODE == kModeSkipped) return key == kKeyInvalid ? 1u : 0u;
+      else return (key >> shift) & 255u;
     };
     const int64_t base = lo + (int64_t)wv * 64 * kRadixItems;
     uint32_t k[kRadixItems], v[kRadixItems], rank[kRadixItems];
@@ -510,9 +520,9 @@ __global__ __launch_bounds__(256) void k_copy_pairs(const uint32_t* __restrict__
 }
 
 // workgroups of a pass that loops over `tiles` tiles: no more than the device holds at once
-template <bool SEG>
+template <int MODE>
 unsigned pass_grid(int64_t tiles) {
-  const int64_t r = resident_grid(reinterpret_cast<const void*>(k_sort_pass<SEG, true>), kRadixThreads);
+  const int64_t r = resident_grid(reinterpret_cast<const void*>(k_sort_pass<MODE, true>), kRadixThreads);
   return (unsigned)std::max<int64_t>(1, std::min<int64_t>(tiles, r));
 }
 
@@ -532,7 +542,7 @@ hipError_t sort_pairs(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32_t* vB, in
     uint32_t* ko = *in_B ? kA : kB;
     uint32_t* vo = *in_B ? vA : vB;
     uint32_t* next = pass + 1 < passes ? ss.status[(pass + 1) & 1] : nullptr;
-    k_sort_pass<false, false><<<(unsigned)nb, kRadixThreads, 0, s>>>(ki, vi, ko, vo, n, 8 * pass, ss.gbase + 256 * pass,
+    k_sort_pass<kModeWhole, false><<<(unsigned)nb, kRadixThreads, 0, s>>>(ki, vi, ko, vo, n, 8 * pass, ss.gbase + 256 * pass,
                                                               ss.status[pass & 1], ss.tickets + pass, next, sw, err,
                                                               SegSort{}, nullptr, 0, pass, nullptr);
     *in_B = !*in_B;
@@ -549,13 +559,13 @@ hipError_t sort_pairs_segmented(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32
   if (passes < 1 || passes >= kMaxPasses || n > (int64_t)kStCount || T < 1) return hipErrorInvalidValue;
   const int64_t nb_max = (n + kRadixTile - 1) / kRadixTile + T;  // every segment adds at most one partial tile
   const int64_t sw = 256 * nb_max;
-  uint32_t* top_hist = ss.ghist;
-  uint32_t* top_base = ss.gbase;
+  uint32_t* n_skipped = ss.ghist;  // zeroed by k_sort_begin
+  uint32_t* skip_base = ss.gbase;
   k_sort_begin<<<1, 256, 0, s>>>(ss.ghist, ss.tickets);
   k_seg_setup<<<1, 256, 0, s>>>(off, B, T, n, ctr, sg);
   k_seg_hist<<<(unsigned)((nb_max + kSegHistTiles - 1) / kSegHistTiles), 256, 0, s>>>(
-      kA, n, passes, key_base, T, sg, top_hist, ss.status[0], sw);
-  k_seg_scan<<<(unsigned)T, 256, 0, s>>>(sg, passes, top_hist, top_base);
+      kA, n, passes, key_base, T, sg, n_skipped, ss.status[0], sw);
+  k_seg_scan<<<(unsigned)T, 256, 0, s>>>(sg, passes, n, n_skipped, skip_base);
   for (int pass = 0; pass < passes; ++pass) {
     const uint32_t* ki = *in_B ? kB : kA;
     const uint32_t* vi = *in_B ? vB : vA;
@@ -563,20 +573,20 @@ hipError_t sort_pairs_segmented(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32
     uint32_t* vo = *in_B ? vA : vB;
     // the last segmented pass clears the status words of the pass for skipped keys
     uint32_t* next = ss.status[(pass + 1) & 1];
-    k_sort_pass<true, false><<<(unsigned)nb_max, kRadixThreads, 0, s>>>(ki, vi, ko, vo, n, 8 * pass, nullptr,
+    k_sort_pass<kModeSeg, false><<<(unsigned)nb_max, kRadixThreads, 0, s>>>(ki, vi, ko, vo, n, 8 * pass, nullptr,
                                                                  ss.status[pass & 1], ss.tickets + pass, next, sw,
                                                                  err, sg, key_base, T, pass, nullptr);
     *in_B = !*in_B;
   }
-  // skipped keys (top byte 255) behind every valid key, then back into the same buffer;
-  // both kernels return at once when there is none
+  // skipped keys behind every valid key, then back into the same buffer; both kernels
+  // return at once when there is none
   uint32_t* kr = *in_B ? kB : kA;
   uint32_t* vr = *in_B ? vB : vA;
   uint32_t* ko = *in_B ? kA : kB;
   uint32_t* vo = *in_B ? vA : vB;
-  const uint32_t* any_skipped = top_hist + 255;
+  const uint32_t* any_skipped = n_skipped;
   const int64_t nb = (n + kRadixTile - 1) / kRadixTile;
-  k_sort_pass<false, true><<<pass_grid<false>(nb), kRadixThreads, 0, s>>>(kr, vr, ko, vo, n, 24, top_base,
+  k_sort_pass<kModeSkipped, true><<<pass_grid<kModeSkipped>(nb), kRadixThreads, 0, s>>>(kr, vr, ko, vo, n, 0, skip_base,
                                                             ss.status[passes & 1], ss.tickets + passes, nullptr,
                                                             256 * nb, err, SegSort{}, nullptr, 0, 0, any_skipped);
   k_copy_pairs<<<grid_for(n, 2048), 256, 0, s>>>(ko, vo, kr, vr, n, any_skipped);

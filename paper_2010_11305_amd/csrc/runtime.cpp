@@ -359,12 +359,11 @@ int create_impl(const emb_cache_config* cfg, void* state, size_t state_bytes, vo
   if (h->key_bits < 1) h->key_bits = 1;
   // the lookups come grouped by table: sorting each table's segment by its local key
   // takes fewer passes when every table's key range is much smaller than their sum
-  // (valid keys must keep a top byte below 255, that of the skipped-lookup key)
   {
     int64_t max_range = 1;
     for (int t = 0; t < cfg->num_tables; ++t) max_range = std::max(max_range, p.key_base[t + 1] - p.key_base[t]);
     const int seg = (bit_length((uint64_t)max_range) + 7) / 8;
-    h->seg_passes = (seg < (h->key_bits + 7) / 8 && p.total_keys <= 0xFF000000LL) ? seg : 0;
+    h->seg_passes = seg < (h->key_bits + 7) / 8 ? seg : 0;
   }
 
   uint8_t* sb = static_cast<uint8_t*>(state);
