@@ -165,7 +165,7 @@ def main():
                     help="override a field of the named workload (e.g. bits=16); int, float or text")
     ap.add_argument("--pool", type=int, default=3, help="distinct input batches cycled through")
     ap.add_argument("--stats-steps", type=int, default=3)
-    ap.add_argument("--cpu-steps", type=int, default=20)
+    ap.add_argument("--cpu-steps", type=int, default=60)
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
