@@ -358,7 +358,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_block_partials(Dev dv, Work w
   constexpr int SF = kBlockFloats / kStages;  // floats per stage
   constexpr int GL = D < 64 ? D : 64;  // lanes per row group
   constexpr int CL = D / GL;           // columns per lane (1, 2 or 4)
-  constexpr int U = 16;
+  constexpr int U = 8;
   constexpr int PER = SF / 4 / kBlockThreads;  // float4 staged per thread
   __shared__ float4 stage[SF / 4];
   __shared__ uint32_t lrow[kBlockThreads], lr0[kBlockThreads], lr1[kBlockThreads], cnt_s[4];
