@@ -48,10 +48,10 @@ __global__ void k_check_offsets(Dev dv, const int32_t* __restrict__ off, int64_t
 hipError_t launch_expand(const Dev& dv, const int32_t* idx, int64_t L, const int32_t* off, int32_t B, uint32_t* keys,
                          uint32_t* vals, unsigned long long* ctr, hipStream_t s);
 
-// Unique rows of the sorted stream sk[0, n): their keys, first occurrences and the first
-// unique row of each touched set (tile_cnt / tile_pre: uniq_tile_words(n) words each).
+// Unique rows of the sorted stream sk[0, n): their keys, first occurrences and tables, and
+// the first unique row of each touched set (tile_cnt / tile_pre: uniq_tile_words(n) words each).
 hipError_t launch_unique(const Dev& dv, const uint32_t* sk, int64_t n, unsigned long long* tile_cnt,
                          unsigned long long* tile_pre, unsigned long long* part, uint32_t* uk, uint32_t* seg,
-                         uint32_t* set_first, unsigned long long* ctr, hipStream_t s);
+                         uint32_t* set_first, int32_t* utab, unsigned long long* ctr, hipStream_t s);
 
 }  // namespace embc

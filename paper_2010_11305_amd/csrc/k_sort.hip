@@ -739,7 +739,7 @@ struct TabCursor {
   __device__ uint32_t set_of(uint32_t key) const { return div_by((uint32_t)((int64_t)key - kb), byQ); }
 };
 
-// Walks the thread's keys; calls on_start(i, key, is_set_start) for every row start.
+// Walks the thread's keys; calls on_start(i, key, is_set_start, table) for every row start.
 // Returns the index of the first invalid key if it lies in the thread's range, else -1.
 template <typename F>
 __device__ __forceinline__ int64_t walk_starts(const Dev& dv, const uint32_t* __restrict__ sk, int64_t n,
@@ -770,7 +770,7 @@ __device__ __forceinline__ int64_t walk_starts(const Dev& dv, const uint32_t* __
           pset = st;
         }
         pt = cur.t;
-        on_start(i, key, new_set);
+        on_start(i, key, new_set, cur.t);
       }
       prev = key;
     }
@@ -801,7 +801,7 @@ __global__ __launch_bounds__(256) void k_uniq_count(Dev dv, const uint32_t* __re
   uint32_t k[kUqPer];
   load_tile_keys(sk, n, i0, k);
   unsigned long long c = 0;
-  const int64_t fi = walk_starts(dv, sk, n, i0, k, [&](int64_t, uint32_t, bool ns) {
+  const int64_t fi = walk_starts(dv, sk, n, i0, k, [&](int64_t, uint32_t, bool ns, int) {
     c += 1ull + (ns ? (1ull << 32) : 0ull);
   });
   if (fi >= 0) ctr[kCValid] = (unsigned long long)fi;
@@ -813,7 +813,7 @@ __global__ __launch_bounds__(256) void k_uniq_count(Dev dv, const uint32_t* __re
 __global__ __launch_bounds__(256) void k_uniq_write(Dev dv, const uint32_t* __restrict__ sk, int64_t n,
                                                     const unsigned long long* __restrict__ tile_pre,
                                                     uint32_t* __restrict__ uk, uint32_t* __restrict__ seg,
-                                                    uint32_t* __restrict__ set_first,
+                                                    uint32_t* __restrict__ set_first, int32_t* __restrict__ utab,
                                                     unsigned long long* __restrict__ ctr) {
   __shared__ unsigned long long lds4[4];
   if (blockIdx.x == 0 && threadIdx.x == 0) {
@@ -828,13 +828,14 @@ __global__ __launch_bounds__(256) void k_uniq_write(Dev dv, const uint32_t* __re
   uint32_t k[kUqPer];
   load_tile_keys(sk, n, i0, k);
   unsigned long long c = 0;
-  walk_starts(dv, sk, n, i0, k, [&](int64_t, uint32_t, bool ns) { c += 1ull + (ns ? (1ull << 32) : 0ull); });
+  walk_starts(dv, sk, n, i0, k, [&](int64_t, uint32_t, bool ns, int) { c += 1ull + (ns ? (1ull << 32) : 0ull); });
   unsigned long long tot;
   const unsigned long long base = block_exclusive_scan<unsigned long long>(c, lds4, tot) + tile_pre[blockIdx.x];
   uint32_t u = (uint32_t)(base & 0xFFFFFFFFull), st = (uint32_t)(base >> 32);
-  walk_starts(dv, sk, n, i0, k, [&](int64_t i, uint32_t key, bool ns) {
+  walk_starts(dv, sk, n, i0, k, [&](int64_t i, uint32_t key, bool ns, int t) {
     uk[u] = key;
     seg[u] = (uint32_t)i;
+    utab[u] = t;
     if (ns) set_first[st++] = u;
     ++u;
   });
@@ -842,12 +843,13 @@ __global__ __launch_bounds__(256) void k_uniq_write(Dev dv, const uint32_t* __re
 
 hipError_t launch_unique(const Dev& dv, const uint32_t* sk, int64_t n, unsigned long long* tile_cnt,
                          unsigned long long* tile_pre, unsigned long long* part, uint32_t* uk, uint32_t* seg,
-                         uint32_t* set_first, unsigned long long* ctr, hipStream_t s) {
+                         uint32_t* set_first, int32_t* utab, unsigned long long* ctr, hipStream_t s) {
   const int64_t tiles = (n + kUqTile - 1) / kUqTile;
   if (tiles > 0) k_uniq_count<<<(unsigned)tiles, 256, 0, s>>>(dv, sk, n, tile_cnt, ctr);
   hipError_t e = scan_exclusive<unsigned long long>(tile_cnt, tile_pre, tiles, nullptr, part, ctr + kCScanTotal, s);
   if (e != hipSuccess) return e;
-  k_uniq_write<<<(unsigned)(tiles > 0 ? tiles : 1), 256, 0, s>>>(dv, sk, n, tile_pre, uk, seg, set_first, ctr);
+  k_uniq_write<<<(unsigned)(tiles > 0 ? tiles : 1), 256, 0, s>>>(dv, sk, n, tile_pre, uk, seg, set_first, utab,
+                                                                 ctr);
   return hipGetLastError();
 }
 

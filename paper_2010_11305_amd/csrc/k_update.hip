@@ -80,7 +80,7 @@ __global__ __launch_bounds__(256) void k_probe(Dev dv, Work w, uint32_t step) {
     bool nocache = false;
     if (act) {
       const uint32_t key = w.uniq_key[u];
-      t = table_of_key(dv.key_base, dv.T, key);
+      t = w.utab[u];  // written with the key by k_uniq_write
       const TableDesc td = dv.desc[t];
       const int64_t local = (int64_t)key - td.key_base;
       int64_t r = local;
@@ -93,7 +93,6 @@ __global__ __launch_bounds__(256) void k_probe(Dev dv, Work w, uint32_t step) {
       const uint32_t count = w.seg[u + 1] - w.seg[u];
       slot = probe_slot(dv, td, (int32_t)r);
       w.urow[u] = (int32_t)grow;
-      w.utab[u] = t;
       w.uslot[u] = slot;
       w.uact[u] = slot >= 0 ? kActHitStay : kActBypass;
       // chunks of kSumChunk lookups for 64 < count <= kBlockAbove; bag blocks above
@@ -964,7 +963,7 @@ hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int6
   if (e != hipSuccess) return e;
   const uint32_t* sk = in_B ? w.keysB : w.keysA;
   const uint32_t* sv = in_B ? w.valsB : w.valsA;
-  e = launch_unique(d, sk, L, w.tile_cnt, w.tile_pre, w.part, w.uniq_key, w.seg, w.set_first, w.ctr, s);
+  e = launch_unique(d, sk, L, w.tile_cnt, w.tile_pre, w.part, w.uniq_key, w.seg, w.set_first, w.utab, w.ctr, s);
   if (e != hipSuccess) return e;
   const auto grid = [](auto kernel) { return resident_grid(reinterpret_cast<const void*>(kernel)); };
   k_probe<<<grid(k_probe), 256, 0, s>>>(d, w, step);
