@@ -54,6 +54,8 @@ constexpr int kMaxPasses = 4;  // 8-bit digits of a 32-bit sort key
 struct DivConst {
   uint32_t d = 1, m = 1, s1 = 0, s2 = 0;
 };
+// Its magic numbers for 1 <= d < 2^31 (host).
+DivConst div_const(uint32_t d);
 
 struct TableDesc {
   int64_t N;

@@ -599,7 +599,7 @@ hipError_t sort_pairs_segmented(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32
 // key: set-major row key (kKeyInvalid for an out-of-range row); value: the bag b
 // within its table (its gradient row in grad_out [B][T][d] is b*T + t).
 __global__ __launch_bounds__(256) void k_expand(Dev dv, const int32_t* __restrict__ idx, int64_t L,
-                                                const int32_t* __restrict__ off, int32_t B,
+                                                const int32_t* __restrict__ off, int32_t B, DivConst byB,
                                                 uint32_t* __restrict__ keys, uint32_t* __restrict__ vals,
                                                 int64_t nbag_waves, const unsigned long long* __restrict__ ctr) {
   const int lane = threadIdx.x & 63;
@@ -630,10 +630,14 @@ __global__ __launch_bounds__(256) void k_expand(Dev dv, const int32_t* __restric
   const int64_t P0 = min<int64_t>(max<int64_t>(off[bag0], 0), L);
   const int64_t P1 = min<int64_t>(max<int64_t>(off[lastbag], P0), L);
   uint32_t n_ok = 0, n_bad = 0;
-  int t_run = (int)(bag0 / B);
+  // global bags are below 2^32 (checked when the handle is created): their table by
+  // one high multiply; the descriptor of the wave's first table is loaded once
+  const int t_run = (int)div_by((uint32_t)bag0, byB);
+  const TableDesc td_run = dv.desc[t_run];
   for (int64_t pc = P0; pc < P1; pc += 64) {
     const int64_t p = pc + lane;
     const bool in = p < P1;
+    const int32_t r = in ? idx[p] : 0;  // in flight during the search
     // largest lane j with start_j <= p
     int j = 0;
 #pragma unroll
@@ -642,11 +646,10 @@ __global__ __launch_bounds__(256) void k_expand(Dev dv, const int32_t* __restric
       if (j + step < 64 && s2 <= p) j += step;
     }
     if (in) {
-      const int64_t bag = bag0 + j;
-      const int t = (int)(bag / B);
-      const int b = (int)(bag - (int64_t)t * B);
-      const TableDesc td = dv.desc[t];
-      const int32_t r = idx[p];
+      const uint32_t bag = (uint32_t)(bag0 + j);
+      const int t = (int)div_by(bag, byB);
+      const int b = (int)(bag - (uint32_t)t * (uint32_t)B);
+      const TableDesc td = t == t_run ? td_run : dv.desc[t];
       uint32_t key = kKeyInvalid;
       if (r >= 0 && (int64_t)r < td.N) {
         if (td.n_sets > 0) {
@@ -695,7 +698,8 @@ hipError_t launch_expand(const Dev& dv, const int32_t* idx, int64_t L, const int
   const int64_t nbag_waves = (nbags + 63) / 64;
   const int64_t tail_waves = 64;
   const int64_t waves = nbag_waves + tail_waves;
-  k_expand<<<(unsigned)((waves + 3) / 4), 256, 0, s>>>(dv, idx, L, off, B, keys, vals, nbag_waves, ctr);
+  const DivConst byB = div_const(B > 0 ? (uint32_t)B : 1u);  // no bag when B = 0
+  k_expand<<<(unsigned)((waves + 3) / 4), 256, 0, s>>>(dv, idx, L, off, B, byB, keys, vals, nbag_waves, ctr);
   return hipGetLastError();
 }
 

@@ -40,13 +40,9 @@ unsigned resident_grid(const void* kernel, int threads) {
   return n;
 }
 
-}  // namespace embc
-
-namespace {
-
 // Magic numbers of DivConst for 1 <= d < 2^31.
-embc::DivConst div_const(uint32_t d) {
-  embc::DivConst c;
+DivConst div_const(uint32_t d) {
+  DivConst c;
   uint32_t l = 0;
   while (l < 32 && (1ull << l) < d) ++l;  // ceil(log2 d)
   c.d = d;
@@ -56,6 +52,10 @@ embc::DivConst div_const(uint32_t d) {
   return c;
 }
 
+}  // namespace embc
+
+namespace {
+using embc::div_const;
 }  // namespace
 
 namespace {
