@@ -352,6 +352,9 @@ template <int D>
 __global__ __launch_bounds__(kBlockThreads) void k_block_partials(Dev dv, Work w, const uint32_t* __restrict__ sval,
                                                                   const float* __restrict__ grad, int32_t B,
                                                                   int nblk) {
+  // the gradient sums run beside the eviction on the second stream and decide when the
+  // row update can start: their waves issue first where they share a SIMD
+  __builtin_amdgcn_s_setprio(3);
   constexpr int NB = kBlockFloats / D;
   constexpr int NS = NB / kStages;  // bags per stage
   constexpr int SF = kBlockFloats / kStages;  // floats per stage
@@ -527,6 +530,9 @@ __global__ __launch_bounds__(256) void k_chunk_spans(Work w) {
 template <int D>
 __global__ __launch_bounds__(256) void k_partials(Dev dv, Work w, const uint32_t* __restrict__ sval,
                                                   const float* __restrict__ grad) {
+  // the gradient sums run beside the eviction on the second stream and decide when the
+  // row update can start: their waves issue first where they share a SIMD
+  __builtin_amdgcn_s_setprio(3);
   constexpr int LPR = Geo<D>::LPR;
   constexpr int GPB = 256 / LPR;
   const int g = threadIdx.x & (LPR - 1);
