@@ -97,6 +97,18 @@ STEP_CASES = {
                                   "cache_fraction": 0.02, "policy": "lfu", "rounding": "stochastic",
                                   "optimizer": "adagrad", "bits": 4, "sb_fp16": True, "dim": 32,
                                   "pooling": ("poisson", 12), "zipf": 1.1},
+    # rows with more than 512 lookups at every row width: bag blocks of 32768/d bags, staged
+    # in halves, with ragged last blocks and halves (d32: 1500 bags = blocks of 1024; d64:
+    # 700 of 512; d256: 300 of 128)
+    "big_rows_d32": {"rows": [200, 3000], "dim": 32, "batch": 1500, "pooling": ("poisson", 6), "zipf": 1.5,
+                     "assoc": 8, "cache_fraction": 0.1},
+    "big_rows_d64_lfu_sr": {"rows": [150, 900], "dim": 64, "batch": 700, "pooling": ("poisson", 5), "zipf": 1.4,
+                            "assoc": 4, "cache_fraction": 0.05, "policy": "lfu", "rounding": "stochastic",
+                            "bits": 4, "sb_fp16": True},
+    "big_rows_d256_adagrad": {"rows": [120], "dim": 256, "batch": 300, "pooling": ("poisson", 8), "zipf": 1.3,
+                              "assoc": 16, "cache_fraction": 0.3, "optimizer": "adagrad", "rounding": "stochastic"},
+    "big_rows_d128_fp16": {"rows": [400, 77], "dim": 128, "batch": 520, "pooling": ("poisson", 4), "zipf": 1.6,
+                           "assoc": 2, "cache_fraction": 0.05, "bits": 16, "optimizer": "adagrad"},
     # 360 small tables: every segment's keys fit one digit pass, their sum needs two
     "seg_tables_small": {"rows": [200, 250, 17, 240, 1, 199] * 60, "batch": 40, "assoc": 2, "cache_fraction": 0.05,
                          "pooling": ("uniform", 0, 5)},
@@ -196,6 +208,16 @@ def test_kaggle_int4_full_size(torch):
         step_both(o, g, cfg, workload.make_step(cfg, k), torch)
     log("kaggle_int4: comparing state")
     compare_state(o, g, cfg)
+
+
+def test_big_row_cases_have_rows_past_512_lookups():
+    """The cases above reach the block sums (a row with more than 512 lookups in a step)."""
+    for case in ("big_rows_d32", "big_rows_d64_lfu_sr", "big_rows_d256_adagrad", "big_rows_d128_fp16"):
+        cfg = custom_cfg(**STEP_CASES[case])
+        idx, off = workload.make_indices(cfg, 0)
+        B = cfg["batch"]
+        most = max(np.bincount(idx[off[t * B]:off[(t + 1) * B]]).max() for t in range(len(cfg["rows"])))
+        assert most > 512, case
 
 
 def test_seg_cases_take_the_per_table_sort():
