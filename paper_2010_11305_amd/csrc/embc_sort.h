@@ -9,6 +9,12 @@ template <typename T>
 hipError_t scan_exclusive(const T* in, T* out, int64_t n, const unsigned long long* dev_n, T* part, T* total,
                           hipStream_t s);
 
+// Exclusive scans of two u32 arrays in one pass (out_a / out_b may alias a / b; the sums
+// of a must stay below 2^32); *total = total(a) + total(b) * 2^32.
+hipError_t scan_exclusive_pair(const uint32_t* a, const uint32_t* b, uint32_t* out_a, uint32_t* out_b, int64_t n,
+                               const unsigned long long* dev_n, unsigned long long* part,
+                               unsigned long long* total, hipStream_t s);
+
 // Scratch of the radix sort, carved from the workspace.
 struct SortScratch {
   uint32_t* ghist;      // [kMaxPasses][256] digit counts

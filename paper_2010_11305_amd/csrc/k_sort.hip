@@ -119,6 +119,67 @@ hipError_t scan_exclusive(const T* in, T* out, int64_t n, const unsigned long lo
   return hipGetLastError();
 }
 
+// Exclusive scans of two u32 arrays at once (a + b * 2^32 as one u64 value per element:
+// the prefix sums of a stay below 2^32), written to out_a and out_b (which may be a and
+// b); *total = the two totals packed the same way.
+__global__ __launch_bounds__(kScanThreads) void k_scan2_reduce(const uint32_t* __restrict__ a,
+                                                               const uint32_t* __restrict__ b, int64_t n,
+                                                               const unsigned long long* dev_n,
+                                                               unsigned long long* part) {
+  __shared__ unsigned long long lds4[4];
+  if (dev_n) n = min(n, (int64_t)*dev_n);
+  if ((int64_t)blockIdx.x * kScanTile >= n) return;
+  const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
+  unsigned long long s = 0;
+#pragma unroll
+  for (int i = 0; i < kScanItems; ++i)
+    if (base + i < n) s += (unsigned long long)a[base + i] | ((unsigned long long)b[base + i] << 32);
+  unsigned long long tot;
+  block_exclusive_scan<unsigned long long>(s, lds4, tot);
+  if (threadIdx.x == 0) part[blockIdx.x] = tot;
+}
+
+__global__ __launch_bounds__(kScanThreads) void k_scan2_down(const uint32_t* a, const uint32_t* b, uint32_t* out_a,
+                                                             uint32_t* out_b, int64_t n,
+                                                             const unsigned long long* dev_n,
+                                                             const unsigned long long* part) {
+  __shared__ unsigned long long lds4[4];
+  if (dev_n) n = min(n, (int64_t)*dev_n);
+  if ((int64_t)blockIdx.x * kScanTile >= n) return;
+  const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
+  unsigned long long v[kScanItems];
+  unsigned long long s = 0;
+#pragma unroll
+  for (int i = 0; i < kScanItems; ++i) {
+    v[i] = base + i < n ? ((unsigned long long)a[base + i] | ((unsigned long long)b[base + i] << 32)) : 0ull;
+    s += v[i];
+  }
+  unsigned long long tot;
+  unsigned long long run = block_exclusive_scan<unsigned long long>(s, lds4, tot) + part[blockIdx.x];
+#pragma unroll
+  for (int i = 0; i < kScanItems; ++i) {
+    if (base + i < n) {
+      out_a[base + i] = (uint32_t)run;
+      out_b[base + i] = (uint32_t)(run >> 32);
+    }
+    run += v[i];
+  }
+}
+
+hipError_t scan_exclusive_pair(const uint32_t* a, const uint32_t* b, uint32_t* out_a, uint32_t* out_b, int64_t n,
+                               const unsigned long long* dev_n, unsigned long long* part,
+                               unsigned long long* total, hipStream_t s) {
+  if (n <= 0) {
+    k_scan_top<unsigned long long><<<1, kScanThreads, 0, s>>>(part, 0, 0, nullptr, total);
+    return hipGetLastError();
+  }
+  const int64_t nb = (n + kScanTile - 1) / kScanTile;
+  k_scan2_reduce<<<(unsigned)nb, kScanThreads, 0, s>>>(a, b, n, dev_n, part);
+  k_scan_top<unsigned long long><<<1, kScanThreads, 0, s>>>(part, nb, n, dev_n, total);
+  k_scan2_down<<<(unsigned)nb, kScanThreads, 0, s>>>(a, b, out_a, out_b, n, dev_n, part);
+  return hipGetLastError();
+}
+
 template hipError_t scan_exclusive<uint32_t>(const uint32_t*, uint32_t*, int64_t, const unsigned long long*,
                                              uint32_t*, uint32_t*, hipStream_t);
 template hipError_t scan_exclusive<unsigned long long>(const unsigned long long*, unsigned long long*, int64_t,

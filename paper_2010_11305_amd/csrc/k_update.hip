@@ -42,11 +42,12 @@ __device__ __forceinline__ void wave_stat_add(unsigned long long* stats, int t, 
   if (active && !same && v) atomicAdd(&stats[(int64_t)t * kNStat + field], (unsigned long long)v);
 }
 
-__global__ void k_chunks_total(unsigned long long* ctr) { ctr[kCChunks] = ctr[kCScanTotal] & 0xFFFFFFFFull; }
-
-// After the scan of the big-row flags: their total, also as ubig[nU].
-__global__ void k_big_total(Work w) {
-  const unsigned long long nb = w.ctr[kCScanTotal] & 0xFFFFFFFFull;
+// After the paired scan of the chunk counts and big-row flags: the chunk total, and the
+// big-row total, also as ubig[nU].
+__global__ void k_scan_totals(Work w) {
+  const unsigned long long tot = w.ctr[kCScanTotal];
+  w.ctr[kCChunks] = tot & 0xFFFFFFFFull;
+  const unsigned long long nb = tot >> 32;
   w.ctr[kCBig] = nb;
   w.ubig[w.ctr[kCUnique]] = (uint32_t)nb;
 }
@@ -974,14 +975,9 @@ hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int6
   const auto grid = [](auto kernel) { return resident_grid(reinterpret_cast<const void*>(kernel)); };
   k_probe<<<grid(k_probe), 256, 0, s>>>(d, w, step);
   k_tab_first<<<1, 256, 0, s>>>(w, d.T);
-  e = scan_exclusive<uint32_t>(w.nch, w.chunk_base, L, w.ctr + kCUnique, reinterpret_cast<uint32_t*>(w.part),
-                               reinterpret_cast<uint32_t*>(w.ctr + kCScanTotal), s);
+  e = scan_exclusive_pair(w.nch, w.ubig, w.chunk_base, w.ubig, L, w.ctr + kCUnique, w.part, w.ctr + kCScanTotal, s);
   if (e != hipSuccess) return e;
-  k_chunks_total<<<1, 1, 0, s>>>(w.ctr);
-  e = scan_exclusive<uint32_t>(w.ubig, w.ubig, L, w.ctr + kCUnique, reinterpret_cast<uint32_t*>(w.part),
-                               reinterpret_cast<uint32_t*>(w.ctr + kCScanTotal), s);
-  if (e != hipSuccess) return e;
-  k_big_total<<<1, 1, 0, s>>>(w);
+  k_scan_totals<<<1, 1, 0, s>>>(w);
   k_chunk_spans<<<grid(k_chunk_spans), 256, 0, s>>>(w);
   // bag blocks of NB = kBlockFloats/d bags (a power of two) for the big rows
   const int nb_shift = __builtin_ctz((unsigned)(kBlockFloats / d.dim));
