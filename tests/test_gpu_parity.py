@@ -287,6 +287,31 @@ def test_malformed_offsets_skip_the_step(torch):
     assert np.array_equal(before["codes"], after["codes"]) and g.stats(0)["unique"] == 0
 
 
+def test_malformed_offsets_per_table_sort(torch):
+    """Malformed offsets with the per-table sort (every key skipped, the stream one
+    segment): no fault, the flag set, no state change; the next good step matches the oracle."""
+    from paper_2010_11305_amd.emb_cache import EMB_EINDEX, EMB_OK
+    cfg = custom_cfg(**dict(STEP_CASES["seg_tables"], batch=64))
+    assert sort_passes(cfg)[1] < sort_passes(cfg)[0]
+    T, B = len(cfg["rows"]), cfg["batch"]
+    log("malformed offsets, per-table sort")
+    o, g = make_pair(cfg, max_indices=20000)
+    st = workload.make_step(cfg, 0)
+    before = [g.export_rows(t) for t in range(T)]
+    off = st["offsets"].copy()
+    off[T * B // 2] = off[-1] + 5   # past the end
+    idx_t, _, grad_t = to_dev(st, torch)
+    off_t = torch.from_numpy(off).cuda()
+    g.backward_update(idx_t, off_t, B, grad_t)
+    assert g.check() == EMB_EINDEX
+    for t in range(T):
+        assert np.array_equal(before[t]["codes"], g.export_rows(t)["codes"]) and g.stats(t)["unique"] == 0
+    g.step = o.step   # the skipped call still counted a step; the oracle made none
+    step_both(o, g, cfg, workload.make_step(cfg, 1), torch)
+    compare_state(o, g, cfg)
+    assert g.check() == EMB_OK
+
+
 def test_determinism_and_resume(torch):
     cfg = custom_cfg(bits=4, sb_fp16=True, rounding="stochastic", policy="lfu", lfu_decay_interval=2,
                      optimizer="adagrad", assoc=4)
