@@ -312,6 +312,41 @@ def test_malformed_offsets_per_table_sort(torch):
     assert g.check() == EMB_OK
 
 
+@pytest.mark.parametrize("case", ["tiny", "seg_tables"])
+def test_empty_steps(torch, case):
+    """A step without bags (B = 0) and a step whose bags are all empty (no lookups): no
+    fault, no error, pooled outputs +0, no state change; the oracle agrees on both, and
+    a full step afterwards still matches it."""
+    from paper_2010_11305_amd.emb_cache import EMB_OK
+    cfg = custom_cfg(**dict(STEP_CASES.get(case, {}), batch=32))
+    T, B, d = len(cfg["rows"]), cfg["batch"], cfg["dim"]
+    log(f"empty steps {case}")
+    o, g = make_pair(cfg, max_indices=30000)
+    step_both(o, g, cfg, workload.make_step(cfg, 0), torch)
+    before = [g.export_rows(t) for t in range(T)]
+    # no bags at all
+    st0 = {"indices": np.zeros(0, dtype=np.int32), "offsets": np.zeros(1, dtype=np.int32), "batch": 0,
+           "grad": np.zeros((0, T, d), dtype=np.float32)}
+    step_both(o, g, cfg, st0, torch)
+    # B bags per table, every one empty
+    st1 = {"indices": np.zeros(0, dtype=np.int32), "offsets": np.zeros(T * B + 1, dtype=np.int32), "batch": B,
+           "grad": np.ones((B, T, d), dtype=np.float32)}
+    idx, off, grad = to_dev(st1, torch)
+    out = g.forward(idx, off, B)
+    assert not torch.any(out != 0) and not torch.any(torch.signbit(out))
+    o.forward(st1["indices"], st1["offsets"], B)
+    g.backward_update(idx, off, B, grad)
+    o.backward_update(st1["indices"], st1["offsets"], B, st1["grad"])
+    torch.cuda.synchronize()
+    assert g.check() == EMB_OK
+    for t in range(T):
+        a = g.export_rows(t)
+        assert np.array_equal(a["codes"], before[t]["codes"]) and g.stats(t) == o.stats(t)
+    compare_state(o, g, cfg)
+    step_both(o, g, cfg, workload.make_step(cfg, 1), torch)
+    compare_state(o, g, cfg)
+
+
 def test_determinism_and_resume(torch):
     cfg = custom_cfg(bits=4, sb_fp16=True, rounding="stochastic", policy="lfu", lfu_decay_interval=2,
                      optimizer="adagrad", assoc=4)
