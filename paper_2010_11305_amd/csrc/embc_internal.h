@@ -108,6 +108,7 @@ struct Work {
   unsigned long long* part;  // scan partials
   unsigned long long* tile_cnt;  // unique rows and touched sets per tile of sorted keys, packed (sets << 32 | rows)
   unsigned long long* tile_pre;  // their exclusive prefix sums
+  unsigned long long* thread_pre;  // [256 per tile] each thread's offset inside its tile
   uint32_t* uniq_key;    // [L]
   uint32_t* seg;         // [L+1] start of each unique row's occurrences in the sorted stream
   uint32_t* set_first;   // [L+1] first unique row of each touched set

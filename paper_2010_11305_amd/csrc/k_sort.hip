@@ -860,6 +860,7 @@ __device__ __forceinline__ void load_tile_keys(const uint32_t* __restrict__ sk, 
 
 __global__ __launch_bounds__(256) void k_uniq_count(Dev dv, const uint32_t* __restrict__ sk, int64_t n,
                                                     unsigned long long* __restrict__ tile_cnt,
+                                                    unsigned long long* __restrict__ thread_pre,
                                                     unsigned long long* __restrict__ ctr) {
   __shared__ unsigned long long lds4[4];
   const int64_t i0 = (int64_t)blockIdx.x * kUqTile + (int64_t)threadIdx.x * kUqPer;
@@ -871,16 +872,16 @@ __global__ __launch_bounds__(256) void k_uniq_count(Dev dv, const uint32_t* __re
   });
   if (fi >= 0) ctr[kCValid] = (unsigned long long)fi;
   unsigned long long tot;
-  block_exclusive_scan<unsigned long long>(c, lds4, tot);
+  thread_pre[(int64_t)blockIdx.x * 256 + threadIdx.x] = block_exclusive_scan<unsigned long long>(c, lds4, tot);
   if (threadIdx.x == 0) tile_cnt[blockIdx.x] = tot;
 }
 
 __global__ __launch_bounds__(256) void k_uniq_write(Dev dv, const uint32_t* __restrict__ sk, int64_t n,
                                                     const unsigned long long* __restrict__ tile_pre,
+                                                    const unsigned long long* __restrict__ thread_pre,
                                                     uint32_t* __restrict__ uk, uint32_t* __restrict__ seg,
                                                     uint32_t* __restrict__ set_first, int32_t* __restrict__ utab,
                                                     unsigned long long* __restrict__ ctr) {
-  __shared__ unsigned long long lds4[4];
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     const unsigned long long tot = ctr[kCScanTotal];
     const uint32_t nu = (uint32_t)(tot & 0xFFFFFFFFull), ns = (uint32_t)(tot >> 32);
@@ -892,10 +893,8 @@ __global__ __launch_bounds__(256) void k_uniq_write(Dev dv, const uint32_t* __re
   const int64_t i0 = (int64_t)blockIdx.x * kUqTile + (int64_t)threadIdx.x * kUqPer;
   uint32_t k[kUqPer];
   load_tile_keys(sk, n, i0, k);
-  unsigned long long c = 0;
-  walk_starts(dv, sk, n, i0, k, [&](int64_t, uint32_t, bool ns, int) { c += 1ull + (ns ? (1ull << 32) : 0ull); });
-  unsigned long long tot;
-  const unsigned long long base = block_exclusive_scan<unsigned long long>(c, lds4, tot) + tile_pre[blockIdx.x];
+  // the thread's offset: its tile's, plus its own inside the tile (both from k_uniq_count)
+  const unsigned long long base = thread_pre[(int64_t)blockIdx.x * 256 + threadIdx.x] + tile_pre[blockIdx.x];
   uint32_t u = (uint32_t)(base & 0xFFFFFFFFull), st = (uint32_t)(base >> 32);
   walk_starts(dv, sk, n, i0, k, [&](int64_t i, uint32_t key, bool ns, int t) {
     uk[u] = key;
@@ -907,14 +906,15 @@ __global__ __launch_bounds__(256) void k_uniq_write(Dev dv, const uint32_t* __re
 }
 
 hipError_t launch_unique(const Dev& dv, const uint32_t* sk, int64_t n, unsigned long long* tile_cnt,
-                         unsigned long long* tile_pre, unsigned long long* part, uint32_t* uk, uint32_t* seg,
-                         uint32_t* set_first, int32_t* utab, unsigned long long* ctr, hipStream_t s) {
+                         unsigned long long* tile_pre, unsigned long long* thread_pre, unsigned long long* part,
+                         uint32_t* uk, uint32_t* seg, uint32_t* set_first, int32_t* utab, unsigned long long* ctr,
+                         hipStream_t s) {
   const int64_t tiles = (n + kUqTile - 1) / kUqTile;
-  if (tiles > 0) k_uniq_count<<<(unsigned)tiles, 256, 0, s>>>(dv, sk, n, tile_cnt, ctr);
+  if (tiles > 0) k_uniq_count<<<(unsigned)tiles, 256, 0, s>>>(dv, sk, n, tile_cnt, thread_pre, ctr);
   hipError_t e = scan_exclusive<unsigned long long>(tile_cnt, tile_pre, tiles, nullptr, part, ctr + kCScanTotal, s);
   if (e != hipSuccess) return e;
-  k_uniq_write<<<(unsigned)(tiles > 0 ? tiles : 1), 256, 0, s>>>(dv, sk, n, tile_pre, uk, seg, set_first, utab,
-                                                                 ctr);
+  k_uniq_write<<<(unsigned)(tiles > 0 ? tiles : 1), 256, 0, s>>>(dv, sk, n, tile_pre, thread_pre, uk, seg,
+                                                                 set_first, utab, ctr);
   return hipGetLastError();
 }
 

@@ -81,7 +81,7 @@ struct Plan {
   // state offsets
   size_t o_rec, o_crow, o_tag, o_ts, o_cnt, o_G, o_desc, o_keyb, o_stats, o_err, state_bytes, table_bytes;
   // workspace offsets
-  size_t o_kA, o_vA, o_kB, o_vB, o_ssmall, o_sst0, o_sst1, o_sseg, o_part, o_tcnt, o_tpre, o_uk, o_seg, o_setf, o_urow, o_utab, o_uslot,
+  size_t o_kA, o_vA, o_kB, o_vB, o_ssmall, o_sst0, o_sst1, o_sseg, o_part, o_tcnt, o_tpre, o_tthr, o_uk, o_seg, o_setf, o_urow, o_utab, o_uslot,
       o_uact, o_udest, o_umeta, o_nch, o_cbase, o_uvrow, o_uvu, o_partial, o_span, o_ubig, o_brows, o_bbound, o_bpart, o_tabf, o_src, o_ctr, ws_bytes;
   int64_t max_partials = 0;
   int64_t max_big = 0;
@@ -178,6 +178,7 @@ int plan_config(const emb_cache_config* c, Plan* p) {
   p->o_part = take(8 * embc::scan_partial_words((int64_t)L + 256 * 64));
   p->o_tcnt = take(8 * embc::uniq_tile_words((int64_t)L));
   p->o_tpre = take(8 * embc::uniq_tile_words((int64_t)L));
+  p->o_tthr = take(8 * 256 * embc::uniq_tile_words((int64_t)L));
   p->o_uk = take(4 * L);
   p->o_seg = take(4 * (L + 1));
   p->o_setf = take(4 * (L + 1));
@@ -406,6 +407,7 @@ int create_impl(const emb_cache_config* cfg, void* state, size_t state_bytes, vo
   w.part = reinterpret_cast<unsigned long long*>(wb + p.o_part);
   w.tile_cnt = reinterpret_cast<unsigned long long*>(wb + p.o_tcnt);
   w.tile_pre = reinterpret_cast<unsigned long long*>(wb + p.o_tpre);
+  w.thread_pre = reinterpret_cast<unsigned long long*>(wb + p.o_tthr);
   w.uniq_key = reinterpret_cast<uint32_t*>(wb + p.o_uk);
   w.seg = reinterpret_cast<uint32_t*>(wb + p.o_seg);
   w.set_first = reinterpret_cast<uint32_t*>(wb + p.o_setf);
