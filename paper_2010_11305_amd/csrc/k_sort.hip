@@ -276,7 +276,7 @@ __global__ __launch_bounds__(256) void k_sort_hist(const uint32_t* __restrict__ 
     const uint32_t k = valid ? keys[i] : 0u;
     for (int p = 0; p < passes; ++p) {
       const uint32_t d = (k >> (8 * p)) & 255u;
-      const uint32_t d0 = __shfl(d, 0);
+      const uint32_t d0 = __builtin_amdgcn_readfirstlane(d);  // all lanes active: lane 0's
       const uint64_t same = __ballot(valid && d == d0);
       if (lane == 0) atomicAdd(&h[wv][p][d0], (uint32_t)__popcll(same));
       if (valid && d != d0) atomicAdd(&h[wv][p][d], 1u);
@@ -388,13 +388,11 @@ __global__ __launch_bounds__(256) void k_seg_hist(const uint32_t* __restrict__ k
       const uint32_t k = valid ? keys[i] : 0u;
       const uint32_t nsk = (uint32_t)__popcll(__ballot(valid && k == kKeyInvalid));
       if (lane == 0 && nsk) atomicAdd(&skipped_s, nsk);
-      for (int p = 0; p < passes; ++p) {
-        const uint32_t d = seg_digit(k, kb, 8 * p);
-        const uint32_t d0 = __shfl(d, 0);
-        const uint64_t same = __ballot(valid && d == d0);
-        if (lane == 0) atomicAdd(&h[wv][p][d0], (uint32_t)__popcll(same));
-        if (valid && d != d0) atomicAdd(&h[wv][p][d], 1u);
-      }
+      // one LDS atomic per lane: within a table the digits of neighbouring lookups
+      // are spread, so the cross-lane step of a wave leader costs more than the
+      // collisions it saves; a wave of one digit serialises on one LDS word only
+      for (int p = 0; p < passes; ++p)
+        if (valid) atomicAdd(&h[wv][p][seg_digit(k, kb, 8 * p)], 1u);
     }
   }
   if (cur >= 0) flush(cur);
