@@ -192,9 +192,10 @@ __device__ __forceinline__ uint64_t match_digit(uint32_t d, bool valid) {
   uint64_t m = __ballot(valid);
 #pragma unroll
   for (int b = 0; b < 8; ++b) {
-    const bool bit = (d >> b) & 1u;
-    const uint64_t bb = __ballot(bit);
-    m &= bit ? bb : ~bb;
+    // keep the lanes whose bit b equals this lane's: bit b sign-extended, XNOR the ballot
+    const uint32_t s = (uint32_t)((int32_t)(d << (31 - b)) >> 31);
+    const uint64_t bb = __ballot(s != 0);
+    m &= ~(bb ^ (((uint64_t)s << 32) | s));
   }
   return m;
 }
@@ -488,12 +489,14 @@ __global__ __launch_bounds__(kRadixThreads) void k_sort_pass(const uint32_t* __r
       const uint32_t d = digit(k[i]);
       const uint64_t peers = match_digit(d, valid);
       const uint32_t before = (uint32_t)__popcll(peers & lanemask_lt());
+      // the first lane of each digit adds the digit's lanes to the wave's count and
+      // hands the old count to the others; a wave's LDS operations complete in issue
+      // order, so each item sees the counts of the items before it, and the 16
+      // atomics of a thread are in flight together
       uint32_t old = 0;
-      if (valid) old = wcnt[wv][d];
-      __builtin_amdgcn_wave_barrier();
-      if (valid && before == 0) wcnt[wv][d] = old + (uint32_t)__popcll(peers);
-      __builtin_amdgcn_wave_barrier();
-      rank[i] = old + before;
+      if (valid && before == 0) old = atomicAdd(&wcnt[wv][d], (uint32_t)__popcll(peers));
+      const int first = valid ? (int)__builtin_ctzll(peers) : lane;
+      rank[i] = __shfl(old, first) + before;
     }
     __syncthreads();
     {
