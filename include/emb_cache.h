@@ -146,7 +146,7 @@ int emb_cache_create(const emb_cache_config* cfg, void* state, size_t state_byte
  * `table` (table_bytes >= the queried table_bytes, 256-byte aligned) is device
  * memory, or pinned host memory from hipHostMalloc, which the kernels then reach
  * over the host link -- the paper's table in unified memory with the FP32 cache
- * in device memory (Sec. 5.3, Fig. 7).  `state` then needs only state_bytes -
+ * in device memory (Sec. 5.2 "Speed improvement", Fig. 9).  `state` then needs only state_bytes -
  * table_bytes.  Any other host memory is refused (EMB_EINVAL): a kernel could not
  * reach it.  Synchronizes `stream`. */
 int emb_cache_create_with_table(const emb_cache_config* cfg, void* state, size_t state_bytes, void* table,
@@ -156,13 +156,19 @@ int emb_cache_create_with_table(const emb_cache_config* cfg, void* state, size_t
 /* Release host metadata.  Does not touch device memory. */
 int emb_cache_destroy(emb_cache_t h);
 
-/* Fill every row of every table with x_j = u*(hi-lo)+lo (fused multiply-add),
- * u a 24-bit uniform from Philox4x32-10 keyed on init_seed with counter
- * (j/4, row, table, 0xFFFFFFFF), then quantize each row with round-to-nearest-
- * even (Alg. 1).  Empties the cache.  Enqueue-only. */
+/* Initial table.  The paper does not state how its tables are initialised; the
+ * reading here: fill every row of every table with x_j = u*(hi-lo)+lo (fused
+ * multiply-add), u a 24-bit uniform from Philox4x32-10 keyed on init_seed with
+ * counter (j/4, row, table, 0xFFFFFFFF), then down-convert each row into T as
+ * Sec. 3 "Precision" and Alg. 1 define it, with round-to-nearest-even ("Rounding"
+ * knob).  Empties the cache, zeroes LFU counts and Adagrad state.  Enqueue-only. */
 int emb_cache_init_uniform(emb_cache_t h, float lo, float hi, uint64_t init_seed, void* stream);
 
-/* Forward: pooled[b][t][:] = sum over positions p in [offsets[t*batch+b],
+/* Forward: the fetch operator of Sec. 3 (the FP32 cache row of a row resident
+ * in set h(i), else the row up-converted as in Alg. 1, q*s + b with one
+ * rounding), pooled per bag (multi-hot lookups, Sec. 5.1; the paper does not
+ * state the pooling mode, the reading is a sum):
+ * pooled[b][t][:] = sum over positions p in [offsets[t*batch+b],
  * offsets[t*batch+b+1]) of fetch(T_t, C_t, indices[p]), summed left to right
  * in FP32 starting from the first term; an empty bag gives +0.
  *   indices   device int32 [num_indices], flat, table-major.
@@ -172,19 +178,39 @@ int emb_cache_init_uniform(emb_cache_t h, float lo, float hi, uint64_t init_seed
 int emb_cache_forward(emb_cache_t h, const int32_t* indices, int64_t num_indices, const int32_t* offsets,
                       int32_t batch, float* out, void* stream);
 
-/* Backward + sparse update of one training step, for the same indices/offsets
- * as the forward and grad_out = dL/d(pooled), device FP32 [batch][num_tables][dim].
- * Per table: sort the lookups by row; merge each row's gradient (chunks of 64
- * occurrences in position order, each summed left to right, then the chunk
- * sums left to right); update priorities (LRU: hit ways stamped with the step;
- * LFU: count += occurrences, saturating); decide per set which missed rows
- * enter the cache (victims by (priority asc, way asc), empty ways first;
- * candidates by (priority desc, row asc); the k-th candidate takes the k-th
- * victim while its priority is strictly higher); apply SGD or row-wise
- * Adagrad in FP32 to fetch(T,C,row); write each row to its cache way, or
- * quantize it into T (nearest-even or stochastic rounding keyed on
- * (seed, step, table, row, column)); quantize displaced residents into T.
- * Then step += 1.  Enqueue-only. */
+/* Backward + sparse update of one training step: the update operator of Sec. 3
+ * under the "Cache Replacement Policy" knob and Alg. 2, applied once per unique
+ * row after the gradients of the mini-batch are sorted by row and merged
+ * (Sec. 5.1, "De-duplicate gradients"), for the same indices/offsets as the
+ * forward and grad_out = dL/d(pooled), device FP32 [batch][num_tables][dim].
+ * Per table:
+ *   - sort the lookups by row and merge each row's gradient, its lookups taken
+ *     in position order (the paper fixes no order; this one is fixed so that
+ *     results are reproducible bit for bit): up to 64 lookups summed left to
+ *     right from the first; 65..512 in chunks of 64 consecutive lookups, each
+ *     summed left to right, then the chunk sums left to right; more than 512
+ *     grouped by bag block (bags [k*NB, (k+1)*NB), NB = 32768/dim), each
+ *     non-empty group summed left to right, then the group sums left to right
+ *     in block order;
+ *   - update priorities (LRU: hit ways stamped with the step; LFU: count +=
+ *     occurrences, saturating; counts halved first on decay steps);
+ *   - decide per set which missed rows enter the cache (victims by (priority
+ *     asc, way asc), empty ways first; candidates by (priority desc, row asc);
+ *     the k-th candidate takes the k-th victim while its priority is strictly
+ *     higher; direct-mapped LRU always replaces);
+ *   - apply SGD or row-wise Adagrad in FP32 to fetch(T,C,row); write each row
+ *     to its cache way, or down-convert it into T (Alg. 1; nearest-even or
+ *     stochastic rounding keyed on (seed, step, table, row, column));
+ *     down-convert displaced residents into T.
+ * Then step += 1.  Enqueue-only.
+ * Malformed offsets (negative, decreasing, or past num_indices) reject the
+ * call on the device: it changes no table, cache, count or accumulator (not
+ * even the LFU decay of that step), its backward statistics read 0, and the
+ * next emb_cache_check returns EMB_EINDEX.  A rejected call still counts as a
+ * step (step += 1): the step counter lives on the host, which learns of the
+ * rejection only at that check; a caller that retries the step with corrected
+ * offsets gets LRU stamps and stochastic-rounding keys one step later, and a
+ * decay that fell on the rejected step is skipped. */
 int emb_cache_backward_update(emb_cache_t h, const int32_t* indices, int64_t num_indices, const int32_t* offsets,
                               int32_t batch, const float* grad_out, void* stream);
 

@@ -55,6 +55,7 @@ def lib():
         L.orc_set_step.argtypes = [P, c.c_uint64]
         L.orc_init_uniform.argtypes = [P, c.c_float, c.c_float, c.c_uint64]
         L.orc_forward.argtypes = [P, P, c.c_int64, P, c.c_int32, P]
+        L.orc_backward_update.restype = c.c_int
         L.orc_backward_update.argtypes = [P, P, c.c_int64, P, c.c_int32, P]
         L.orc_stats.argtypes = [P, c.c_int, P]
         L.orc_export_rows.argtypes = [P, c.c_int, c.c_int64, c.c_int64, P, P, P, P, P]
@@ -161,7 +162,8 @@ class Oracle:
         off = np.ascontiguousarray(offsets, dtype=np.int32)
         g = np.ascontiguousarray(grad, dtype=np.float32)
         assert off.size == self.T * batch + 1 and g.shape == (batch, self.T, self.dim)
-        lib().orc_backward_update(self._h, _ptr(idx), idx.size, _ptr(off), int(batch), _ptr(g))
+        # True when the call was rejected for malformed offsets (no state change; the step still counts)
+        return bool(lib().orc_backward_update(self._h, _ptr(idx), idx.size, _ptr(off), int(batch), _ptr(g)))
 
     def stats(self, t):
         out = np.zeros(NSTAT, dtype=np.int64)

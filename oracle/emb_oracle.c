@@ -486,11 +486,26 @@ enum { ACT_HIT_STAY = 0, ACT_HIT_EVICT = 1, ACT_INSERT = 2, ACT_BYPASS = 3 };
 #define SUM_BLOCK_ABOVE 512 /* rows with more occurrences sum by bag blocks */
 #define BLOCK_FLOATS 32768  /* a bag block spans 32768/d bags */
 
-void orc_backward_update(orc_t *o, const int32_t *idx, int64_t n_idx, const int32_t *off, int32_t B,
-                         const float *grad) {
+/* Returns 0, or 1 when the call is rejected: offsets that are negative, decrease,
+ * or point past the end of the indices make the call change no table, cache,
+ * count or accumulator (not even the LFU decay of that step); the backward
+ * statistics read 0 and the step counter still advances. */
+int orc_backward_update(orc_t *o, const int32_t *idx, int64_t n_idx, const int32_t *off, int32_t B,
+                        const float *grad) {
   const orc_config *c = &o->cfg;
   int T = c->num_tables, d = c->dim, A = c->assoc;
   uint64_t step = o->step;
+
+  for (int64_t i = 0; i < (int64_t)T * B; ++i) {
+    if (off[i] < 0 || off[i + 1] < off[i] || off[i + 1] > n_idx) {
+      for (int t = 0; t < T; ++t) {
+        for (int k = ST_BWD_LOOKUPS; k <= ST_HIT_EVICTIONS; ++k) o->tab[t].stat[k] = 0;
+        o->tab[t].stat[ST_INVALID_BWD] = 0;
+      }
+      o->step = step + 1;
+      return 1;
+    }
+  }
 
   /* Decay of LFU counts: halve every count at the start of every K-th step. */
   if (c->policy == ORC_LFU && c->lfu_decay_interval > 0 && step > 0 &&
@@ -760,6 +775,7 @@ void orc_backward_update(orc_t *o, const int32_t *idx, int64_t n_idx, const int3
     free(g); free(x); free(part);
   }
   o->step = step + 1;
+  return 0;
 }
 
 /* ------------------------------------------------------------------------- */

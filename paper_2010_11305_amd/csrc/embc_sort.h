@@ -51,6 +51,8 @@ hipError_t sort_pairs_segmented(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32
 __global__ void k_check_offsets(Dev dv, const int32_t* __restrict__ off, int64_t nbags, int64_t L,
                                 unsigned long long* __restrict__ ctr);
 
+// Lookups -> (set-major key, bag) pairs; every key is skipped when ctr[kCBadOffsets]
+// is set (k_check_offsets must have run first on the same stream).
 hipError_t launch_expand(const Dev& dv, const int32_t* idx, int64_t L, const int32_t* off, int32_t B, uint32_t* keys,
                          uint32_t* vals, unsigned long long* ctr, hipStream_t s);
 

@@ -200,7 +200,11 @@ __device__ __forceinline__ uint64_t match_digit(uint32_t d, bool valid) {
   return m;
 }
 
-// Stable LSD radix sort, one kernel per 8-bit digit pass ("single sweep"):
+// Stable LSD radix sort, one kernel per 8-bit digit pass, after the Onesweep method
+// (Adinets and Merrill, "Onesweep: A Faster Least Significant Digit Radix Sort for
+// GPUs", 2022): one histogram pass for every digit, then per digit pass a single
+// sweep in which each tile finds its output offsets by decoupled look-back (Merrill
+// and Garland, "Single-pass Parallel Prefix Scan with Decoupled Look-back", 2016):
 //   k_sort_hist   global histograms of every pass's digit in one read of the keys
 //   k_sort_scan   their exclusive prefix sums: where each digit's run starts
 //   k_sort_pass   per tile of kRadixTile pairs (tiles taken in launch order from an
@@ -755,8 +759,6 @@ __global__ __launch_bounds__(256) void k_check_offsets(Dev dv, const int32_t* __
 hipError_t launch_expand(const Dev& dv, const int32_t* idx, int64_t L, const int32_t* off, int32_t B, uint32_t* keys,
                          uint32_t* vals, unsigned long long* ctr, hipStream_t s) {
   const int64_t nbags = (int64_t)dv.T * B;
-  const unsigned cgrid = grid_for(nbags, 2048);
-  k_check_offsets<<<cgrid, 256, 0, s>>>(dv, off, nbags, L, ctr);
   const int64_t nbag_waves = (nbags + 63) / 64;
   const int64_t tail_waves = 64;
   const int64_t waves = nbag_waves + tail_waves;

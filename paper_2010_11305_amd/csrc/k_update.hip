@@ -63,8 +63,11 @@ __global__ void k_bwd_begin(Dev dv, unsigned long long* ctr, int64_t L) {
   }
 }
 
-// LFU decay: every count halved.
-__global__ __launch_bounds__(256) void k_decay(int32_t* __restrict__ cnt, int64_t n) {
+// LFU decay: every count halved, unless the step's offsets were rejected (such a call
+// changes no state).
+__global__ __launch_bounds__(256) void k_decay(int32_t* __restrict__ cnt, int64_t n,
+                                               const unsigned long long* __restrict__ ctr) {
+  if (ctr[kCBadOffsets]) return;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) cnt[i] >>= 1;
 }
@@ -952,7 +955,10 @@ hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int6
                            const hipEvent_t* update_events, const SideStream& side, hipStream_t s) {
   const uint32_t step = (uint32_t)step64;
   k_bwd_begin<<<1, 256, 0, s>>>(d, w.ctr, L);
-  if (decay && d.cnt) k_decay<<<grid_for(d.total_rows), 256, 0, s>>>(d.cnt, d.total_rows);
+  // offsets first: a rejected call must not reach the decay either
+  const int64_t nbags = (int64_t)d.T * B;
+  k_check_offsets<<<grid_for(nbags, 2048), 256, 0, s>>>(d, off, nbags, L, w.ctr);
+  if (decay && d.cnt) k_decay<<<grid_for(d.total_rows), 256, 0, s>>>(d.cnt, d.total_rows, w.ctr);
   hipError_t e = launch_expand(d, idx, L, off, B, w.keysA, w.valsA, w.ctr, s);
   if (e != hipSuccess) return e;
   const int passes = (key_bits + 7) / 8;

@@ -10,6 +10,7 @@
 #include <map>
 #include <mutex>
 #include <new>
+#include <tuple>
 #include <utility>
 #include <vector>
 
@@ -23,11 +24,11 @@ namespace embc {
 
 unsigned resident_grid(const void* kernel, int threads) {
   static std::mutex mu;
-  static std::map<std::pair<const void*, int>, unsigned> known;
+  static std::map<std::tuple<const void*, int, int>, unsigned> known;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) dev = 0;
   std::lock_guard<std::mutex> lock(mu);
-  const auto key = std::make_pair(kernel, dev);
+  const auto key = std::make_tuple(kernel, dev, threads);
   const auto it = known.find(key);
   if (it != known.end()) return it->second;
   int per_cu = 0, cus = 0;

@@ -1,5 +1,5 @@
 """Effective bandwidth against cache hit rate, with the low-precision table in device
-memory or in pinned host memory (the paper's Fig. 7 experiment, Sec. 5.3).
+memory or in pinned host memory (the experiment of Fig. 9 in Sec. 5.2, "Speed improvement").
 
 The paper puts a large FP16 table in unified memory and the FP32 LRU cache in device
 memory, and plots the effective bandwidth of the forward and backward passes against

@@ -303,12 +303,43 @@ def test_malformed_offsets_per_table_sort(torch):
     idx_t, _, grad_t = to_dev(st, torch)
     off_t = torch.from_numpy(off).cuda()
     g.backward_update(idx_t, off_t, B, grad_t)
+    assert o.backward_update(st["indices"], off, B, st["grad"])   # the oracle rejects it too
     assert g.check() == EMB_EINDEX
     for t in range(T):
         assert np.array_equal(before[t]["codes"], g.export_rows(t)["codes"]) and g.stats(t)["unique"] == 0
-    g.step = o.step   # the skipped call still counted a step; the oracle made none
+    assert g.step == o.step == 1   # the rejected call still counts a step on both sides
+    compare_state(o, g, cfg)
     step_both(o, g, cfg, workload.make_step(cfg, 1), torch)
     compare_state(o, g, cfg)
+    assert g.check() == EMB_OK
+
+
+def test_malformed_offsets_on_a_decay_step(torch):
+    """LFU with counts halved every 2 steps: the call of step 2 (a decay step) has
+    malformed offsets.  It is rejected on both sides without halving the counts, both
+    count the step, and the next steps (3 without decay, 4 with) match the oracle."""
+    from paper_2010_11305_amd.emb_cache import EMB_EINDEX, EMB_OK
+    cfg = custom_cfg(policy="lfu", lfu_decay_interval=2, assoc=4, rounding="stochastic")
+    B = cfg["batch"]
+    log("malformed offsets on an LFU decay step")
+    o, g = make_pair(cfg)
+    for k in range(2):
+        step_both(o, g, cfg, workload.make_step(cfg, k), torch)
+    counts = g.export_rows(0)["cnt"].copy()
+    assert counts.max() > 1
+    st = workload.make_step(cfg, 2)
+    off = st["offsets"].copy()
+    off[B // 2] = -1
+    idx_t, _, grad_t = to_dev(st, torch)
+    g.backward_update(idx_t, torch.from_numpy(off).cuda(), B, grad_t)
+    assert o.backward_update(st["indices"], off, B, st["grad"])
+    assert g.check() == EMB_EINDEX
+    assert np.array_equal(g.export_rows(0)["cnt"], counts)   # no decay on the rejected step
+    assert g.step == o.step == 3
+    compare_state(o, g, cfg)
+    for k in (3, 4):
+        step_both(o, g, cfg, workload.make_step(cfg, k), torch)
+        compare_state(o, g, cfg)
     assert g.check() == EMB_OK
 
 
