@@ -178,6 +178,24 @@ int emb_cache_init_uniform(emb_cache_t h, float lo, float hi, uint64_t init_seed
 int emb_cache_forward(emb_cache_t h, const int32_t* indices, int64_t num_indices, const int32_t* offsets,
                       int32_t batch, float* out, void* stream);
 
+/* Forward for callers that cannot allocate device memory or pass a workspace:
+ * code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation.  Same computation, results and statistics as emb_cache_forward,
+ * but the per-call temporaries (one code per lookup and a few counter words)
+ * live in a static device array owned by the library, EMB_NOALLOC_SCRATCH_BYTES
+ * (64 MiB) per GPU, instead of the handle's workspace; the call allocates
+ * nothing and calls no allocating routine.  num_indices may be at most
+ * EMB_NOALLOC_MAX_INDICES; beyond it the call returns EMB_ENOMEM and enqueues
+ * nothing (max_indices of the handle does not apply).  Each GPU the library
+ * runs on holds its own copy of the array from the first handle created on it
+ * until the process ends, and every call on that GPU shares it: calls that may
+ * overlap on one GPU (on several streams, or from several handles) race on it
+ * and must be serialised by the caller.  Enqueue-only. */
+#define EMB_NOALLOC_SCRATCH_BYTES (64u << 20)
+#define EMB_NOALLOC_MAX_INDICES ((int64_t)((EMB_NOALLOC_SCRATCH_BYTES - 256u) / 4u))
+int emb_cache_forward_noalloc(emb_cache_t h, const int32_t* indices, int64_t num_indices, const int32_t* offsets,
+                              int32_t batch, float* out, void* stream);
+
 /* Backward + sparse update of one training step: the update operator of Sec. 3
  * under the "Cache Replacement Policy" knob and Alg. 2, applied once per unique
  * row after the gradients of the mini-batch are sorted by row and merged

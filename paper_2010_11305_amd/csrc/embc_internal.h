@@ -157,6 +157,11 @@ hipError_t launch_reset_state(const Dev& d, hipStream_t s);
 hipError_t launch_init_uniform(const Dev& d, float lo, float hi, uint64_t init_seed, hipStream_t s);
 hipError_t launch_forward(const Dev& d, const Work& w, const int32_t* idx, int64_t L, const int32_t* off,
                           int32_t B, float* out, hipStream_t s);
+// The forward with its temporaries in the library's static scratch array instead of a
+// workspace (L <= EMB_NOALLOC_MAX_INDICES); scratch_dev from noalloc_scratch.
+hipError_t noalloc_scratch(uint8_t** out);
+hipError_t launch_forward_noalloc(const Dev& d, uint8_t* scratch_dev, const int32_t* idx, int64_t L,
+                                  const int32_t* off, int32_t B, float* out, hipStream_t s);
 // A second stream of the handle and two events: the replacement decisions and the
 // write-back of displaced residents run there while the merged gradients are summed
 // on the caller's stream.

@@ -1,5 +1,9 @@
 // State reset, uniform initialisation, and the forward pass:
 // pooled[b][t] = sum over the bag of fetch(T_t, C_t, i) (Sec. 3 fetch operator).
+#include <map>
+#include <mutex>
+
+#include "emb_cache.h"
 #include "embc_device.h"
 #include "embc_dispatch.h"
 #include "embc_sort.h"
@@ -329,6 +333,50 @@ hipError_t launch_forward(const Dev& d, const Work& w, const int32_t* idx, int64
     k_fwd_gather<D, BITS, SB16><<<(unsigned)blocks, 256, 0, s>>>(d, w.fwd_src, L, off, B, out);
     return hipGetLastError();
   });
+}
+
+// ---- forward without a workspace ---------------------------------------------------------
+// For callers that cannot allocate: the forward's per-call temporaries (the counter words
+// written by the offset check, then one code per lookup) live in `scratch`, a static
+// device array that every GPU the library runs on holds until the process ends.  Host
+// code never passes the array's name to a kernel (on the host it is only a stand-in): it
+// passes the device address that hipGetSymbolAddress returns for the current device,
+// looked up once per device.
+constexpr size_t kNoAllocHeader = 256;
+static_assert(EMB_NOALLOC_MAX_INDICES == (EMB_NOALLOC_SCRATCH_BYTES - kNoAllocHeader) / 4, "scratch layout");
+static_assert(kNCounters * sizeof(unsigned long long) <= kNoAllocHeader, "counter words");
+static __device__ __align__(256) uint8_t scratch[EMB_NOALLOC_SCRATCH_BYTES];
+
+hipError_t noalloc_scratch(uint8_t** out) {
+  static std::mutex mu;
+  static std::map<int, uint8_t*> addr;  // device -> address of its copy of `scratch`
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lock(mu);
+  const auto it = addr.find(dev);
+  if (it != addr.end()) {
+    *out = it->second;
+    return hipSuccess;
+  }
+  void* p = nullptr;
+  e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+  if (e != hipSuccess || p == nullptr) return e != hipSuccess ? e : hipErrorInvalidSymbol;
+  addr[dev] = static_cast<uint8_t*>(p);
+  *out = static_cast<uint8_t*>(p);
+  return hipSuccess;
+}
+
+hipError_t launch_forward_noalloc(const Dev& d, uint8_t* scratch_dev, const int32_t* idx, int64_t L,
+                                  const int32_t* off, int32_t B, float* out, hipStream_t s) {
+  if (scratch_dev == nullptr || L < 0 || L > EMB_NOALLOC_MAX_INDICES) return hipErrorInvalidValue;
+  // the same kernels as launch_forward; nothing in the scratch is read before it is written
+  // in the same call (the counter words are only written), so it needs no clearing
+  Work w{};
+  w.ctr = reinterpret_cast<unsigned long long*>(scratch_dev);
+  w.fwd_src = reinterpret_cast<int32_t*>(scratch_dev + kNoAllocHeader);
+  w.max_indices = EMB_NOALLOC_MAX_INDICES;
+  return launch_forward(d, w, idx, L, off, B, out, s);
 }
 
 }  // namespace embc

@@ -229,6 +229,7 @@ struct emb_cache {
   std::vector<hipEvent_t> tev;
   uint64_t timed = 0;
   embc::SideStream side;  // default priority, non-blocking; events without timing
+  uint8_t* noalloc = nullptr;  // device address of the static scratch of emb_cache_forward_noalloc
   ~emb_cache() {
     for (hipEvent_t e : tev) (void)hipEventDestroy(e);
     if (side.fork) (void)hipEventDestroy(side.fork);
@@ -445,6 +446,7 @@ int create_impl(const emb_cache_config* cfg, void* state, size_t state_bytes, vo
   if (e == hipSuccess) e = hipStreamCreateWithFlags(&h->side.s, hipStreamNonBlocking);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&h->side.fork, hipEventDisableTiming);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&h->side.join, hipEventDisableTiming);
+  if (e == hipSuccess) e = embc::noalloc_scratch(&h->noalloc);  // once per device, this device current
   if (e == hipSuccess) e = embc::launch_reset_state(d, s);
   if (e == hipSuccess) e = hipStreamSynchronize(s);
   if (e != hipSuccess) {
@@ -474,6 +476,16 @@ int emb_cache_forward(emb_cache_t h, const int32_t* indices, int64_t num_indices
     return EMB_EINVAL;
   if ((num_indices > 0 && !indices) || !offsets || (batch > 0 && !out)) return EMB_EINVAL;
   return hip_status(embc::launch_forward(h->dev, h->work, indices, num_indices, offsets, batch, out, S(stream)));
+}
+
+int emb_cache_forward_noalloc(emb_cache_t h, const int32_t* indices, int64_t num_indices, const int32_t* offsets,
+                              int32_t batch, float* out, void* stream) {
+  if (!h || batch < 0 || batch > h->cfg.max_batch || num_indices < 0) return EMB_EINVAL;
+  if ((num_indices > 0 && !indices) || !offsets || (batch > 0 && !out)) return EMB_EINVAL;
+  if (num_indices > EMB_NOALLOC_MAX_INDICES) return EMB_ENOMEM;  // beyond the static scratch
+  if (!h->noalloc) return EMB_EHIP;
+  return hip_status(
+      embc::launch_forward_noalloc(h->dev, h->noalloc, indices, num_indices, offsets, batch, out, S(stream)));
 }
 
 int emb_cache_backward_update(emb_cache_t h, const int32_t* indices, int64_t num_indices, const int32_t* offsets,

@@ -84,6 +84,7 @@ def load():
         "emb_cache_destroy": [P],
         "emb_cache_init_uniform": [P, f32, f32, u64, P],
         "emb_cache_forward": [P, P, i64, P, i32, P, P],
+        "emb_cache_forward_noalloc": [P, P, i64, P, i32, P, P],
         "emb_cache_backward_update": [P, P, i64, P, i32, P, P],
         "emb_cache_get_stats": [P, i32, P, P],
         "emb_cache_check": [P, P],
@@ -246,6 +247,16 @@ class EmbCache:
             out = torch.empty((batch, self.T, self.dim), dtype=torch.float32, device=self.device)
         assert out.shape == (batch, self.T, self.dim) and out.is_contiguous() and out.dtype == torch.float32
         _check(load().emb_cache_forward(self._h, ip, n, op, int(batch), _dptr(out), self._stream()), "forward")
+        return out
+
+    def forward_noalloc(self, indices, offsets, batch, out):
+        """emb_cache_forward_noalloc: the forward with the library's static scratch in place
+        of the workspace; `out` is the caller's (nothing is allocated here either)."""
+        torch = self.torch
+        ip, n, op = self._inputs(indices, offsets, batch)
+        assert out.shape == (batch, self.T, self.dim) and out.is_contiguous() and out.dtype == torch.float32
+        _check(load().emb_cache_forward_noalloc(self._h, ip, n, op, int(batch), _dptr(out), self._stream()),
+               "forward_noalloc")
         return out
 
     def backward_update(self, indices, offsets, batch, grad_out):
