@@ -88,11 +88,15 @@ hipError_t launch_init_uniform(const Dev& d, float lo, float hi, uint64_t init_s
 // valid lookup gives +0.
 constexpr int kFwdUnroll = 2;
 
-constexpr int kProbeUnroll = 4;  // lookups in flight per lane group of the probe
+#ifndef EMBC_PROBE_PU
+#define EMBC_PROBE_PU 4
+#endif
+constexpr int kProbeUnroll = EMBC_PROBE_PU;  // lookups in flight per lane group of the probe
 
-// QL = min(assoc, 4) lanes share one lookup, each comparing W = assoc/QL of the set's
-// tags, so a wave-wide tag load touches 64/QL sets instead of 64; every lane group
-// keeps kProbeUnroll lookups in flight (all index loads, then all tag loads).
+// QL = assoc/W lanes share one lookup (one lane up to 16 ways, W = min(assoc, 16)), each
+// comparing W of the set's tags loaded 16 bytes at a time; every lane group keeps
+// kProbeUnroll lookups in flight (all index loads, then all tag loads).  One lane per
+// lookup pays the set index, the addressing and the store of a lookup once.
 template <int W>
 __global__ __launch_bounds__(256) void k_fwd_probe(Dev dv, const int32_t* __restrict__ idx, int64_t L,
                                                    const int32_t* __restrict__ off, int32_t B,
@@ -108,7 +112,7 @@ __global__ __launch_bounds__(256) void k_fwd_probe(Dev dv, const int32_t* __rest
     for (int64_t p = last + threadIdx.x; p < L; p += blockDim.x) src[p] = -1;
   }
   const int A = dv.assoc;
-  const int QL = A / W;  // 1, 2 or 4
+  const int QL = A / W;  // 1 up to 16 ways, 2 or 4 for 32 or 64
   const int sub = threadIdx.x % QL;
   const int64_t ptid = tid / QL, pstride = stride / QL;
   for (int seg = xs.xcd; seg < xs.segments(dv.T); seg += kXcds) {
@@ -315,7 +319,7 @@ hipError_t launch_forward(const Dev& d, const Work& w, const int32_t* idx, int64
     const auto probe = [&](auto kernel) {
       kernel<<<resident_grid(reinterpret_cast<const void*>(kernel)), 256, 0, s>>>(d, idx, L, off, B, w.fwd_src);
     };
-    switch (d.assoc <= 4 ? 1 : d.assoc / 4) {
+    switch (d.assoc < 16 ? d.assoc : 16) {
       case 1: probe(k_fwd_probe<1>); break;
       case 2: probe(k_fwd_probe<2>); break;
       case 4: probe(k_fwd_probe<4>); break;

@@ -201,12 +201,17 @@ def test_kaggle_int8_full_size(torch):
 
 
 def test_kaggle_int4_full_size(torch):
+    """12 steps (across the LFU decay at step 10); LFU displaces residents right after
+    their own update here (hit evictions), which the state comparison covers."""
     cfg = configs.get("kaggle_int4")
     log("kaggle_int4 full size: oracle init (33.7M rows) ...")
     o, g = make_pair(cfg)
+    hit_evictions = 0
     for k in range(12):   # crosses the LFU decay at step 10
         step_both(o, g, cfg, workload.make_step(cfg, k), torch)
-    log("kaggle_int4: comparing state")
+        hit_evictions += sum(g.stats(t)["hit_evictions"] for t in range(len(cfg["rows"])))
+    log(f"kaggle_int4: comparing state ({hit_evictions} hit evictions)")
+    assert hit_evictions > 0
     compare_state(o, g, cfg)
 
 
