@@ -194,11 +194,16 @@ def _oracle_table_run(cfg, t, steps, budget_s, out, slot):
     out[slot] = (lookups, elapsed, done)
 
 
-def cpu_baseline(cfg, steps, budget_s, threads):
+def cpu_baseline(cfg, steps, budget_s, threads, max_rows=0):
     """The CPU oracle, threads over tables (tables are independent): thread i runs table
-    i alone; the rate is the sum of lookups over the slowest thread's oracle time."""
+    i alone; the rate is the sum of lookups over the slowest thread's oracle time.  With
+    max_rows, each table is cut to that many rows (a row-scaled slice of the same batch
+    shape, for tables too large for the host's memory or time)."""
     import threading
 
+    full = cfg
+    if max_rows:
+        cfg = dict(cfg, rows=[min(int(r), int(max_rows)) for r in cfg["rows"]])
     T = len(cfg["rows"])
     n = max(1, min(threads, T))
     res = [None] * n
@@ -211,7 +216,8 @@ def cpu_baseline(cfg, steps, budget_s, threads):
     wall = max(r[1] for r in res)
     one = res[0][0] / res[0][1]
     desc = host_description()
-    sample = (f"tables 0..{n - 1} of {T} ({cfg['rows'][0]} rows each), one oracle instance and one thread per "
+    sliced = f" (row-scaled slice: {cfg['rows'][0]} of {full['rows'][0]} rows)" if cfg["rows"] != full["rows"] else ""
+    sample = (f"tables 0..{n - 1} of {T} ({cfg['rows'][0]} rows each{sliced}), one oracle instance and one thread per "
               f"table, {min(r[2] for r in res)}-{max(r[2] for r in res)} steps of fwd+bwd+update each, "
               f"{lookups} lookups; the rate is per lookup of this {n}-table slice (tables are independent, so the "
               f"whole workload runs at the same rate per lookup); host: {desc['nproc']} usable cores, "
@@ -285,6 +291,7 @@ def main():
     ap.add_argument("--cpu-steps", type=int, default=60)
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="oracle seconds per thread")
     ap.add_argument("--cpu-threads", type=int, default=0, help="oracle threads (0: usable host cores, at most 16)")
+    ap.add_argument("--cpu-rows", type=int, default=0, help="cut each table to this many rows for the oracle")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-copy-bw", action="store_true")
     ap.add_argument("--calibration", action="store_true",
@@ -454,7 +461,7 @@ def main():
         torch.cuda.empty_cache()
         threads = args.cpu_threads or min(16, host_description()["nproc"] or 1)
         print(f"[bench] CPU oracle baseline, {threads} threads ...", file=sys.stderr, flush=True)
-        result["cpu_baseline"] = cpu_baseline(cfg, args.cpu_steps, args.cpu_budget, threads)
+        result["cpu_baseline"] = cpu_baseline(cfg, args.cpu_steps, args.cpu_budget, threads, args.cpu_rows)
     print(json.dumps(result), flush=True)
 
 

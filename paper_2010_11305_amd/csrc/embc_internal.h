@@ -122,6 +122,7 @@ struct Work {
   int32_t* uvic_row;     // [L] insert: table-local row displaced from its way, -1 = empty way
   int32_t* uvic_u;       // [L] insert: unique index of that row if it was updated this step, else -1
   uint4* umeta;          // [L] per unique row, the inputs of the row update in one word (k_pack_meta)
+  unsigned long long* ukey;  // [L] LFU: a missed row's rank key (count << 32 | ~row), 0 for a hit
   float* partial;        // [L/32 + 2][dim] chunk sums
   uint2* chunk_span;     // [L/32 + 2] occurrences [x, y) of the sorted stream summed by each chunk
   uint32_t* ubig;        // [L] 1 for a row with more than kBlockAbove lookups, then its exclusive prefix

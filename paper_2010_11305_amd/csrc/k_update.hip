@@ -107,7 +107,10 @@ __global__ __launch_bounds__(256) void k_probe(Dev dv, Work w, uint32_t step) {
         if (slot >= 0) dv.ts[slot] = (int32_t)step;
       } else {
         const int64_t c = (int64_t)dv.cnt[grow] + count;
-        dv.cnt[grow] = c > 0x7FFFFFFF ? 0x7FFFFFFF : (int32_t)c;
+        const int32_t cn = c > 0x7FFFFFFF ? 0x7FFFFFFF : (int32_t)c;
+        dv.cnt[grow] = cn;
+        // a missed row's rank among the candidates of its set: count, then lower row first
+        w.ukey[u] = slot >= 0 ? 0ull : ((unsigned long long)(uint32_t)cn << 32) | (uint32_t)~(uint32_t)grow;
       }
     }
     wave_stat_add(dv.stats, t, kStUnique, 1u, act);
@@ -715,7 +718,7 @@ __global__ __launch_bounds__(256) void k_policy(Dev dv, Work w, uint32_t step) {
         L.vic_pv[gb + vr] = vpv;
       }
       // candidates ranked by (priority desc, row asc); only ranks < A matter
-      const int64_t K = M < A ? M : A;
+      int64_t K = M < A ? M : A;
       if (lru) {
         int64_t seen = 0;
         for (int64_t c = u0; c < u1 && seen < K; c += G) {
@@ -730,30 +733,41 @@ __global__ __launch_bounds__(256) void k_policy(Dev dv, Work w, uint32_t step) {
           seen += __popcll(m);
         }
       } else {
-        for (int64_t c = u0; c < u1; c += G) {
-          const int64_t u = c + l;
-          const bool miss = u < u1 && w.uslot[u] < 0;
-          const long long mypv = miss ? (long long)dv.cnt[w.urow[u]] : 0;
-          const int32_t myrow = u < u1 ? w.urow[u] : 0;
-          int64_t rank = 0;
-          for (int64_t c2 = u0; c2 < u1; c2 += G) {
-            const int64_t u2 = c2 + l;
-            const bool miss2 = u2 < u1 && w.uslot[u2] < 0;
-            const long long pv2 = miss2 ? (long long)dv.cnt[w.urow[u2]] : 0;
-            const int32_t row2 = u2 < u1 ? w.urow[u2] : 0;
-#pragma unroll 4
-            for (int j = 0; j < G; ++j) {
-              const long long pj = __shfl(pv2, gb + j);
-              const int32_t rj = __shfl(row2, gb + j);
-              const int mj = __shfl((int)miss2, gb + j);
-              if (mj && (pj > mypv || (pj == mypv && rj < myrow))) ++rank;
+        // the candidates in rank order, found one at a time as the largest key below the
+        // previous one (keys are unique: they hold the row), for as long as the k-th
+        // candidate beats the k-th victim; the first that does not ends the inserts
+        __builtin_amdgcn_wave_barrier();
+        unsigned long long prev = ~0ull;
+        int64_t taken = 0;
+        for (int64_t r = 0; r < K; ++r) {
+          unsigned long long best = 0;
+          int32_t bu = -1;
+          for (int64_t c = u0 + l; c < u1; c += G) {
+            const unsigned long long k = w.ukey[c];
+            if (k < prev && k > best) {
+              best = k;
+              bu = (int32_t)c;
             }
           }
-          if (miss && rank < K) {
-            L.cand_u[gb + rank] = (int32_t)u;
-            L.cand_pv[gb + rank] = mypv;
+#pragma unroll
+          for (int o = G / 2; o >= 1; o >>= 1) {
+            const unsigned long long ob = __shfl_xor(best, o, G);
+            const int32_t ou = __shfl_xor(bu, o, G);
+            if (ob > best) {
+              best = ob;
+              bu = ou;
+            }
           }
+          const long long cpv = (long long)(best >> 32);
+          if (best == 0 || !(cpv > L.vic_pv[gb + r])) break;
+          if (l == 0) {
+            L.cand_u[gb + r] = bu;
+            L.cand_pv[gb + r] = cpv;
+          }
+          prev = best;
+          taken = r + 1;
         }
+        K = taken;  // every listed candidate beats its victim
       }
       __builtin_amdgcn_wave_barrier();
       // the k-th candidate takes the k-th victim while strictly higher; stop at the first failure

@@ -83,7 +83,7 @@ struct Plan {
   size_t o_rec, o_crow, o_tag, o_ts, o_cnt, o_G, o_desc, o_keyb, o_stats, o_err, state_bytes, table_bytes;
   // workspace offsets
   size_t o_kA, o_vA, o_kB, o_vB, o_ssmall, o_sst0, o_sst1, o_sseg, o_part, o_tcnt, o_tpre, o_tthr, o_uk, o_seg, o_setf, o_urow, o_utab, o_uslot,
-      o_uact, o_udest, o_umeta, o_nch, o_cbase, o_uvrow, o_uvu, o_partial, o_span, o_ubig, o_brows, o_bbound, o_bpart, o_tabf, o_src, o_ctr, ws_bytes;
+      o_uact, o_udest, o_umeta, o_ukey, o_nch, o_cbase, o_uvrow, o_uvu, o_partial, o_span, o_ubig, o_brows, o_bbound, o_bpart, o_tabf, o_src, o_ctr, ws_bytes;
   int64_t max_partials = 0;
   int64_t max_big = 0;
   int32_t max_nblk = 0;
@@ -189,6 +189,7 @@ int plan_config(const emb_cache_config* c, Plan* p) {
   p->o_uact = take(4 * L);
   p->o_udest = take(4 * L);
   p->o_umeta = take(16 * L);
+  p->o_ukey = take(c->policy == EMB_LFU ? 8 * L : 0);
   p->o_nch = take(4 * L);
   p->o_cbase = take(4 * (L + 1));
   p->o_uvrow = take(4 * L);
@@ -419,6 +420,7 @@ int create_impl(const emb_cache_config* cfg, void* state, size_t state_bytes, vo
   w.uact = reinterpret_cast<int32_t*>(wb + p.o_uact);
   w.udest = reinterpret_cast<int32_t*>(wb + p.o_udest);
   w.umeta = reinterpret_cast<uint4*>(wb + p.o_umeta);
+  w.ukey = reinterpret_cast<unsigned long long*>(wb + p.o_ukey);
   w.nch = reinterpret_cast<uint32_t*>(wb + p.o_nch);
   w.chunk_base = reinterpret_cast<uint32_t*>(wb + p.o_cbase);
   w.uvic_row = reinterpret_cast<int32_t*>(wb + p.o_uvrow);
