@@ -362,26 +362,44 @@ __device__ __forceinline__ int table_of_key(const int64_t* key_base, int T, uint
   return lo;
 }
 
-// Global slot of table-local row r if resident, else -1 (the set's tags are
-// compared with int4 loads when assoc is a multiple of 4).
+// Global slot of table-local row r if resident, else -1.  All of the set's tags are
+// loaded before any is compared (16 bytes at a time when assoc is a multiple of 4), so a
+// probe waits for one round of loads rather than one per 16 bytes.
+template <int A>
+__device__ __forceinline__ int32_t probe_set(const int32_t* __restrict__ tg, int32_t r) {
+  int32_t v[A];
+  if constexpr (A % 4 == 0) {
+#pragma unroll
+    for (int w = 0; w < A; w += 4) {
+      const int4 q = *reinterpret_cast<const int4*>(tg + w);
+      v[w] = q.x; v[w + 1] = q.y; v[w + 2] = q.z; v[w + 3] = q.w;
+    }
+  } else {
+#pragma unroll
+    for (int w = 0; w < A; ++w) v[w] = tg[w];
+  }
+  int32_t found = -1;
+#pragma unroll
+  for (int w = 0; w < A; ++w) found = v[w] == r ? w : found;
+  return found;
+}
+
 __device__ __forceinline__ int32_t probe_slot(const Dev& dv, const TableDesc& td, int32_t r) {
   if (td.n_sets == 0) return -1;
   const int64_t set = (int64_t)mod_by((uint32_t)r, td.by_sets);
   const int64_t base = td.slot_base + set * dv.assoc;
   const int32_t* tg = dv.tag + base;
-  if ((dv.assoc & 3) == 0) {
-    for (int w = 0; w < dv.assoc; w += 4) {
-      const int4 v = *reinterpret_cast<const int4*>(tg + w);
-      if (v.x == r) return (int32_t)(base + w);
-      if (v.y == r) return (int32_t)(base + w + 1);
-      if (v.z == r) return (int32_t)(base + w + 2);
-      if (v.w == r) return (int32_t)(base + w + 3);
-    }
-  } else {
-    for (int w = 0; w < dv.assoc; ++w)
-      if (tg[w] == r) return (int32_t)(base + w);
+  int32_t w = -1;
+  switch (dv.assoc) {
+    case 1: w = probe_set<1>(tg, r); break;
+    case 2: w = probe_set<2>(tg, r); break;
+    case 4: w = probe_set<4>(tg, r); break;
+    case 8: w = probe_set<8>(tg, r); break;
+    case 16: w = probe_set<16>(tg, r); break;
+    case 32: w = probe_set<32>(tg, r); break;
+    default: w = probe_set<64>(tg, r); break;
   }
-  return -1;
+  return w >= 0 ? (int32_t)(base + w) : -1;
 }
 
 // XCD-aware work split.  Workgroups are dispatched round-robin over the 8 XCDs

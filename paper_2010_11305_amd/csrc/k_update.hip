@@ -25,23 +25,6 @@ constexpr int32_t kActDone = 4;  // row fully handled by k_policy
 
 constexpr int kUnroll = 2;  // independent row loads in flight per row group
 
-// Per-table counts of the active lanes (tables may differ across lanes): one atomic
-// for the lanes sharing the first active lane's table, one per lane for the others.
-// Must be called by all 64 lanes.
-__device__ __forceinline__ void wave_stat_add(unsigned long long* stats, int t, int field, uint32_t v, bool active) {
-  const uint64_t act = __ballot(active && v != 0);
-  if (!act) return;
-  const int leader = __ffsll((unsigned long long)act) - 1;
-  const int t0 = __shfl(t, leader);
-  const bool same = active && t == t0;
-  uint32_t s = same ? v : 0u;
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o);
-  const int lane = threadIdx.x & 63;
-  if (lane == leader && s) atomicAdd(&stats[(int64_t)t0 * kNStat + field], (unsigned long long)s);
-  if (active && !same && v) atomicAdd(&stats[(int64_t)t * kNStat + field], (unsigned long long)v);
-}
-
 // After the paired scan of the chunk counts and big-row flags: the chunk total, and the
 // big-row total, also as ubig[nU].
 __global__ void k_scan_totals(Work w) {
@@ -81,7 +64,6 @@ __global__ __launch_bounds__(256) void k_probe(Dev dv, Work w, uint32_t step) {
     const bool act = u < nU;
     int t = 0;
     int32_t slot = -1;
-    bool nocache = false;
     if (act) {
       const uint32_t key = w.uniq_key[u];
       t = w.utab[u];  // written with the key by k_uniq_write
@@ -92,7 +74,6 @@ __global__ __launch_bounds__(256) void k_probe(Dev dv, Work w, uint32_t step) {
         const uint32_t sq = div_by((uint32_t)local, td.by_Q);  // local = set * Q + q
         r = (int64_t)((uint32_t)local - sq * (uint32_t)td.Q) * td.n_sets + sq;
       }
-      nocache = td.n_sets == 0;
       const int64_t grow = td.row_base + r;
       const uint32_t count = w.seg[u + 1] - w.seg[u];
       slot = probe_slot(dv, td, (int32_t)r);
@@ -113,9 +94,6 @@ __global__ __launch_bounds__(256) void k_probe(Dev dv, Work w, uint32_t step) {
         w.ukey[u] = slot >= 0 ? 0ull : ((unsigned long long)(uint32_t)cn << 32) | (uint32_t)~(uint32_t)grow;
       }
     }
-    wave_stat_add(dv.stats, t, kStUnique, 1u, act);
-    wave_stat_add(dv.stats, t, kStUniqueHits, slot >= 0 ? 1u : 0u, act);
-    wave_stat_add(dv.stats, t, kStBypasses, nocache ? 1u : 0u, act);
   }
 }
 
@@ -504,15 +482,29 @@ __device__ __forceinline__ void table_rows(const Work& w, int t, int64_t& lo, in
 }
 
 // tab_first[t] = first unique row of table t (>= t), tab_first[T] = number of unique rows.
-__global__ void k_tab_first(Work w, int T) {
+// Also the statistics that follow from those ranges: the unique rows of each table, and,
+// for a table without a cache, its bypasses (every row).  (Unique hits are counted by
+// k_policy, inserts and the other bypasses too.)
+__device__ __forceinline__ int64_t first_row_of_table(const Work& w, int64_t nU, int t) {
+  int64_t a = 0, b = nU;
+  while (a < b) {
+    const int64_t m = (a + b) >> 1;
+    if (w.utab[m] < t) a = m + 1; else b = m;
+  }
+  return a;
+}
+
+__global__ void k_tab_first(Dev dv, Work w, int T) {
   const int64_t nU = (int64_t)w.ctr[kCUnique];
   for (int t = blockIdx.x * blockDim.x + threadIdx.x; t <= T; t += gridDim.x * blockDim.x) {
-    int64_t a = 0, b = nU;
-    while (a < b) {
-      const int64_t m = (a + b) >> 1;
-      if (w.utab[m] < t) a = m + 1; else b = m;
+    const int64_t lo = first_row_of_table(w, nU, t);
+    w.tab_first[t] = (int32_t)lo;
+    if (t < T) {
+      const int64_t n = first_row_of_table(w, nU, t + 1) - lo;
+      unsigned long long* st = dv.stats + (int64_t)t * kNStat;
+      st[kStUnique] = (unsigned long long)n;
+      if (dv.desc[t].n_sets == 0) st[kStBypasses] = (unsigned long long)n;
     }
-    w.tab_first[t] = (int32_t)a;
   }
 }
 
@@ -616,16 +608,17 @@ struct PolicyLds {
 // Statistics of the sets a wave handles, accumulated while the table does not change.
 struct PolicyStats {
   int t = -1;
-  uint32_t ins = 0, byp = 0, ev = 0, em = 0, he = 0;
+  uint32_t ins = 0, byp = 0, ev = 0, em = 0, he = 0, hits = 0;
   __device__ void flush(unsigned long long* stats) {
     if (t < 0) return;
     unsigned long long* s = stats + (int64_t)t * kNStat;
+    if (hits) atomicAdd(s + kStUniqueHits, (unsigned long long)hits);
     if (ins) atomicAdd(s + kStInserts, (unsigned long long)ins);
     if (byp) atomicAdd(s + kStBypasses, (unsigned long long)byp);
     if (ev) atomicAdd(s + kStEvictions, (unsigned long long)ev);
     if (em) atomicAdd(s + kStEmptyFills, (unsigned long long)em);
     if (he) atomicAdd(s + kStHitEvictions, (unsigned long long)he);
-    ins = byp = ev = em = he = 0;
+    ins = byp = ev = em = he = hits = 0;
   }
 };
 
@@ -659,26 +652,32 @@ __global__ __launch_bounds__(256) void k_policy(Dev dv, Work w, uint32_t step) {
     const int64_t r0 = (int64_t)w.urow[u0] - td.row_base;
     const int64_t sbase = td.slot_base + (r0 % td.n_sets) * A;
 
-    // residents that hit this step, and the number of missed rows
-    L.hitu[lane] = -1;
-    __builtin_amdgcn_wave_barrier();
-    int64_t M = 0;
-    for (int64_t c = u0; c < u1; c += G) {
-      const int64_t u = c + l;
-      bool miss = false;
-      if (u < u1) {
-        const int32_t sl = w.uslot[u];
-        if (sl >= 0) L.hitu[gb + (sl - sbase)] = (int32_t)u;
-        else miss = true;
-      }
-      M += __popcll(__ballot(miss) & gmask);
-    }
-    __builtin_amdgcn_wave_barrier();
-    if (M == 0) continue;
     if (t != ps.t) {
       if (l == 0) ps.flush(dv.stats);
       ps.t = t;
     }
+    // residents that hit this step, and the number of missed rows
+    L.hitu[lane] = -1;
+    __builtin_amdgcn_wave_barrier();
+    int64_t M = 0, H = 0;
+    for (int64_t c = u0; c < u1; c += G) {
+      const int64_t u = c + l;
+      bool miss = false, hit = false;
+      if (u < u1) {
+        const int32_t sl = w.uslot[u];
+        if (sl >= 0) {
+          L.hitu[gb + (sl - sbase)] = (int32_t)u;
+          hit = true;
+        } else {
+          miss = true;
+        }
+      }
+      M += __popcll(__ballot(miss) & gmask);
+      H += __popcll(__ballot(hit) & gmask);
+    }
+    __builtin_amdgcn_wave_barrier();
+    if (l == 0) ps.hits += (uint32_t)H;
+    if (M == 0) continue;
 
     // ways, their tags and priorities (empty = lowest)
     int32_t tg = -1;
@@ -995,7 +994,7 @@ hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int6
   if (e != hipSuccess) return e;
   const auto grid = [](auto kernel) { return resident_grid(reinterpret_cast<const void*>(kernel)); };
   k_probe<<<grid(k_probe), 256, 0, s>>>(d, w, step);
-  k_tab_first<<<1, 256, 0, s>>>(w, d.T);
+  k_tab_first<<<(d.T + 256) / 256, 256, 0, s>>>(d, w, d.T);
   e = scan_exclusive_pair(w.nch, w.ubig, w.chunk_base, w.ubig, L, w.ctr + kCUnique, w.part, w.ctr + kCScanTotal, s);
   if (e != hipSuccess) return e;
   k_scan_totals<<<1, 1, 0, s>>>(w);
