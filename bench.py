@@ -42,9 +42,10 @@ def update_kernel_digest():
 
 
 def measured_update_traffic():
-    """HBM bytes per k_update launch from the committed counter summary (FETCH_SIZE x 2 +
-    WRITE_SIZE x 1, see that file's calibration), or None when the summary was taken on
-    other kernel sources."""
+    """HBM bytes per k_update launch from the committed counter summary (reads from the L2's
+    requests to the memory fabric by size, writes from WRITE_SIZE; that file gives the
+    commands and the calibration), or None when the summary was taken on other kernel
+    sources."""
     try:
         text = open(COUNTERS_FILE).read()
     except OSError:
@@ -248,7 +249,7 @@ def copy_bandwidth(dev, mib=4096, reps=5):
 
 
 def calibration_kernels(dev):
-    """Kernels of known HBM traffic for the FETCH_SIZE / WRITE_SIZE counters: a 2 GiB copy,
+    """Kernels of known HBM traffic for the read-request and WRITE_SIZE counters: a 2 GiB copy,
     a 2 GiB streaming read (sum), and gathers of 1 GiB of random 512-byte rows and of
     random 64-byte rows out of 8 GiB tables (far beyond the 256 MB last-level cache)."""
     import torch
@@ -295,7 +296,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-copy-bw", action="store_true")
     ap.add_argument("--calibration", action="store_true",
-                    help="first run kernels of known HBM traffic (for the FETCH_SIZE / WRITE_SIZE counters)")
+                    help="first run kernels of known HBM traffic (for the HBM read and write counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the multi-GPU path is not built.",

@@ -79,8 +79,8 @@ hipError_t launch_init_uniform(const Dev& d, float lo, float hi, uint64_t init_s
 }
 
 // ---- forward --------------------------------------------------------------------------
-// Two passes.  k_fwd_probe: up to 4 lanes per lookup (tables split over the XCDs) check
-// the row, probe its set, and write a code: the cache slot (hit), -2-row (miss) or
+// Two passes.  k_fwd_probe: one lane per lookup up to 16 ways, 2 or 4 lanes for 32 or 64
+// (tables split over the XCDs), checks the row, probes its set, and write a code: the cache slot (hit), -2-row (miss) or
 // -1 (skipped).  k_fwd_gather: one group of LPR
 // lanes per bag (64/LPR bags per wave), tables split over the XCDs; lane j reads the
 // code of position j of each chunk of LPR positions, the rows are fetched FU at a time
