@@ -37,10 +37,29 @@ struct SegSort {
 hipError_t sort_pairs(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32_t* vB, int64_t n, int passes,
                       const SortScratch& ss, int32_t* err, int* in_B, hipStream_t s);
 
+// The counting of the per-table sort mode, when the expansion does it (launch_expand
+// with an ExpandHist from seg_begin): per-table digit counts, skipped keys, and the
+// first pass's status words.
+struct ExpandHist {
+  uint32_t* hist = nullptr;            // SegSort::hist
+  const int64_t* key_base = nullptr;   // [T+1]
+  uint32_t* n_skipped = nullptr;       // zeroed by seg_begin
+  uint32_t* status = nullptr;          // status words of the first pass
+  int64_t status_words = 0;
+  int passes = 0;
+};
+
+// Clears the counts and writes the segment starts for n > 0 keys (the same checks as
+// sort_pairs_segmented), and fills *eh for the expansion.
+hipError_t seg_begin(int64_t n, int passes, const int32_t* off, int32_t B, int T, const int64_t* key_base,
+                     const unsigned long long* ctr, const SortScratch& ss, const SegSort& sg, ExpandHist* eh,
+                     hipStream_t s);
+
 // The same order from `passes` (< kMaxPasses) digit passes over each table's segment
 // of the stream (lookups of table t at [off[t*B], off[(t+1)*B])), sorted by the local
 // key; every table's key range must be below 2^(8*passes).  One more pass and a copy
-// run only when some key is kKeyInvalid.
+// run only when some key is kKeyInvalid.  The counting is done before: seg_begin, then
+// launch_expand with its ExpandHist.
 hipError_t sort_pairs_segmented(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32_t* vB, int64_t n, int passes,
                                 const int32_t* off, int32_t B, int T, const int64_t* key_base,
                                 const unsigned long long* ctr, const SortScratch& ss, const SegSort& sg, int32_t* err,
@@ -52,9 +71,10 @@ __global__ void k_check_offsets(Dev dv, const int32_t* __restrict__ off, int64_t
                                 unsigned long long* __restrict__ ctr);
 
 // Lookups -> (set-major key, bag) pairs; every key is skipped when ctr[kCBadOffsets]
-// is set (k_check_offsets must have run first on the same stream).
+// is set (k_check_offsets must have run first on the same stream).  eh: nullptr, or the
+// per-table counting to do on the way (seg_begin first).
 hipError_t launch_expand(const Dev& dv, const int32_t* idx, int64_t L, const int32_t* off, int32_t B, uint32_t* keys,
-                         uint32_t* vals, unsigned long long* ctr, hipStream_t s);
+                         uint32_t* vals, unsigned long long* ctr, const ExpandHist* eh, hipStream_t s);
 
 // Unique rows of the sorted stream sk[0, n): their keys, first occurrences and tables, and
 // the first unique row of each touched set (tile_cnt / tile_pre: uniq_tile_words(n) words each).

@@ -224,7 +224,9 @@ __device__ __forceinline__ uint64_t match_digit(uint32_t d, bool valid) {
 // table's key base) gives the global order in fewer passes when every table's key
 // range is far smaller than the sum of them (100 tables of 5M rows: 3 passes instead
 // of 4).  Tiles never straddle a segment (each segment starts a new tile), a look-back
-// ends at the segment's first tile, and digit runs start at P_t.  A skipped lookup
+// ends at the segment's first tile, and digit runs start at P_t.  The per-table digit
+// counts are taken by the expansion (k_expand) as it forms the keys, so this mode has
+// no histogram pass of its own.  A skipped lookup
 // (kKeyInvalid) takes digit 255 in every pass, above every valid local key, so it ends
 // its table's segment; when there is any, one more stable pass (digit 1 for a skipped
 // key, 0 for the others) moves them behind every valid key, and the pairs are copied
@@ -344,66 +346,6 @@ __global__ __launch_bounds__(256) void k_seg_setup(const int32_t* __restrict__ o
   }
   const int64_t hw = (int64_t)T * kMaxPasses * 256;
   for (int64_t i = threadIdx.x; i < hw; i += 256) sg.hist[i] = 0;
-}
-
-// Per-table histograms of the local-key digits of every segmented pass, and the number
-// of skipped keys (n_skipped[0], for the pass that moves them last), in one read of the
-// keys; each block takes kSegHistTiles consecutive tiles and adds its counts when the
-// table changes.  Also clears the status words of the first pass.
-constexpr int kSegHistTiles = 8;
-
-__global__ __launch_bounds__(256) void k_seg_hist(const uint32_t* __restrict__ keys, int64_t n, int passes,
-                                                  const int64_t* __restrict__ key_base, int T, SegSort sg,
-                                                  uint32_t* __restrict__ n_skipped, uint32_t* __restrict__ status,
-                                                  int64_t status_words) {
-  __shared__ uint32_t h[kRadixWaves][kMaxPasses][256];
-  __shared__ uint32_t skipped_s;
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  for (int i = threadIdx.x; i < kRadixWaves * kMaxPasses * 256; i += 256) (&h[0][0][0])[i] = 0;
-  if (threadIdx.x == 0) skipped_s = 0;
-  __syncthreads();
-  const uint32_t ntiles = sg.tbase[T];
-  int cur = -1;  // table whose counts the LDS holds
-  const auto flush = [&](int t) {
-    __syncthreads();
-    for (int p = 0; p < passes; ++p) {
-      uint32_t c = 0;
-#pragma unroll
-      for (int w = 0; w < kRadixWaves; ++w) {
-        c += h[w][p][threadIdx.x];
-        h[w][p][threadIdx.x] = 0;
-      }
-      if (c) atomicAdd(&sg.hist[((int64_t)t * kMaxPasses + p) * 256 + threadIdx.x], c);
-    }
-    __syncthreads();
-  };
-  for (uint32_t tile = blockIdx.x * kSegHistTiles; tile < min<uint32_t>(ntiles, (blockIdx.x + 1) * kSegHistTiles);
-       ++tile) {
-    const int t = seg_of_tile(sg.tbase, T, tile);
-    if (t != cur) {
-      if (cur >= 0) flush(cur);
-      cur = t;
-    }
-    const int64_t lo = sg.pos[t] + (int64_t)(tile - sg.tbase[t]) * kRadixTile;
-    const int64_t hi = min<int64_t>(sg.pos[t + 1], lo + kRadixTile);
-    const uint32_t kb = (uint32_t)key_base[t];
-    for (int64_t i0 = lo + wv * 64; i0 < hi; i0 += 256) {
-      const int64_t i = i0 + lane;
-      const bool valid = i < hi;
-      const uint32_t k = valid ? keys[i] : 0u;
-      const uint32_t nsk = (uint32_t)__popcll(__ballot(valid && k == kKeyInvalid));
-      if (lane == 0 && nsk) atomicAdd(&skipped_s, nsk);
-      // one LDS atomic per lane: within a table the digits of neighbouring lookups
-      // are spread, so the cross-lane step of a wave leader costs more than the
-      // collisions it saves; a wave of one digit serialises on one LDS word only
-      for (int p = 0; p < passes; ++p)
-        if (valid) atomicAdd(&h[wv][p][seg_digit(k, kb, 8 * p)], 1u);
-    }
-  }
-  if (cur >= 0) flush(cur);
-  if (threadIdx.x == 0 && skipped_s) atomicAdd(n_skipped, skipped_s);
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < status_words; i += stride) status[i] = 0;
 }
 
 // base[t][p][d] = P_t + number of table t's keys whose pass-p digit is below d (one
@@ -616,6 +558,21 @@ hipError_t sort_pairs(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32_t* vB, in
   return hipGetLastError();
 }
 
+hipError_t seg_begin(int64_t n, int passes, const int32_t* off, int32_t B, int T, const int64_t* key_base,
+                     const unsigned long long* ctr, const SortScratch& ss, const SegSort& sg, ExpandHist* eh,
+                     hipStream_t s) {
+  if (n <= 0 || passes < 1 || passes >= kMaxPasses || n > (int64_t)kStCount || T < 1) return hipErrorInvalidValue;
+  k_sort_begin<<<1, 256, 0, s>>>(ss.ghist, ss.tickets);
+  k_seg_setup<<<1, 256, 0, s>>>(off, B, T, n, ctr, sg);
+  eh->hist = sg.hist;
+  eh->key_base = key_base;
+  eh->n_skipped = ss.ghist;
+  eh->status = ss.status[0];
+  eh->status_words = 256 * ((n + kRadixTile - 1) / kRadixTile + T);
+  eh->passes = passes;
+  return hipGetLastError();
+}
+
 hipError_t sort_pairs_segmented(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32_t* vB, int64_t n, int passes,
                                 const int32_t* off, int32_t B, int T, const int64_t* key_base,
                                 const unsigned long long* ctr, const SortScratch& ss, const SegSort& sg, int32_t* err,
@@ -627,10 +584,6 @@ hipError_t sort_pairs_segmented(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32
   const int64_t sw = 256 * nb_max;
   uint32_t* n_skipped = ss.ghist;  // zeroed by k_sort_begin
   uint32_t* skip_base = ss.gbase;
-  k_sort_begin<<<1, 256, 0, s>>>(ss.ghist, ss.tickets);
-  k_seg_setup<<<1, 256, 0, s>>>(off, B, T, n, ctr, sg);
-  k_seg_hist<<<(unsigned)((nb_max + kSegHistTiles - 1) / kSegHistTiles), 256, 0, s>>>(
-      kA, n, passes, key_base, T, sg, n_skipped, ss.status[0], sw);
   k_seg_scan<<<(unsigned)T, 256, 0, s>>>(sg, passes, n, n_skipped, skip_base);
   for (int pass = 0; pass < passes; ++pass) {
     const uint32_t* ki = *in_B ? kB : kA;
@@ -664,84 +617,152 @@ hipError_t sort_pairs_segmented(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32
 // bags finds its bag by a binary search over the 64 lane-held bag starts.
 // key: set-major row key (kKeyInvalid for an out-of-range row); value: the bag b
 // within its table (its gradient row in grad_out [B][T][d] is b*T + t).
+// With SEG (the per-table sort mode) the expansion also does the counting of that mode,
+// from the keys it forms rather than from a second read of them: per table, the digit
+// counts of every pass of the local key (255 in every digit for a skipped key), the
+// number of skipped keys, and the cleared status words of the first pass.  A
+// workgroup gathers the counts of its first bag's table in LDS and adds them once; a
+// key of another table (a workgroup across a table boundary) is added directly.
+// Positions outside every bag belong to the first table's segment (before the first
+// bag) or the last one's (after the last bag), as the segment starts place them.
+template <bool SEG>
 __global__ __launch_bounds__(256) void k_expand(Dev dv, const int32_t* __restrict__ idx, int64_t L,
                                                 const int32_t* __restrict__ off, int32_t B, DivConst byB,
                                                 uint32_t* __restrict__ keys, uint32_t* __restrict__ vals,
-                                                int64_t nbag_waves, const unsigned long long* __restrict__ ctr) {
-  const int lane = threadIdx.x & 63;
-  const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+                                                int64_t nbag_waves, int64_t bag_blocks,
+                                                const unsigned long long* __restrict__ ctr, ExpandHist eh) {
+  __shared__ uint32_t h[SEG ? kMaxPasses * 256 : 1];
+  __shared__ uint32_t skipped_s;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int64_t nbags = (int64_t)dv.T * B;
+  if constexpr (SEG) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < eh.status_words; i += stride)
+      eh.status[i] = 0;
+  }
   if (ctr[kCBadOffsets]) {
-    // offsets failed validation: every lookup of the step is skipped
+    // offsets failed validation: every lookup of the step is skipped (and the whole
+    // stream is the first table's segment)
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < L; p += stride)
       keys[p] = kKeyInvalid, vals[p] = 0;
+    if constexpr (SEG) {
+      if (blockIdx.x == 0 && threadIdx.x == 0 && L > 0) {
+        for (int p = 0; p < eh.passes; ++p) atomicAdd(&eh.hist[p * 256 + 255], (uint32_t)L);
+        atomicAdd(eh.n_skipped, (uint32_t)L);
+      }
+    }
     return;
   }
-  if (wave >= nbag_waves) {
+  if ((int64_t)blockIdx.x >= bag_blocks) {
     // positions outside every bag: [0, off[0]) and [off[nbags], L)
     const int64_t head = min<int64_t>(max<int64_t>(off[0], 0), L);
     const int64_t tail = min<int64_t>(max<int64_t>(off[nbags], head), L);
-    const int64_t tid = ((wave - nbag_waves) << 6) + lane;
-    const int64_t stride = 64 * (int64_t)(gridDim.x * (blockDim.x >> 6) - nbag_waves);
+    const int64_t tid = ((int64_t)blockIdx.x - bag_blocks) * blockDim.x + threadIdx.x;
+    const int64_t stride = ((int64_t)gridDim.x - bag_blocks) * blockDim.x;
     for (int64_t p = tid; p < head; p += stride) keys[p] = kKeyInvalid, vals[p] = 0;
     for (int64_t p = tail + tid; p < L; p += stride) keys[p] = kKeyInvalid, vals[p] = 0;
+    if constexpr (SEG) {
+      if (tid == 0 && head + (L - tail) > 0) {
+        const int64_t last = (int64_t)(dv.T - 1) * kMaxPasses * 256;
+        for (int p = 0; p < eh.passes; ++p) {
+          if (head) atomicAdd(&eh.hist[p * 256 + 255], (uint32_t)head);
+          if (L - tail) atomicAdd(&eh.hist[last + p * 256 + 255], (uint32_t)(L - tail));
+        }
+        atomicAdd(eh.n_skipped, (uint32_t)(head + (L - tail)));
+      }
+    }
     return;
   }
-  const int64_t bag0 = wave * 64;
-  const int64_t mybag = bag0 + lane;
-  const int64_t lastbag = min<int64_t>(bag0 + 64, nbags);
-  int64_t st = L;
-  if (mybag < nbags) st = min<int64_t>(max<int64_t>(off[mybag], 0), L);
-  const int64_t P0 = min<int64_t>(max<int64_t>(off[bag0], 0), L);
-  const int64_t P1 = min<int64_t>(max<int64_t>(off[lastbag], P0), L);
-  uint32_t n_ok = 0, n_bad = 0;
-  // global bags are below 2^32 (checked when the handle is created): their table by
-  // one high multiply; the descriptor of the wave's first table is loaded once
-  const int t_run = (int)div_by((uint32_t)bag0, byB);
-  const TableDesc td_run = dv.desc[t_run];
-  for (int64_t pc = P0; pc < P1; pc += 64) {
-    const int64_t p = pc + lane;
-    const bool in = p < P1;
-    const int32_t r = in ? idx[p] : 0;  // in flight during the search
-    // largest lane j with start_j <= p
-    int j = 0;
+  // the table whose counts this workgroup gathers in LDS: that of its first bag
+  const int t_wg = (int)div_by((uint32_t)((int64_t)blockIdx.x * 256), byB);
+  uint32_t kb_wg = 0;
+  if constexpr (SEG) {
+    kb_wg = (uint32_t)eh.key_base[t_wg];
+    for (int i = threadIdx.x; i < kMaxPasses * 256; i += 256) h[i] = 0;
+    if (threadIdx.x == 0) skipped_s = 0;
+    __syncthreads();
+  }
+  uint32_t n_skip = 0;
+  const int64_t bw = (int64_t)blockIdx.x * 4 + wv;
+  if (bw < nbag_waves) {
+    const int64_t bag0 = bw * 64;
+    const int64_t mybag = bag0 + lane;
+    const int64_t lastbag = min<int64_t>(bag0 + 64, nbags);
+    int64_t st = L;
+    if (mybag < nbags) st = min<int64_t>(max<int64_t>(off[mybag], 0), L);
+    const int64_t P0 = min<int64_t>(max<int64_t>(off[bag0], 0), L);
+    const int64_t P1 = min<int64_t>(max<int64_t>(off[lastbag], P0), L);
+    uint32_t n_ok = 0, n_bad = 0;
+    // global bags are below 2^32 (checked when the handle is created): their table by
+    // one high multiply; the descriptor of the wave's first table is loaded once
+    const int t_run = (int)div_by((uint32_t)bag0, byB);
+    const TableDesc td_run = dv.desc[t_run];
+    for (int64_t pc = P0; pc < P1; pc += 64) {
+      const int64_t p = pc + lane;
+      const bool in = p < P1;
+      const int32_t r = in ? idx[p] : 0;  // in flight during the search
+      // largest lane j with start_j <= p
+      int j = 0;
 #pragma unroll
-    for (int step = 32; step >= 1; step >>= 1) {
-      const int64_t s2 = __shfl(st, j + step);
-      if (j + step < 64 && s2 <= p) j += step;
-    }
-    if (in) {
-      const uint32_t bag = (uint32_t)(bag0 + j);
-      const int t = (int)div_by(bag, byB);
-      const int b = (int)(bag - (uint32_t)t * (uint32_t)B);
-      const TableDesc td = t == t_run ? td_run : dv.desc[t];
-      uint32_t key = kKeyInvalid;
-      if (r >= 0 && (int64_t)r < td.N) {
-        if (td.n_sets > 0) {
-          const uint32_t q = div_by((uint32_t)r, td.by_sets);
-          const uint32_t set = (uint32_t)r - q * (uint32_t)td.n_sets;
-          key = (uint32_t)(td.key_base + (int64_t)set * td.Q + q);
-        } else {
-          key = (uint32_t)(td.key_base + r);
-        }
-        if (t == t_run) ++n_ok; else atomicAdd(&dv.stats[(int64_t)t * kNStat + kStBwdLookups], 1ull);
-      } else {
-        if (t == t_run) ++n_bad; else atomicAdd(&dv.stats[(int64_t)t * kNStat + kStInvalidBwd], 1ull);
-        atomicOr(dv.err, kErrIndex);
+      for (int step = 32; step >= 1; step >>= 1) {
+        const int64_t s2 = __shfl(st, j + step);
+        if (j + step < 64 && s2 <= p) j += step;
       }
-      keys[p] = key;
-      vals[p] = (uint32_t)b;
+      if (in) {
+        const uint32_t bag = (uint32_t)(bag0 + j);
+        const int t = (int)div_by(bag, byB);
+        const int b = (int)(bag - (uint32_t)t * (uint32_t)B);
+        const TableDesc td = t == t_run ? td_run : dv.desc[t];
+        uint32_t key = kKeyInvalid;
+        if (r >= 0 && (int64_t)r < td.N) {
+          if (td.n_sets > 0) {
+            const uint32_t q = div_by((uint32_t)r, td.by_sets);
+            const uint32_t set = (uint32_t)r - q * (uint32_t)td.n_sets;
+            key = (uint32_t)(td.key_base + (int64_t)set * td.Q + q);
+          } else {
+            key = (uint32_t)(td.key_base + r);
+          }
+          if (t == t_run) ++n_ok; else atomicAdd(&dv.stats[(int64_t)t * kNStat + kStBwdLookups], 1ull);
+        } else {
+          if (t == t_run) ++n_bad; else atomicAdd(&dv.stats[(int64_t)t * kNStat + kStInvalidBwd], 1ull);
+          atomicOr(dv.err, kErrIndex);
+        }
+        keys[p] = key;
+        vals[p] = (uint32_t)b;
+        if constexpr (SEG) {
+          n_skip += key == kKeyInvalid;
+          if (t == t_wg) {
+            for (int q = 0; q < eh.passes; ++q) atomicAdd(&h[q * 256 + seg_digit(key, kb_wg, 8 * q)], 1u);
+          } else {
+            const uint32_t kb = (uint32_t)eh.key_base[t];
+            uint32_t* ht = eh.hist + (int64_t)t * kMaxPasses * 256;
+            for (int q = 0; q < eh.passes; ++q) atomicAdd(&ht[q * 256 + seg_digit(key, kb, 8 * q)], 1u);
+          }
+        }
+      }
     }
-  }
-  // lookups of the wave's first table: one atomic per wave
+    // lookups of the wave's first table: one atomic per wave
 #pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) {
-    n_ok += __shfl_xor(n_ok, o);
-    n_bad += __shfl_xor(n_bad, o);
+    for (int o = 32; o >= 1; o >>= 1) {
+      n_ok += __shfl_xor(n_ok, o);
+      n_bad += __shfl_xor(n_bad, o);
+    }
+    if (lane == 0 && n_ok) atomicAdd(&dv.stats[(int64_t)t_run * kNStat + kStBwdLookups], (unsigned long long)n_ok);
+    if (lane == 0 && n_bad) atomicAdd(&dv.stats[(int64_t)t_run * kNStat + kStInvalidBwd], (unsigned long long)n_bad);
   }
-  if (lane == 0 && n_ok) atomicAdd(&dv.stats[(int64_t)t_run * kNStat + kStBwdLookups], (unsigned long long)n_ok);
-  if (lane == 0 && n_bad) atomicAdd(&dv.stats[(int64_t)t_run * kNStat + kStInvalidBwd], (unsigned long long)n_bad);
+  if constexpr (SEG) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) n_skip += __shfl_xor(n_skip, o);
+    if (lane == 0 && n_skip) atomicAdd(&skipped_s, n_skip);
+    __syncthreads();
+    uint32_t* ht = eh.hist + (int64_t)t_wg * kMaxPasses * 256;
+    for (int i = threadIdx.x; i < eh.passes * 256; i += 256) {
+      const uint32_t c = h[i];
+      if (c) atomicAdd(&ht[i], c);
+    }
+    if (threadIdx.x == 0 && skipped_s) atomicAdd(eh.n_skipped, skipped_s);
+  }
 }
 
 __global__ __launch_bounds__(256) void k_check_offsets(Dev dv, const int32_t* __restrict__ off, int64_t nbags,
@@ -757,13 +778,19 @@ __global__ __launch_bounds__(256) void k_check_offsets(Dev dv, const int32_t* __
 }
 
 hipError_t launch_expand(const Dev& dv, const int32_t* idx, int64_t L, const int32_t* off, int32_t B, uint32_t* keys,
-                         uint32_t* vals, unsigned long long* ctr, hipStream_t s) {
+                         uint32_t* vals, unsigned long long* ctr, const ExpandHist* eh, hipStream_t s) {
   const int64_t nbags = (int64_t)dv.T * B;
   const int64_t nbag_waves = (nbags + 63) / 64;
-  const int64_t tail_waves = 64;
-  const int64_t waves = nbag_waves + tail_waves;
+  const int64_t bag_blocks = (nbag_waves + 3) / 4;
+  const int64_t tail_blocks = 16;
   const DivConst byB = div_const(B > 0 ? (uint32_t)B : 1u);  // no bag when B = 0
-  k_expand<<<(unsigned)((waves + 3) / 4), 256, 0, s>>>(dv, idx, L, off, B, byB, keys, vals, nbag_waves, ctr);
+  const unsigned grid = (unsigned)(bag_blocks + tail_blocks);
+  if (eh) {
+    k_expand<true><<<grid, 256, 0, s>>>(dv, idx, L, off, B, byB, keys, vals, nbag_waves, bag_blocks, ctr, *eh);
+  } else {
+    k_expand<false><<<grid, 256, 0, s>>>(dv, idx, L, off, B, byB, keys, vals, nbag_waves, bag_blocks, ctr,
+                                         ExpandHist{});
+  }
   return hipGetLastError();
 }
 

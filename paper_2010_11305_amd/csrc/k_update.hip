@@ -972,19 +972,24 @@ hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int6
   const int64_t nbags = (int64_t)d.T * B;
   k_check_offsets<<<grid_for(nbags, 2048), 256, 0, s>>>(d, off, nbags, L, w.ctr);
   if (decay && d.cnt) k_decay<<<grid_for(d.total_rows), 256, 0, s>>>(d.cnt, d.total_rows, w.ctr);
-  hipError_t e = launch_expand(d, idx, L, off, B, w.keysA, w.valsA, w.ctr, s);
-  if (e != hipSuccess) return e;
   const int passes = (key_bits + 7) / 8;
   int in_B = 0;
   const SortScratch ss{w.sort_small, w.sort_small + kMaxPasses * 256, w.sort_small + 2 * kMaxPasses * 256,
                        {w.sort_status[0], w.sort_status[1]}};
-  if (seg_passes > 0 && seg_passes < passes) {
+  hipError_t e;
+  if (seg_passes > 0 && seg_passes < passes && L > 0) {
+    // per-table sort: the expansion also counts the digits
     const size_t TT = (size_t)d.T * kMaxPasses * 256;
     const SegSort sg{w.sort_seg, w.sort_seg + (d.T + 1), w.sort_seg + 2 * (d.T + 1), w.sort_seg + 2 * (d.T + 1) + TT};
-    e = sort_pairs_segmented(w.keysA, w.valsA, w.keysB, w.valsB, L, seg_passes, off, B, d.T, d.key_base, w.ctr, ss,
-                             sg, d.err, &in_B, s);
+    ExpandHist eh;
+    e = seg_begin(L, seg_passes, off, B, d.T, d.key_base, w.ctr, ss, sg, &eh, s);
+    if (e == hipSuccess) e = launch_expand(d, idx, L, off, B, w.keysA, w.valsA, w.ctr, &eh, s);
+    if (e == hipSuccess)
+      e = sort_pairs_segmented(w.keysA, w.valsA, w.keysB, w.valsB, L, seg_passes, off, B, d.T, d.key_base, w.ctr,
+                               ss, sg, d.err, &in_B, s);
   } else {
-    e = sort_pairs(w.keysA, w.valsA, w.keysB, w.valsB, L, passes, ss, d.err, &in_B, s);
+    e = launch_expand(d, idx, L, off, B, w.keysA, w.valsA, w.ctr, nullptr, s);
+    if (e == hipSuccess) e = sort_pairs(w.keysA, w.valsA, w.keysB, w.valsB, L, passes, ss, d.err, &in_B, s);
   }
   if (e != hipSuccess) return e;
   const uint32_t* sk = in_B ? w.keysB : w.keysA;
