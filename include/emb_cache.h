@@ -120,7 +120,9 @@ typedef struct emb_cache_sizes {
   size_t workspace_bytes; /* per-call temporaries of forward/backward_update */
   int64_t total_rows;     /* sum of rows[t] */
   int64_t total_slots;    /* sum over tables of n_sets*assoc */
-  int32_t row_bytes;      /* bytes of one low-precision row record (codes + scale + bias) */
+  int32_t row_bytes;      /* bytes of one low-precision row record: codes + scale + bias, then,
+                             under row-wise Adagrad, the row's FP32 accumulator, padded to the
+                             alignment of the first part (at most 16 bytes) */
   int32_t pad;
   size_t table_bytes;     /* the low-precision table: the last table_bytes of state_bytes */
 } emb_cache_sizes;

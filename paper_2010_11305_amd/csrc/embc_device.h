@@ -27,12 +27,28 @@ struct Geo {
 
 // A row record of the low-precision table: the codes (BITS 8, 4, 2) followed by the
 // row's (scale, bias), FP16 pair or FP32 pair; or, for BITS 16, the row's binary16
-// elements alone.
+// elements alone.  Under row-wise Adagrad the row's FP32 accumulator follows at byte
+// BYTES, and the record is padded to a multiple of ALIGN (the alignment BYTES has, at
+// most 16), so that every record keeps the alignment of its code words.  The stride
+// is Dev::rec_bytes.
 template <int D, int BITS, bool SB16>
 struct Rec {
   static constexpr int CODE_BYTES = D * BITS / 8;
   static constexpr int BYTES = CODE_BYTES + (BITS == 16 ? 0 : SB16 ? 4 : 8);
+  static constexpr int ALIGN = (BYTES & -BYTES) < 16 ? (BYTES & -BYTES) : 16;
 };
+
+// Record of global row grow.
+template <int D, int BITS, bool SB16>
+__device__ __forceinline__ uint8_t* rec_of(const Dev& dv, int64_t grow) {
+  return static_cast<uint8_t*>(__builtin_assume_aligned(dv.rec + grow * dv.rec_bytes, Rec<D, BITS, SB16>::ALIGN));
+}
+
+// The row-wise Adagrad accumulator inside a record.
+template <int D, int BITS, bool SB16>
+__device__ __forceinline__ float* acc_of(uint8_t* rec) {
+  return reinterpret_cast<float*>(rec + Rec<D, BITS, SB16>::BYTES);
+}
 
 // ---- lane exchange inside a row group ---------------------------------------------------
 // x of lane (lane ^ M), for M < LPR.  Masks 1..8 stay inside a 16-lane DPP row and use

@@ -3,12 +3,16 @@
 // Data layout in HBM (one caller-owned state buffer, 256-byte aligned pieces):
 //   rec   [total_rows][row_bytes]   low-precision row records: codes, then scale, then bias
 //                                   (INT4: two codes per byte, even column in the low nibble;
-//                                   scale/bias FP32 pair, or FP16 pair packed in one dword)
+//                                   scale/bias FP32 pair, or FP16 pair packed in one dword),
+//                                   then, under row-wise Adagrad, the row's FP32 accumulator
+//                                   while the row is not cached (a miss reads it with the codes)
 //   crow  [total_slots][dim] FP32   cache rows; slot = slot_base[t] + set*assoc + way
 //   tag   [total_slots] int32       resident row id (table-local), -1 = empty way
 //   ts    [total_slots] int32       LRU: step of last access (-1 = empty); absent under LFU
+//   acc_slot [total_slots] FP32     row-wise Adagrad: the accumulator of the row cached in the
+//                                   slot (it moves between record and slot with the row); absent
+//                                   under SGD
 //   cnt   [total_rows] int32        LFU: access counts; absent under LRU
-//   G     [total_rows] FP32         row-wise Adagrad accumulators; absent under SGD
 //   desc  [T] TableDesc, key_base [T+1], stats [T][kNStat] u64, err flags
 // Rows of all tables are concatenated (global row = row_base[t] + row), and so
 // are cache slots, so one base pointer serves every table.
@@ -75,7 +79,7 @@ struct Dev {
   int32_t* tag;
   int32_t* ts;
   int32_t* cnt;
-  float* G;
+  float* acc_slot;
   const TableDesc* desc;
   const int64_t* key_base;       // [T+1], key_base[T] = total key space
   unsigned long long* stats;     // [T][kNStat]
@@ -85,7 +89,8 @@ struct Dev {
   int32_t bits;
   int32_t sb16;
   int32_t assoc;
-  int32_t rec_bytes;
+  int32_t rec_bytes;  // record stride (Rec<>::BYTES, plus the accumulator and padding under Adagrad)
+  int32_t acc_offset; // byte of the accumulator in a record (Rec<>::BYTES)
   int32_t policy;     // 0 LRU, 1 LFU
   int32_t rounding;   // 0 nearest, 1 stochastic
   int32_t optimizer;  // 0 SGD, 1 row-wise Adagrad
@@ -156,6 +161,10 @@ enum : int {
 hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int64_t n, hipStream_t s);
 hipError_t launch_reset_state(const Dev& d, hipStream_t s);
 hipError_t launch_init_uniform(const Dev& d, float lo, float hi, uint64_t init_seed, hipStream_t s);
+// Row-wise Adagrad: the accumulators of the rows cached in global slots [slot0, slot0 + slots)
+// (one table, whose rows start at row_base) from the slot array to the records (to_rec),
+// or from the records to the slot array.
+hipError_t launch_move_acc(const Dev& d, int64_t slot0, int64_t slots, int64_t row_base, bool to_rec, hipStream_t s);
 hipError_t launch_forward(const Dev& d, const Work& w, const int32_t* idx, int64_t L, const int32_t* off,
                           int32_t B, float* out, hipStream_t s);
 // The forward with its temporaries in the library's static scratch array instead of a

@@ -27,7 +27,7 @@ hipError_t launch_reset_state(const Dev& d, hipStream_t s) {
   if (e == hipSuccess) e = launch_fill_u32(reinterpret_cast<uint32_t*>(d.tag), 0xFFFFFFFFu, d.total_slots, s);
   if (e == hipSuccess && d.ts) e = launch_fill_u32(reinterpret_cast<uint32_t*>(d.ts), 0xFFFFFFFFu, d.total_slots, s);
   if (e == hipSuccess && d.cnt) e = launch_fill_u32(reinterpret_cast<uint32_t*>(d.cnt), 0u, d.total_rows, s);
-  if (e == hipSuccess && d.G) e = launch_fill_u32(reinterpret_cast<uint32_t*>(d.G), 0u, d.total_rows, s);
+  if (e == hipSuccess && d.acc_slot) e = launch_fill_u32(reinterpret_cast<uint32_t*>(d.acc_slot), 0u, d.total_slots, s);
   if (e == hipSuccess) e = launch_fill_u32(reinterpret_cast<uint32_t*>(d.stats), 0u, (int64_t)d.T * kNStat * 2, s);
   if (e == hipSuccess) e = launch_fill_u32(reinterpret_cast<uint32_t*>(d.err), 0u, 1, s);
   return e;
@@ -44,11 +44,10 @@ __device__ __forceinline__ int table_of_row(const Dev& dv, int64_t grow) {
 }
 
 // x_j = u*(hi-lo) + lo (fused), u = Philox uniform keyed (init_seed; j/4, row, table, 0xFFFFFFFF),
-// then nearest-even quantization of the row.
+// then nearest-even quantization of the row; its Adagrad accumulator (if any) to 0.
 template <int D, int BITS, bool SB16>
 __global__ __launch_bounds__(256) void k_init_uniform(Dev dv, float lo, float hi, uint64_t init_seed) {
   constexpr int LPR = Geo<D>::LPR;
-  constexpr int RB = Rec<D, BITS, SB16>::BYTES;
   const int g = threadIdx.x & (LPR - 1);
   const int64_t ngroups = (int64_t)gridDim.x * blockDim.x / LPR;
   const float width = hi - lo;
@@ -60,8 +59,29 @@ __global__ __launch_bounds__(256) void k_init_uniform(Dev dv, float lo, float hi
     uniforms8(init_seed, 0xFFFFFFFFu, (uint32_t)t, r, g, u);
 #pragma unroll
     for (int i = 0; i < 8; ++i) x[i] = __builtin_fmaf(u[i], width, lo);
-    quantize_store<D, BITS, SB16>(x, g, dv.rec + grow * RB, false, 0, 0, 0, 0);
+    uint8_t* rec = rec_of<D, BITS, SB16>(dv, grow);
+    quantize_store<D, BITS, SB16>(x, g, rec, false, 0, 0, 0, 0);
+    if (dv.optimizer && g == 0) *acc_of<D, BITS, SB16>(rec) = 0.0f;
   }
+}
+
+// Row-wise Adagrad: the accumulators of the rows cached in slots [s0, s0 + n) of the table
+// whose rows start at row_base, moved from the slots to the records (to_rec) or back.
+__global__ __launch_bounds__(256) void k_move_acc(Dev dv, int64_t s0, int64_t n, int64_t row_base, bool to_rec) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+    const int32_t r = dv.tag[s0 + i];
+    if (r < 0) continue;
+    float* a = reinterpret_cast<float*>(dv.rec + (row_base + r) * dv.rec_bytes + dv.acc_offset);
+    if (to_rec) *a = dv.acc_slot[s0 + i];
+    else dv.acc_slot[s0 + i] = *a;
+  }
+}
+
+hipError_t launch_move_acc(const Dev& d, int64_t slot0, int64_t slots, int64_t row_base, bool to_rec, hipStream_t s) {
+  if (!d.acc_slot || slots <= 0) return hipSuccess;
+  k_move_acc<<<grid_for(slots), 256, 0, s>>>(d, slot0, slots, row_base, to_rec);
+  return hipGetLastError();
 }
 
 hipError_t launch_init_uniform(const Dev& d, float lo, float hi, uint64_t init_seed, hipStream_t s) {
@@ -69,7 +89,7 @@ hipError_t launch_init_uniform(const Dev& d, float lo, float hi, uint64_t init_s
   if (e == hipSuccess && d.ts) e = launch_fill_u32(reinterpret_cast<uint32_t*>(d.ts), 0xFFFFFFFFu, d.total_slots, s);
   if (e == hipSuccess) e = launch_fill_u32(reinterpret_cast<uint32_t*>(d.crow), 0u, d.total_slots * d.dim, s);
   if (e == hipSuccess && d.cnt) e = launch_fill_u32(reinterpret_cast<uint32_t*>(d.cnt), 0u, d.total_rows, s);
-  if (e == hipSuccess && d.G) e = launch_fill_u32(reinterpret_cast<uint32_t*>(d.G), 0u, d.total_rows, s);
+  if (e == hipSuccess && d.acc_slot) e = launch_fill_u32(reinterpret_cast<uint32_t*>(d.acc_slot), 0u, d.total_slots, s);
   if (e != hipSuccess) return e;
   return dispatch_row(d.dim, d.bits, d.sb16, [&]<int D, int BITS, bool SB16>() -> hipError_t {
     const int64_t threads = d.total_rows * Geo<D>::LPR;
@@ -219,7 +239,7 @@ __global__ __launch_bounds__(256) void k_fwd_gather(Dev dv, const int32_t* __res
                                                     float* __restrict__ out) {
   constexpr int LPR = Geo<D>::LPR, FU = kFwdUnroll;
   constexpr int GPB = 256 / LPR;
-  constexpr int RB = Rec<D, BITS, SB16>::BYTES;
+  const int64_t RB = dv.rec_bytes;
   const int g = threadIdx.x & (LPR - 1);
   const XcdSplit xs(dv.T);
   const int64_t gx = xs.unit * GPB + threadIdx.x / LPR, gstride = xs.units * GPB;
@@ -273,7 +293,8 @@ __global__ __launch_bounds__(256) void k_fwd_gather(Dev dv, const int32_t* __res
             if (kind[q] == 1) {
               load_frow8(dv.crow + (int64_t)cq * D, g, raw[q]);
             } else if (kind[q] == 2) {
-              const uint8_t* rec = rec0 + (int64_t)(-2 - cq) * RB;
+              const uint8_t* rec = static_cast<const uint8_t*>(
+                  __builtin_assume_aligned(rec0 + (int64_t)(-2 - cq) * RB, Rec<D, BITS, SB16>::ALIGN));
               cw[q] = load_code_words<BITS>(rec, g);
               sbw[q] = load_sb_words<D, BITS, SB16>(rec);
             }

@@ -567,7 +567,7 @@ __global__ __launch_bounds__(256) void k_partials(Dev dv, Work w, const uint32_t
 // (a[j] += a[j + h] for h = D/2, ..., 1: across lanes g ^ (h/8) while h >= 8, then
 // inside the lane), G += S * (1/D), r = lr / (sqrt(G) + eps), x = fma(-r, g, x).
 template <int D>
-__device__ __forceinline__ void apply_optimizer(const Dev& dv, float (&x)[8], const float (&gr)[8], int64_t grow,
+__device__ __forceinline__ void apply_optimizer(const Dev& dv, float (&x)[8], const float (&gr)[8], float* acc,
                                                 int g, float G_old) {
   constexpr int LPR = Geo<D>::LPR;
   if (dv.optimizer == 0) {
@@ -585,15 +585,16 @@ __device__ __forceinline__ void apply_optimizer(const Dev& dv, float (&x)[8], co
 #pragma unroll
     for (int i = 0; i < h; ++i) a[i] = a[i] + a[i + h];
   const float Gn = G_old + a[0] * (1.0f / (float)D);
-  if (g == 0) __builtin_nontemporal_store(Gn, dv.G + grow);
+  if (g == 0) *acc = Gn;
   const float rate = dv.lr / (__builtin_sqrtf(Gn) + dv.eps);
 #pragma unroll
   for (int i = 0; i < 8; ++i) x[i] = __builtin_fmaf(-rate, gr[i], x[i]);
 }
 
-// The accumulator of a row is read and written once per step (nontemporal).
-__device__ __forceinline__ float load_G(const Dev& dv, int64_t grow) {
-  return dv.optimizer ? __builtin_nontemporal_load(dv.G + grow) : 0.0f;
+// A row's Adagrad accumulator: in the slot array while the row is cached, in its record
+// otherwise (it moves with the row on an insert and an eviction).
+__device__ __forceinline__ float load_G(const Dev& dv, const float* acc) {
+  return dv.optimizer ? *acc : 0.0f;
 }
 
 // ---- replacement decision, one wave per touched set ------------------------------------------
@@ -811,7 +812,6 @@ __global__ __launch_bounds__(256) void k_evict(Dev dv, Work w, const uint32_t* _
   if (UPDATED && w.ctr[kCHitEv] == 0) return;
   constexpr int LPR = Geo<D>::LPR;
   constexpr int GPW = 64 / LPR;  // row groups per wave
-  constexpr int RB = Rec<D, BITS, SB16>::BYTES;
   const int lane = threadIdx.x & 63;
   const int g = lane & (LPR - 1), grp = lane / LPR;
   const bool sr = dv.rounding != 0;
@@ -849,17 +849,22 @@ __global__ __launch_bounds__(256) void k_evict(Dev dv, Work w, const uint32_t* _
         const int32_t e_dst = __shfl(dst, src), e_vrow = __shfl(vrow, src), e_vu = __shfl(vu, src);
         if (!mine) continue;
         const int64_t vgrow = td.row_base + e_vrow;
+        uint8_t* vrec = rec_of<D, BITS, SB16>(dv, vgrow);
         float xv[8];
         load_frow8_nt(dv.crow + (int64_t)e_dst * D, g, xv);
+        // the displaced row's accumulator leaves the slot for its record (before the
+        // insert that takes the slot writes its own there)
+        float* acc = dv.optimizer ? acc_of<D, BITS, SB16>(vrec) : nullptr;
         if (UPDATED) {
           // the displaced resident was updated this step (LFU): its new value goes to T
-          const float Gv = load_G(dv, vgrow);
+          const float Gv = dv.optimizer ? dv.acc_slot[e_dst] : 0.0f;
           float gv[8];
           merged_grad<D>(w, sval, grad_rows<D>(grad, t, dv.T), e_vu, g, gv);
-          apply_optimizer<D>(dv, xv, gv, vgrow, g, Gv);
+          apply_optimizer<D>(dv, xv, gv, acc, g, Gv);
+        } else if (dv.optimizer && g == 0) {
+          *acc = dv.acc_slot[e_dst];
         }
-        quantize_store<D, BITS, SB16>(xv, g, dv.rec + vgrow * RB, sr, dv.seed, step, (uint32_t)t,
-                                      (uint32_t)e_vrow);
+        quantize_store<D, BITS, SB16>(xv, g, vrec, sr, dv.seed, step, (uint32_t)t, (uint32_t)e_vrow);
       }
     }
   }
@@ -897,7 +902,6 @@ __global__ __launch_bounds__(256) void k_update(Dev dv, Work w, const uint32_t* 
                                                 const float* __restrict__ grad, uint32_t step) {
   constexpr int LPR = Geo<D>::LPR;
   constexpr int GPB = 256 / LPR;
-  constexpr int RB = Rec<D, BITS, SB16>::BYTES;
   const int g = threadIdx.x & (LPR - 1);
   const bool sr = dv.rounding != 0;
   const XcdSplit xs(dv.T, true);
@@ -919,8 +923,16 @@ __global__ __launch_bounds__(256) void k_update(Dev dv, Work w, const uint32_t* 
       const uint32_t kind = m.w >> 30, n = m.w & kLookupMask;
       if (kind == kKindDone) continue;
       const int64_t grow = m.x;
-      uint8_t* rec = dv.rec + grow * RB;
+      uint8_t* rec = rec_of<D, BITS, SB16>(dv, grow);
       const bool hit = kind == kKindHit;
+      // the accumulator: in the slot of a hit, in the record of a miss; an insert takes it
+      // to the slot it fills, a bypass leaves it in the record
+      float* acc = nullptr;
+      float* acc_out = nullptr;
+      if (dv.optimizer) {
+        acc = hit ? dv.acc_slot + (int32_t)m.y : acc_of<D, BITS, SB16>(rec);
+        acc_out = kind == kKindBypass ? acc : dv.acc_slot + (int32_t)m.y;
+      }
       const bool big = n > kBlockAbove;
       // first level of loads: the row, its accumulator, and the gradient row (one
       // lookup) or the first occurrence values (2 to kSumChunk lookups)
@@ -937,7 +949,7 @@ __global__ __launch_bounds__(256) void k_update(Dev dv, Work w, const uint32_t* 
         cw = load_code_words<BITS, true>(rec, g);
         sbw = load_sb_words<D, BITS, SB16>(rec);
       }
-      const float G_old = load_G(dv, grow);
+      const float G_old = load_G(dv, acc);
       if (big) load_frow8(w.bpart + (int64_t)w.ubig[u] * w.max_nblk * D, g, gr);
       else if (n > (uint32_t)kSumChunk)
         fold_chunks<D>(w.partial, w.chunk_base[u], (n + kSumChunk - 1) / kSumChunk, g, gr);
@@ -947,7 +959,7 @@ __global__ __launch_bounds__(256) void k_update(Dev dv, Work w, const uint32_t* 
         decode_sb<SB16>(sbw, sc, bi);
         dequant8<BITS>(cw, sc, bi, x);
       }
-      apply_optimizer<D>(dv, x, gr, grow, g, G_old);
+      apply_optimizer<D>(dv, x, gr, acc_out, g, G_old);
       if (hit || kind == kKindInsert) {
         const int64_t cs = (int32_t)m.y;
         store_frow8_nt(dv.crow + cs * D, g, x);

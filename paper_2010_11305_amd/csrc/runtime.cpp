@@ -5,6 +5,7 @@
 // library never allocates device memory.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <map>
@@ -77,10 +78,11 @@ int bit_length(uint64_t v) {
 struct Plan {
   int64_t total_rows = 0, total_slots = 0, total_keys = 0;
   int rec_bytes = 0;
+  int acc_offset = 0;  // byte of the Adagrad accumulator in a record (under row-wise Adagrad)
   std::vector<TableDesc> desc;
   std::vector<int64_t> key_base;
   // state offsets
-  size_t o_rec, o_crow, o_tag, o_ts, o_cnt, o_G, o_desc, o_keyb, o_stats, o_err, state_bytes, table_bytes;
+  size_t o_rec, o_crow, o_tag, o_ts, o_cnt, o_accs, o_desc, o_keyb, o_stats, o_err, state_bytes, table_bytes;
   // workspace offsets
   size_t o_kA, o_vA, o_kB, o_vB, o_ssmall, o_sst0, o_sst1, o_sseg, o_part, o_tcnt, o_tpre, o_tthr, o_uk, o_seg, o_setf, o_urow, o_utab, o_uslot,
       o_uact, o_udest, o_umeta, o_ukey, o_nch, o_cbase, o_uvrow, o_uvu, o_partial, o_span, o_ubig, o_brows, o_bbound, o_bpart, o_tabf, o_src, o_ctr, ws_bytes;
@@ -142,8 +144,15 @@ int plan_config(const emb_cache_config* c, Plan* p) {
   p->total_rows = rows;
   p->total_slots = slots;
   p->total_keys = keys;
-  // an FP16 table stores the elements alone; integer codes carry (s, b)
-  p->rec_bytes = c->dim * c->precision / 8 + (c->precision == EMB_FP16 ? 0 : c->sb_dtype == EMB_SB_FP16 ? 4 : 8);
+  // an FP16 table stores the elements alone; integer codes carry (s, b); under row-wise
+  // Adagrad the row's FP32 accumulator follows, the record padded to the alignment of
+  // its first part (at most 16 bytes), as Rec<> in the kernels lays it out
+  p->acc_offset = c->dim * c->precision / 8 + (c->precision == EMB_FP16 ? 0 : c->sb_dtype == EMB_SB_FP16 ? 4 : 8);
+  p->rec_bytes = p->acc_offset;
+  if (c->optimizer == EMB_OPT_ROWWISE_ADAGRAD) {
+    const int a = std::min(p->acc_offset & -p->acc_offset, 16);
+    p->rec_bytes = (p->acc_offset + 4 + a - 1) / a * a;
+  }
 
   size_t o = 0;
   auto take = [&](size_t bytes) {
@@ -156,7 +165,7 @@ int plan_config(const emb_cache_config* c, Plan* p) {
   p->o_tag = take((size_t)slots * 4);
   p->o_ts = take(lru ? (size_t)slots * 4 : 0);
   p->o_cnt = take(lfu ? (size_t)rows * 4 : 0);
-  p->o_G = take(c->optimizer == EMB_OPT_ROWWISE_ADAGRAD ? (size_t)rows * 4 : 0);
+  p->o_accs = take(c->optimizer == EMB_OPT_ROWWISE_ADAGRAD ? (size_t)slots * 4 : 0);
   p->o_desc = take(sizeof(TableDesc) * T);
   p->o_keyb = take(sizeof(int64_t) * (T + 1));
   p->o_stats = take(sizeof(unsigned long long) * T * embc::kNStat);
@@ -377,7 +386,7 @@ int create_impl(const emb_cache_config* cfg, void* state, size_t state_bytes, vo
   d.tag = reinterpret_cast<int32_t*>(sb + p.o_tag);
   d.ts = cfg->policy == EMB_LRU ? reinterpret_cast<int32_t*>(sb + p.o_ts) : nullptr;
   d.cnt = cfg->policy == EMB_LFU ? reinterpret_cast<int32_t*>(sb + p.o_cnt) : nullptr;
-  d.G = cfg->optimizer == EMB_OPT_ROWWISE_ADAGRAD ? reinterpret_cast<float*>(sb + p.o_G) : nullptr;
+  d.acc_slot = cfg->optimizer == EMB_OPT_ROWWISE_ADAGRAD ? reinterpret_cast<float*>(sb + p.o_accs) : nullptr;
   d.desc = reinterpret_cast<const TableDesc*>(sb + p.o_desc);
   d.key_base = reinterpret_cast<const int64_t*>(sb + p.o_keyb);
   d.stats = reinterpret_cast<unsigned long long*>(sb + p.o_stats);
@@ -388,6 +397,7 @@ int create_impl(const emb_cache_config* cfg, void* state, size_t state_bytes, vo
   d.sb16 = cfg->precision != EMB_FP16 && cfg->sb_dtype == EMB_SB_FP16;  // an FP16 table has no (s, b)
   d.assoc = cfg->assoc;
   d.rec_bytes = p.rec_bytes;
+  d.acc_offset = p.acc_offset;
   d.policy = cfg->policy;
   d.rounding = cfg->rounding;
   d.optimizer = cfg->optimizer;
@@ -535,6 +545,25 @@ int emb_cache_check(emb_cache_t h, void* stream) {
   return EMB_OK;
 }
 
+namespace {
+// Row-wise Adagrad: the accumulator of a cached row is in the slot array, not in its record.
+// (row - row0, global slot) of the rows of [row0, row0 + n) of `table` that are cached.
+hipError_t cached_rows(emb_cache_t h, int32_t table, int64_t row0, int64_t n, hipStream_t s,
+                       std::vector<std::pair<int64_t, int64_t>>* out) {
+  out->clear();
+  const TableDesc& td = h->plan.desc[table];
+  const int64_t slots = td.n_sets * h->cfg.assoc;
+  if (slots == 0) return hipSuccess;
+  std::vector<int32_t> tags((size_t)slots);
+  hipError_t e = hipMemcpyAsync(tags.data(), h->dev.tag + td.slot_base, 4 * (size_t)slots, hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return e;
+  for (int64_t i = 0; i < slots; ++i)
+    if (tags[i] >= row0 && tags[i] < row0 + n) out->emplace_back(tags[i] - row0, td.slot_base + i);
+  return hipSuccess;
+}
+}  // namespace
+
 int emb_cache_export_rows(emb_cache_t h, int32_t table, int64_t row0, int64_t n, void* codes_out, float* scale,
                           float* bias, int32_t* lfu_count, float* adagrad, void* stream) {
   if (!h || table < 0 || table >= h->cfg.num_tables || row0 < 0 || n < 0) return EMB_EINVAL;
@@ -544,8 +573,9 @@ int emb_cache_export_rows(emb_cache_t h, int32_t table, int64_t row0, int64_t n,
   hipStream_t s = S(stream);
   const int d = h->cfg.dim, RB = h->plan.rec_bytes, bits = h->cfg.precision;
   const int64_t g0 = td.row_base + row0;
+  const bool ada = h->cfg.optimizer == EMB_OPT_ROWWISE_ADAGRAD;
   hipError_t e = hipSuccess;
-  if (codes_out || scale || bias) {
+  if (codes_out || scale || bias || (adagrad && ada)) {
     std::vector<uint8_t> buf((size_t)n * RB);
     e = hipMemcpyAsync(buf.data(), h->dev.rec + g0 * RB, buf.size(), hipMemcpyDefault, s);  // device or pinned host table
     if (e == hipSuccess) e = hipStreamSynchronize(s);
@@ -554,6 +584,7 @@ int emb_cache_export_rows(emb_cache_t h, int32_t table, int64_t row0, int64_t n,
     uint8_t* codes = static_cast<uint8_t*>(codes_out);
     for (int64_t i = 0; i < n; ++i) {
       const uint8_t* r = buf.data() + i * RB;
+      if (adagrad && ada) std::memcpy(&adagrad[i], r + h->plan.acc_offset, 4);
       if (bits == EMB_FP16) {  // binary16 bit patterns as stored, no (s, b)
         if (codes) std::memcpy(codes + i * d * 2, r, 2 * (size_t)d);
         if (scale) scale[i] = 0.0f;
@@ -583,9 +614,12 @@ int emb_cache_export_rows(emb_cache_t h, int32_t table, int64_t row0, int64_t n,
     if (h->dev.cnt) e = hipMemcpyAsync(lfu_count, h->dev.cnt + g0, 4 * (size_t)n, hipMemcpyDeviceToHost, s);
     else std::memset(lfu_count, 0, 4 * (size_t)n);
   }
-  if (e == hipSuccess && adagrad) {
-    if (h->dev.G) e = hipMemcpyAsync(adagrad, h->dev.G + g0, 4 * (size_t)n, hipMemcpyDeviceToHost, s);
-    else std::memset(adagrad, 0, 4 * (size_t)n);
+  if (adagrad && !ada) std::memset(adagrad, 0, 4 * (size_t)n);
+  if (adagrad && ada) {
+    std::vector<std::pair<int64_t, int64_t>> cached;
+    e = cached_rows(h, table, row0, n, s, &cached);
+    for (size_t k = 0; e == hipSuccess && k < cached.size(); ++k)
+      e = hipMemcpyAsync(&adagrad[cached[k].first], h->dev.acc_slot + cached[k].second, 4, hipMemcpyDeviceToHost, s);
   }
   if (e == hipSuccess) e = hipStreamSynchronize(s);
   return hip_status(e);
@@ -601,42 +635,56 @@ int emb_cache_import_rows(emb_cache_t h, int32_t table, int64_t row0, int64_t n,
   hipStream_t s = S(stream);
   const int d = h->cfg.dim, RB = h->plan.rec_bytes, bits = h->cfg.precision;
   const int64_t g0 = td.row_base + row0;
-  hipError_t e = hipSuccess;
-  std::vector<uint8_t> buf;
+  const bool ada = h->cfg.optimizer == EMB_OPT_ROWWISE_ADAGRAD;
   const uint8_t* codes = static_cast<const uint8_t*>(codes_in);
-  if (bits == EMB_FP16 && codes) {  // binary16 bit patterns as stored; scale and bias are not used
-    buf.assign((size_t)n * RB, 0);
-    for (int64_t i = 0; i < n; ++i) std::memcpy(buf.data() + i * RB, codes + i * d * 2, 2 * (size_t)d);
-    e = hipMemcpyAsync(h->dev.rec + g0 * RB, buf.data(), buf.size(), hipMemcpyDefault, s);
-  } else if (bits != EMB_FP16 && (codes || scale || bias)) {
-    if (!codes || !scale || !bias) return EMB_EINVAL;  // a record is written whole
+  const bool put_codes = bits == EMB_FP16 ? codes != nullptr : (codes || scale || bias);
+  if (bits != EMB_FP16 && put_codes && (!codes || !scale || !bias)) return EMB_EINVAL;  // codes and (s, b) go together
+  const bool put_acc = adagrad && ada;
+  hipError_t e = hipSuccess;
+  if (put_codes || put_acc) {
+    // the records as they are (what is not given stays), then the given parts
+    std::vector<uint8_t> buf((size_t)n * RB);
+    e = hipMemcpyAsync(buf.data(), h->dev.rec + g0 * RB, buf.size(), hipMemcpyDefault, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return EMB_EHIP;
     const int K = (1 << bits) - 1;
     const int cb = d * bits / 8;
-    const int per = 8 / bits;  // codes per byte, column j in bits (j % per) * bits
-    buf.assign((size_t)n * RB, 0);
     for (int64_t i = 0; i < n; ++i) {
       uint8_t* r = buf.data() + i * RB;
-      for (int j = 0; j < d; ++j) {
-        const uint8_t q = codes[i * d + j];
-        if (q > K) return EMB_EINVAL;
-        r[j / per] |= (uint8_t)(q << ((j % per) * bits));
+      if (put_codes && bits == EMB_FP16) {  // binary16 bit patterns as stored; scale and bias are not used
+        std::memcpy(r, codes + i * d * 2, 2 * (size_t)d);
+      } else if (put_codes) {
+        const int per = 8 / bits;  // codes per byte, column j in bits (j % per) * bits
+        std::memset(r, 0, (size_t)cb);
+        for (int j = 0; j < d; ++j) {
+          const uint8_t q = codes[i * d + j];
+          if (q > K) return EMB_EINVAL;
+          r[j / per] |= (uint8_t)(q << ((j % per) * bits));
+        }
+        if (h->cfg.sb_dtype == EMB_SB_FP16) {
+          const uint16_t hs = float_to_half_bits(scale[i]), hb = float_to_half_bits(bias[i]);
+          if (half_bits_to_float(hs) != scale[i] || half_bits_to_float(hb) != bias[i]) return EMB_EINVAL;
+          std::memcpy(r + cb, &hs, 2);
+          std::memcpy(r + cb + 2, &hb, 2);
+        } else {
+          std::memcpy(r + cb, &scale[i], 4);
+          std::memcpy(r + cb + 4, &bias[i], 4);
+        }
       }
-      if (h->cfg.sb_dtype == EMB_SB_FP16) {
-        const uint16_t hs = float_to_half_bits(scale[i]), hb = float_to_half_bits(bias[i]);
-        if (half_bits_to_float(hs) != scale[i] || half_bits_to_float(hb) != bias[i]) return EMB_EINVAL;
-        std::memcpy(r + cb, &hs, 2);
-        std::memcpy(r + cb + 2, &hb, 2);
-      } else {
-        std::memcpy(r + cb, &scale[i], 4);
-        std::memcpy(r + cb + 4, &bias[i], 4);
-      }
+      if (put_acc) std::memcpy(r + h->plan.acc_offset, &adagrad[i], 4);
     }
     e = hipMemcpyAsync(h->dev.rec + g0 * RB, buf.data(), buf.size(), hipMemcpyDefault, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);  // buf is released on return
+  }
+  if (e == hipSuccess && put_acc) {
+    // a cached row's accumulator is in the slot array
+    std::vector<std::pair<int64_t, int64_t>> cached;
+    e = cached_rows(h, table, row0, n, s, &cached);
+    for (size_t k = 0; e == hipSuccess && k < cached.size(); ++k)
+      e = hipMemcpyAsync(h->dev.acc_slot + cached[k].second, &adagrad[cached[k].first], 4, hipMemcpyHostToDevice, s);
   }
   if (e == hipSuccess && lfu_count && h->dev.cnt)
     e = hipMemcpyAsync(h->dev.cnt + g0, lfu_count, 4 * (size_t)n, hipMemcpyHostToDevice, s);
-  if (e == hipSuccess && adagrad && h->dev.G)
-    e = hipMemcpyAsync(h->dev.G + g0, adagrad, 4 * (size_t)n, hipMemcpyHostToDevice, s);
   if (e == hipSuccess) e = hipStreamSynchronize(s);
   return hip_status(e);
 }
@@ -679,8 +727,12 @@ int emb_cache_import_cache(emb_cache_t h, int32_t table, const float* rows, cons
   const int d = h->cfg.dim;
   hipError_t e = hipSuccess;
   if (rows) e = hipMemcpyAsync(h->dev.crow + td.slot_base * d, rows, 4 * (size_t)(slots * d), hipMemcpyHostToDevice, s);
+  // new residents: the accumulators of the rows leaving the cache go back to their
+  // records, those of the rows entering it come from theirs
+  if (e == hipSuccess && tags) e = embc::launch_move_acc(h->dev, td.slot_base, slots, td.row_base, true, s);
   if (e == hipSuccess && tags)
     e = hipMemcpyAsync(h->dev.tag + td.slot_base, tags, 4 * (size_t)slots, hipMemcpyHostToDevice, s);
+  if (e == hipSuccess && tags) e = embc::launch_move_acc(h->dev, td.slot_base, slots, td.row_base, false, s);
   if (e == hipSuccess && lru_stamp && h->dev.ts)
     e = hipMemcpyAsync(h->dev.ts + td.slot_base, lru_stamp, 4 * (size_t)slots, hipMemcpyHostToDevice, s);
   if (e == hipSuccess) e = hipStreamSynchronize(s);

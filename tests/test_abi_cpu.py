@@ -50,7 +50,7 @@ def test_query_sizes_named_configs(lib, name):
     L = 1 << 20
     s = ec.query_sizes(cfg, L)
     N = sum(cfg["rows"])
-    rec = cfg["dim"] * cfg["bits"] // 8 + (4 if cfg["sb_fp16"] else 8)
+    rec = record_layout(cfg["dim"], cfg["bits"], cfg["sb_fp16"], cfg["optimizer"] == "adagrad")
     assert s["row_bytes"] == rec and s["total_rows"] == N
     # the table is the last part of the state, padded to 256 bytes
     assert N * rec <= s["table_bytes"] < N * rec + 256 and s["table_bytes"] < s["state_bytes"]
@@ -58,15 +58,28 @@ def test_query_sizes_named_configs(lib, name):
     assert s["workspace_bytes"] >= 16 * L
 
 
-@pytest.mark.parametrize("bits,sb16,d,rec", [
-    (16, False, 16, 32), (16, True, 128, 256), (8, False, 16, 24), (4, True, 128, 68), (2, False, 16, 12),
-    (2, True, 256, 68),
+def record_layout(d, bits, sb16, adagrad):
+    base = d * bits // 8 + (0 if bits == 16 else 4 if sb16 else 8)
+    if not adagrad:
+        return base
+    a = min(base & -base, 16)
+    return (base + 4 + a - 1) // a * a
+
+
+@pytest.mark.parametrize("bits,sb16,d,opt,rec", [
+    (16, False, 16, "sgd", 32), (16, True, 128, "sgd", 256), (8, False, 16, "sgd", 24), (4, True, 128, "sgd", 68),
+    (2, False, 16, "sgd", 12), (2, True, 256, "sgd", 68),
+    (16, False, 16, "adagrad", 48), (16, True, 128, "adagrad", 272), (8, False, 16, "adagrad", 32),
+    (4, True, 128, "adagrad", 72), (2, False, 16, "adagrad", 16), (2, True, 256, "adagrad", 72),
+    (8, True, 16, "adagrad", 24), (8, False, 256, "adagrad", 272),
 ])
-def test_row_record_bytes(lib, bits, sb16, d, rec):
+def test_row_record_bytes(lib, bits, sb16, d, opt, rec):
     """Record = codes (d*bits/8 bytes) + (s, b) (8 bytes FP32, 4 FP16); an FP16 table
-    stores its elements alone."""
-    s = ec.query_sizes(custom_cfg(bits=bits, sb_fp16=sb16, dim=d), 1024)
+    stores its elements alone.  Under row-wise Adagrad the row's FP32 accumulator follows,
+    the record padded to the alignment of its first part (at most 16 bytes)."""
+    s = ec.query_sizes(custom_cfg(bits=bits, sb_fp16=sb16, dim=d, optimizer=opt), 1024)
     assert s["row_bytes"] == rec
+    assert rec == record_layout(d, bits, sb16, opt == "adagrad")
 
 
 @pytest.mark.parametrize("name,over", [
