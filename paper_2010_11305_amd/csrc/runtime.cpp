@@ -547,20 +547,19 @@ int emb_cache_check(emb_cache_t h, void* stream) {
 
 namespace {
 // Row-wise Adagrad: the accumulator of a cached row is in the slot array, not in its record.
-// (row - row0, global slot) of the rows of [row0, row0 + n) of `table` that are cached.
-hipError_t cached_rows(emb_cache_t h, int32_t table, int64_t row0, int64_t n, hipStream_t s,
-                       std::vector<std::pair<int64_t, int64_t>>* out) {
-  out->clear();
+// The tags and slot accumulators of `table` on the host (synchronizes s).
+hipError_t table_slots(emb_cache_t h, int32_t table, hipStream_t s, std::vector<int32_t>* tags,
+                       std::vector<float>* acc) {
   const TableDesc& td = h->plan.desc[table];
   const int64_t slots = td.n_sets * h->cfg.assoc;
+  tags->assign((size_t)slots, -1);
+  acc->assign((size_t)slots, 0.0f);
   if (slots == 0) return hipSuccess;
-  std::vector<int32_t> tags((size_t)slots);
-  hipError_t e = hipMemcpyAsync(tags.data(), h->dev.tag + td.slot_base, 4 * (size_t)slots, hipMemcpyDeviceToHost, s);
+  hipError_t e = hipMemcpyAsync(tags->data(), h->dev.tag + td.slot_base, 4 * (size_t)slots, hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(acc->data(), h->dev.acc_slot + td.slot_base, 4 * (size_t)slots, hipMemcpyDeviceToHost, s);
   if (e == hipSuccess) e = hipStreamSynchronize(s);
-  if (e != hipSuccess) return e;
-  for (int64_t i = 0; i < slots; ++i)
-    if (tags[i] >= row0 && tags[i] < row0 + n) out->emplace_back(tags[i] - row0, td.slot_base + i);
-  return hipSuccess;
+  return e;
 }
 }  // namespace
 
@@ -615,11 +614,12 @@ int emb_cache_export_rows(emb_cache_t h, int32_t table, int64_t row0, int64_t n,
     else std::memset(lfu_count, 0, 4 * (size_t)n);
   }
   if (adagrad && !ada) std::memset(adagrad, 0, 4 * (size_t)n);
-  if (adagrad && ada) {
-    std::vector<std::pair<int64_t, int64_t>> cached;
-    e = cached_rows(h, table, row0, n, s, &cached);
-    for (size_t k = 0; e == hipSuccess && k < cached.size(); ++k)
-      e = hipMemcpyAsync(&adagrad[cached[k].first], h->dev.acc_slot + cached[k].second, 4, hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess && adagrad && ada) {
+    std::vector<int32_t> tags;
+    std::vector<float> acc;
+    e = table_slots(h, table, s, &tags, &acc);
+    for (size_t i = 0; e == hipSuccess && i < tags.size(); ++i)
+      if (tags[i] >= row0 && tags[i] < row0 + n) adagrad[tags[i] - row0] = acc[i];
   }
   if (e == hipSuccess) e = hipStreamSynchronize(s);
   return hip_status(e);
@@ -678,10 +678,15 @@ int emb_cache_import_rows(emb_cache_t h, int32_t table, int64_t row0, int64_t n,
   }
   if (e == hipSuccess && put_acc) {
     // a cached row's accumulator is in the slot array
-    std::vector<std::pair<int64_t, int64_t>> cached;
-    e = cached_rows(h, table, row0, n, s, &cached);
-    for (size_t k = 0; e == hipSuccess && k < cached.size(); ++k)
-      e = hipMemcpyAsync(h->dev.acc_slot + cached[k].second, &adagrad[cached[k].first], 4, hipMemcpyHostToDevice, s);
+    std::vector<int32_t> tags;
+    std::vector<float> acc;
+    e = table_slots(h, table, s, &tags, &acc);
+    bool any = false;
+    for (size_t i = 0; e == hipSuccess && i < tags.size(); ++i)
+      if (tags[i] >= row0 && tags[i] < row0 + n) acc[i] = adagrad[tags[i] - row0], any = true;
+    if (e == hipSuccess && any)
+      e = hipMemcpyAsync(h->dev.acc_slot + td.slot_base, acc.data(), 4 * acc.size(), hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
   }
   if (e == hipSuccess && lfu_count && h->dev.cnt)
     e = hipMemcpyAsync(h->dev.cnt + g0, lfu_count, 4 * (size_t)n, hipMemcpyHostToDevice, s);

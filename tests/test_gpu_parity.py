@@ -410,6 +410,42 @@ def test_determinism_and_resume(torch):
     assert np.array_equal(g1.export_cache(0)["crow"], g3.export_cache(0)["crow"])
 
 
+@pytest.mark.parametrize("policy", ["lru", "lfu"])
+def test_adagrad_accumulators_follow_the_rows(torch, policy):
+    """A row's Adagrad accumulator lives in its record while the row is not cached and in
+    its cache slot's entry while it is.  Steps that insert and evict, then cache imports
+    that empty the cache and fill it again on a handle that holds residents: the
+    accumulators the rows export never change, and the next step still matches the
+    oracle bit for bit."""
+    cfg = custom_cfg(bits=4, sb_fp16=True, rounding="stochastic", policy=policy, optimizer="adagrad", assoc=4,
+                     **({"lfu_decay_interval": 2} if policy == "lfu" else {}))
+    log(f"accumulators follow the rows ({policy})")
+    o, g = make_pair(cfg)
+    for k in range(4):
+        step_both(o, g, cfg, workload.make_step(cfg, k), torch)
+    assert sum(g.stats(0)[f] for f in ("inserts", "evictions")) > 0
+    compare_state(o, g, cfg)
+    G0 = g.export_rows(0)["G"]
+    assert np.count_nonzero(G0) > 0
+    c = g.export_cache(0)
+    cached = c["tag"] >= 0
+    assert cached.sum() > 0 and np.count_nonzero(G0[c["tag"][cached]]) > 0
+    g.import_cache(0, np.zeros_like(c["crow"]), np.full_like(c["tag"], -1), np.full_like(c["ts"], -1))
+    assert np.array_equal(g.export_rows(0)["G"], G0)
+    g.import_cache(0, c["crow"], c["tag"], c["ts"])
+    assert np.array_equal(g.export_rows(0)["G"], G0)
+    # a row's accumulator written while it is cached, read back, then moved out and in
+    r = g.export_rows(0)
+    G1 = G0.copy()
+    G1[c["tag"][cached]] += 1.0
+    g.import_rows(0, 0, r["codes"], r["scale"], r["bias"], r["cnt"], G1)
+    assert np.array_equal(g.export_rows(0)["G"], G1)
+    g.import_rows(0, 0, r["codes"], r["scale"], r["bias"], r["cnt"], G0)
+    compare_state(o, g, cfg)
+    step_both(o, g, cfg, workload.make_step(cfg, 4), torch)
+    compare_state(o, g, cfg)
+
+
 def test_update_timing_events(torch):
     """The measurement events around the row-update kernel: one duration per timed call,
     and timing does not change results."""
