@@ -445,6 +445,24 @@ struct XcdSplit {
   __device__ int segments(int T) const { return T * parts; }
 };
 
+// Row groups over the segments an XCD handles in turn: a segment with at least as many
+// items as there are groups starts at group 0 (consecutive groups take consecutive
+// items), but a smaller one starts where the previous small segments left off, so that
+// small segments (small tables) spread over all groups instead of all landing on the
+// first ones, one after another.  Returns the group's first item offset in the segment
+// (>= n when it has none) and advances `carry` past the segment.
+// (carry stays below gstride; gx < gstride; 32-bit, no division, so that the per-lane cost
+// is one compare and a subtract)
+__device__ __forceinline__ int64_t spread_start(int64_t gx, int64_t gstride, int64_t n, int64_t& carry) {
+  if (n >= gstride) return gx;
+  const int32_t c = (int32_t)carry, gs = (int32_t)gstride;
+  int32_t s = (int32_t)gx + gs - c;
+  if (s >= gs) s -= gs;
+  carry += n;
+  if (carry >= gstride) carry -= gstride;
+  return s;
+}
+
 // [lo, hi) of `part` out of `parts` equal slices of [a, b).
 __device__ __forceinline__ void part_range(int64_t a, int64_t b, int part, int parts, int64_t& lo, int64_t& hi) {
   const int64_t n = b - a;

@@ -24,6 +24,7 @@ namespace embc {
 constexpr int32_t kActDone = 4;  // row fully handled by k_policy
 
 constexpr int kUnroll = 2;  // independent row loads in flight per row group
+constexpr int64_t kSpreadBelow = 1 << 21;  // lookups per step below which SPREAD kernels run
 
 // After the paired scan of the chunk counts and big-row flags: the chunk total, and the
 // big-row total, also as ubig[nU].
@@ -526,7 +527,7 @@ __global__ __launch_bounds__(256) void k_chunk_spans(Work w) {
   }
 }
 
-template <int D>
+template <int D, bool SPREAD>
 __global__ __launch_bounds__(256) void k_partials(Dev dv, Work w, const uint32_t* __restrict__ sval,
                                                   const float* __restrict__ grad) {
   // the gradient sums run beside the eviction on the second stream and decide when the
@@ -539,7 +540,8 @@ __global__ __launch_bounds__(256) void k_partials(Dev dv, Work w, const uint32_t
   const int64_t nU = (int64_t)w.ctr[kCUnique];
   if (nC == 0) return;
   const XcdSplit xs(dv.T);
-  const int64_t gx = xs.unit * GPB + threadIdx.x / LPR, gstride = xs.units * GPB;
+  const int64_t gx0 = xs.unit * GPB + threadIdx.x / LPR, gstride = xs.units * GPB;
+  int64_t carry = 0;
   for (int seg = xs.xcd; seg < xs.segments(dv.T); seg += kXcds) {
     const int t = seg / xs.parts;
     int64_t ulo, uhi;
@@ -548,6 +550,7 @@ __global__ __launch_bounds__(256) void k_partials(Dev dv, Work w, const uint32_t
     const int64_t chi_t = uhi < nU ? (int64_t)w.chunk_base[uhi] : nC;
     int64_t clo, chi;
     part_range(clo_t, chi_t, seg % xs.parts, xs.parts, clo, chi);
+    const int64_t gx = SPREAD ? spread_start(gx0, gstride, chi - clo, carry) : gx0;
     if (clo + gx >= chi) continue;
     const GradRows gr = grad_rows<D>(grad, t, dv.T);
     // the next chunk's span is loaded one chunk ahead (clamped index, unconditional load)
@@ -897,7 +900,9 @@ __global__ __launch_bounds__(256) void k_pack_meta(Work w, const uint32_t* __res
   }
 }
 
-template <int D, int BITS, bool SB16>
+// SPREAD: small steps (few rows per table), whose segments spread over all row groups
+// (spread_start); large steps keep the plain assignment, which needs fewer registers.
+template <int D, int BITS, bool SB16, bool SPREAD>
 __global__ __launch_bounds__(256) void k_update(Dev dv, Work w, const uint32_t* __restrict__ sval,
                                                 const float* __restrict__ grad, uint32_t step) {
   constexpr int LPR = Geo<D>::LPR;
@@ -905,7 +910,8 @@ __global__ __launch_bounds__(256) void k_update(Dev dv, Work w, const uint32_t* 
   const int g = threadIdx.x & (LPR - 1);
   const bool sr = dv.rounding != 0;
   const XcdSplit xs(dv.T, true);
-  const int64_t gx = xs.unit * GPB + threadIdx.x / LPR, gstride = xs.units * GPB;
+  const int64_t gx0 = xs.unit * GPB + threadIdx.x / LPR, gstride = xs.units * GPB;
+  int64_t carry = 0;
   for (int seg = xs.xcd; seg < xs.segments(dv.T); seg += kXcds) {
     const int t = seg / xs.parts;
     int64_t tlo, thi, lo, hi;
@@ -913,6 +919,7 @@ __global__ __launch_bounds__(256) void k_update(Dev dv, Work w, const uint32_t* 
     part_range(tlo, thi, seg % xs.parts, xs.parts, lo, hi);
     const TableDesc td = dv.desc[t];
     const GradRows gtab = grad_rows<D>(grad, t, dv.T);
+    const int64_t gx = SPREAD ? spread_start(gx0, gstride, hi - lo, carry) : gx0;
     if (lo + gx >= hi) continue;
     uint4 next = w.umeta[lo + gx];
     for (int64_t u = lo + gx; u < hi; u += gstride) {
@@ -1020,6 +1027,9 @@ hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int6
   const int nb_shift = __builtin_ctz((unsigned)(kBlockFloats / d.dim));
   const int stage_shift = nb_shift - __builtin_ctz((unsigned)kStages);
   const int nblk = (int)(((int64_t)B + (kBlockFloats / d.dim) - 1) / (kBlockFloats / d.dim));
+  // a small step spreads its tables' rows over all row groups (a larger one has more rows
+  // per table than groups anyway, and keeps the kernels with fewer registers)
+  const bool spread = L < kSpreadBelow;
   if (nblk > w.max_nblk) return hipErrorInvalidValue;
   if (nblk > 0) k_block_bounds<<<grid(k_block_bounds), 256, 0, s>>>(w, sv, stage_shift, nblk);
   return dispatch_row(d.dim, d.bits, d.sb16, [&]<int D, int BITS, bool SB16>() -> hipError_t {
@@ -1037,7 +1047,8 @@ hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int6
       e2 = hipEventRecord(side.join, side.s);
       if (e2 != hipSuccess) return e2;
     }
-    k_partials<D><<<grid(k_partials<D>), 256, 0, s>>>(d, w, sv, grad);
+    if (spread) k_partials<D, true><<<grid(k_partials<D, true>), 256, 0, s>>>(d, w, sv, grad);
+    else k_partials<D, false><<<grid(k_partials<D, false>), 256, 0, s>>>(d, w, sv, grad);
     if (nblk > 0) {
       k_block_partials<D><<<resident_grid(reinterpret_cast<const void*>(k_block_partials<D>), kBlockThreads),
                             kBlockThreads, 0, s>>>(d, w, sv, grad, B, nblk);
@@ -1053,7 +1064,8 @@ hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int6
       const hipError_t e2 = hipEventRecord(update_events[0], s);
       if (e2 != hipSuccess) return e2;
     }
-    k_update<D, BITS, SB16><<<grid(k_update<D, BITS, SB16>), 256, 0, s>>>(d, w, sv, grad, step);
+    if (spread) k_update<D, BITS, SB16, true><<<grid(k_update<D, BITS, SB16, true>), 256, 0, s>>>(d, w, sv, grad, step);
+    else k_update<D, BITS, SB16, false><<<grid(k_update<D, BITS, SB16, false>), 256, 0, s>>>(d, w, sv, grad, step);
     if (update_events) {
       const hipError_t e2 = hipEventRecord(update_events[1], s);
       if (e2 != hipSuccess) return e2;
