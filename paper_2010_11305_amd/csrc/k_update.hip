@@ -123,10 +123,53 @@ __device__ __forceinline__ GradRows<D> grad_rows(const float* grad, int t, int T
 // stream (i0 < i1), seeded with the first.  Lane j of the group preloads the bag of
 // occurrence j of each run of LPR occurrences (for the first run the caller may pass
 // them in, myv0); U rows are loaded before they are added in order.
+// Rows narrower than 16 lanes (d < 128) hold kRun/LPR bags per lane, so that a run (one
+// load of bags) covers kRun occurrences whatever the width, with kSmallUnroll rows in
+// flight; the order of the additions is the same.
+constexpr int kRun = 16;
+constexpr int kSmallUnroll = 8;
+
 template <int D>
 __device__ __forceinline__ void sum_occ(const uint32_t* __restrict__ sval, int64_t i0, int64_t i1, GradRows<D> gr,
                                         int g, float (&acc)[8], uint32_t myv0 = 0u, bool have0 = false) {
   constexpr int LPR = Geo<D>::LPR, CPL = 8, U = kUnroll;
+  if constexpr (LPR < kRun) {
+    constexpr int BPL = kRun / LPR, US = kSmallUnroll;
+    bool first = true;
+    for (int64_t ic = i0; ic < i1; ic += kRun) {
+      const int n = (int)min<int64_t>(kRun, i1 - ic);
+      // occurrence j of the run: bag myv[j / LPR] of lane j % LPR
+      uint32_t myv[BPL];
+#pragma unroll
+      for (int b = 0; b < BPL; ++b) {
+        const int64_t i = ic + b * LPR + g;
+        myv[b] = (b == 0 && have0 && ic == i0) ? myv0 : (i < i1 ? sval[i] : 0u);
+      }
+#pragma unroll
+      for (int j0 = 0; j0 < kRun; j0 += US) {
+        if (j0 >= n) break;
+        float x[US][CPL];
+#pragma unroll
+        for (int q = 0; q < US; ++q) {
+          const int j = j0 + q;
+          if (j < n) load_frow8(gr.row(__shfl(myv[j / LPR], j % LPR, LPR)), g, x[q]);
+        }
+#pragma unroll
+        for (int q = 0; q < US; ++q) {
+          if (j0 + q >= n) break;
+          if (first) {
+#pragma unroll
+            for (int k = 0; k < CPL; ++k) acc[k] = x[q][k];
+            first = false;
+          } else {
+#pragma unroll
+            for (int k = 0; k < CPL; ++k) acc[k] = acc[k] + x[q][k];
+          }
+        }
+      }
+    }
+    return;
+  }
   bool first = true;
   for (int64_t ic = i0; ic < i1; ic += LPR) {
     const int n = (int)min<int64_t>(LPR, i1 - ic);
@@ -172,6 +215,41 @@ __device__ __forceinline__ void chunk_sum(const uint32_t* __restrict__ sval, int
   // exactly that term, as in the seeded left-to-right sum (the chunk is not empty)
 #pragma unroll
   for (int k = 0; k < CPL; ++k) acc[k] = -0.0f;
+  if constexpr (LPR < kRun) {
+    // narrow rows: runs of kRun occurrences (kRun/LPR bags per lane), kSmallUnroll rows
+    // in flight, the next run's bags loaded while one is summed
+    constexpr int BPL = kRun / LPR, US = kSmallUnroll;
+    uint32_t vn[BPL];
+#pragma unroll
+    for (int b = 0; b < BPL; ++b) vn[b] = i0 + b * LPR + g < i1 ? sval[i0 + b * LPR + g] : 0u;
+    for (int64_t ic = i0; ic < i1; ic += kRun) {
+      const int n = (int)min<int64_t>(kRun, i1 - ic);
+      uint32_t myv[BPL];
+#pragma unroll
+      for (int b = 0; b < BPL; ++b) {
+        myv[b] = vn[b];
+        const int64_t i = ic + kRun + b * LPR + g;
+        vn[b] = i < i1 ? sval[i] : 0u;
+      }
+#pragma unroll
+      for (int j0 = 0; j0 < kRun; j0 += US) {
+        if (j0 >= n) break;
+        float x[US][CPL];
+#pragma unroll
+        for (int q = 0; q < US; ++q) {
+          const int j = j0 + q;
+          if (j < n) load_frow8(gr.row(__shfl(myv[j / LPR], j % LPR, LPR)), g, x[q]);
+        }
+#pragma unroll
+        for (int q = 0; q < US; ++q) {
+          if (j0 + q >= n) break;
+#pragma unroll
+          for (int k = 0; k < CPL; ++k) acc[k] = acc[k] + x[q][k];
+        }
+      }
+    }
+    return;
+  }
   uint32_t pv = 0xFFFFFFFFu;  // bag of the last occurrence added (none yet)
   float last[CPL];
 #pragma unroll
