@@ -122,7 +122,9 @@ typedef struct emb_cache_sizes {
   int64_t total_slots;    /* sum over tables of n_sets*assoc */
   int32_t row_bytes;      /* bytes of one low-precision row record: codes + scale + bias, then,
                              under row-wise Adagrad, the row's FP32 accumulator, padded to the
-                             alignment of the first part (at most 16 bytes) */
+                             alignment of the first part (at most 16 bytes) -- unless the record
+                             would then span one more 64-byte line (FP16 tables of dim >= 32),
+                             whose accumulators are kept apart */
   int32_t pad;
   size_t table_bytes;     /* the low-precision table: the last table_bytes of state_bytes */
 } emb_cache_sizes;

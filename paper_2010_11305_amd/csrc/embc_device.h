@@ -44,10 +44,11 @@ __device__ __forceinline__ uint8_t* rec_of(const Dev& dv, int64_t grow) {
   return static_cast<uint8_t*>(__builtin_assume_aligned(dv.rec + grow * dv.rec_bytes, Rec<D, BITS, SB16>::ALIGN));
 }
 
-// The row-wise Adagrad accumulator inside a record.
+// The row-wise Adagrad accumulator of uncached row grow (record rec): inside the record,
+// or in the per-row array when the records have no room for it.
 template <int D, int BITS, bool SB16>
-__device__ __forceinline__ float* acc_of(uint8_t* rec) {
-  return reinterpret_cast<float*>(rec + Rec<D, BITS, SB16>::BYTES);
+__device__ __forceinline__ float* acc_of(const Dev& dv, int64_t grow, uint8_t* rec) {
+  return dv.acc_rows ? dv.acc_rows + grow : reinterpret_cast<float*>(rec + Rec<D, BITS, SB16>::BYTES);
 }
 
 // ---- lane exchange inside a row group ---------------------------------------------------

@@ -5,10 +5,14 @@
 //                                   (INT4: two codes per byte, even column in the low nibble;
 //                                   scale/bias FP32 pair, or FP16 pair packed in one dword),
 //                                   then, under row-wise Adagrad, the row's FP32 accumulator
-//                                   while the row is not cached (a miss reads it with the codes)
+//                                   while the row is not cached (a miss reads it with the codes),
+//                                   unless that would make the record cross one more 64-byte line
+//                                   (FP16 tables): then it is in acc_rows
 //   crow  [total_slots][dim] FP32   cache rows; slot = slot_base[t] + set*assoc + way
 //   tag   [total_slots] int32       resident row id (table-local), -1 = empty way
 //   ts    [total_slots] int32       LRU: step of last access (-1 = empty); absent under LFU
+//   acc_rows [total_rows] FP32      row-wise Adagrad, accumulator not in the records: the
+//                                   accumulators of the rows not cached
 //   acc_slot [total_slots] FP32     row-wise Adagrad: the accumulator of the row cached in the
 //                                   slot (it moves between record and slot with the row); absent
 //                                   under SGD
@@ -80,6 +84,7 @@ struct Dev {
   int32_t* ts;
   int32_t* cnt;
   float* acc_slot;
+  float* acc_rows;    // nullptr when the accumulators of uncached rows are in the records
   const TableDesc* desc;
   const int64_t* key_base;       // [T+1], key_base[T] = total key space
   unsigned long long* stats;     // [T][kNStat]

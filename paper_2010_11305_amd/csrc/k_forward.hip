@@ -28,6 +28,7 @@ hipError_t launch_reset_state(const Dev& d, hipStream_t s) {
   if (e == hipSuccess && d.ts) e = launch_fill_u32(reinterpret_cast<uint32_t*>(d.ts), 0xFFFFFFFFu, d.total_slots, s);
   if (e == hipSuccess && d.cnt) e = launch_fill_u32(reinterpret_cast<uint32_t*>(d.cnt), 0u, d.total_rows, s);
   if (e == hipSuccess && d.acc_slot) e = launch_fill_u32(reinterpret_cast<uint32_t*>(d.acc_slot), 0u, d.total_slots, s);
+  if (e == hipSuccess && d.acc_rows) e = launch_fill_u32(reinterpret_cast<uint32_t*>(d.acc_rows), 0u, d.total_rows, s);
   if (e == hipSuccess) e = launch_fill_u32(reinterpret_cast<uint32_t*>(d.stats), 0u, (int64_t)d.T * kNStat * 2, s);
   if (e == hipSuccess) e = launch_fill_u32(reinterpret_cast<uint32_t*>(d.err), 0u, 1, s);
   return e;
@@ -61,7 +62,7 @@ __global__ __launch_bounds__(256) void k_init_uniform(Dev dv, float lo, float hi
     for (int i = 0; i < 8; ++i) x[i] = __builtin_fmaf(u[i], width, lo);
     uint8_t* rec = rec_of<D, BITS, SB16>(dv, grow);
     quantize_store<D, BITS, SB16>(x, g, rec, false, 0, 0, 0, 0);
-    if (dv.optimizer && g == 0) *acc_of<D, BITS, SB16>(rec) = 0.0f;
+    if (dv.optimizer && g == 0) *acc_of<D, BITS, SB16>(dv, grow, rec) = 0.0f;
   }
 }
 
@@ -72,7 +73,8 @@ __global__ __launch_bounds__(256) void k_move_acc(Dev dv, int64_t s0, int64_t n,
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
     const int32_t r = dv.tag[s0 + i];
     if (r < 0) continue;
-    float* a = reinterpret_cast<float*>(dv.rec + (row_base + r) * dv.rec_bytes + dv.acc_offset);
+    float* a = dv.acc_rows ? dv.acc_rows + row_base + r
+                           : reinterpret_cast<float*>(dv.rec + (row_base + r) * dv.rec_bytes + dv.acc_offset);
     if (to_rec) *a = dv.acc_slot[s0 + i];
     else dv.acc_slot[s0 + i] = *a;
   }
@@ -90,6 +92,7 @@ hipError_t launch_init_uniform(const Dev& d, float lo, float hi, uint64_t init_s
   if (e == hipSuccess) e = launch_fill_u32(reinterpret_cast<uint32_t*>(d.crow), 0u, d.total_slots * d.dim, s);
   if (e == hipSuccess && d.cnt) e = launch_fill_u32(reinterpret_cast<uint32_t*>(d.cnt), 0u, d.total_rows, s);
   if (e == hipSuccess && d.acc_slot) e = launch_fill_u32(reinterpret_cast<uint32_t*>(d.acc_slot), 0u, d.total_slots, s);
+  if (e == hipSuccess && d.acc_rows) e = launch_fill_u32(reinterpret_cast<uint32_t*>(d.acc_rows), 0u, d.total_rows, s);
   if (e != hipSuccess) return e;
   return dispatch_row(d.dim, d.bits, d.sb16, [&]<int D, int BITS, bool SB16>() -> hipError_t {
     const int64_t threads = d.total_rows * Geo<D>::LPR;

@@ -935,7 +935,7 @@ __global__ __launch_bounds__(256) void k_evict(Dev dv, Work w, const uint32_t* _
         load_frow8_nt(dv.crow + (int64_t)e_dst * D, g, xv);
         // the displaced row's accumulator leaves the slot for its record (before the
         // insert that takes the slot writes its own there)
-        float* acc = dv.optimizer ? acc_of<D, BITS, SB16>(vrec) : nullptr;
+        float* acc = dv.optimizer ? acc_of<D, BITS, SB16>(dv, vgrow, vrec) : nullptr;
         if (UPDATED) {
           // the displaced resident was updated this step (LFU): its new value goes to T
           const float Gv = dv.optimizer ? dv.acc_slot[e_dst] : 0.0f;
@@ -1015,7 +1015,7 @@ __global__ __launch_bounds__(256) void k_update(Dev dv, Work w, const uint32_t* 
       float* acc = nullptr;
       float* acc_out = nullptr;
       if (dv.optimizer) {
-        acc = hit ? dv.acc_slot + (int32_t)m.y : acc_of<D, BITS, SB16>(rec);
+        acc = hit ? dv.acc_slot + (int32_t)m.y : acc_of<D, BITS, SB16>(dv, grow, rec);
         acc_out = kind == kKindBypass ? acc : dv.acc_slot + (int32_t)m.y;
       }
       const bool big = n > kBlockAbove;

@@ -79,10 +79,11 @@ struct Plan {
   int64_t total_rows = 0, total_slots = 0, total_keys = 0;
   int rec_bytes = 0;
   int acc_offset = 0;  // byte of the Adagrad accumulator in a record (under row-wise Adagrad)
+  bool acc_in_rec = false;  // the accumulators of uncached rows are in the records (else acc_rows)
   std::vector<TableDesc> desc;
   std::vector<int64_t> key_base;
   // state offsets
-  size_t o_rec, o_crow, o_tag, o_ts, o_cnt, o_accs, o_desc, o_keyb, o_stats, o_err, state_bytes, table_bytes;
+  size_t o_rec, o_crow, o_tag, o_ts, o_cnt, o_accs, o_accr, o_desc, o_keyb, o_stats, o_err, state_bytes, table_bytes;
   // workspace offsets
   size_t o_kA, o_vA, o_kB, o_vB, o_ssmall, o_sst0, o_sst1, o_sseg, o_part, o_tcnt, o_tpre, o_tthr, o_uk, o_seg, o_setf, o_urow, o_utab, o_uslot,
       o_uact, o_udest, o_umeta, o_ukey, o_nch, o_cbase, o_uvrow, o_uvu, o_partial, o_span, o_ubig, o_brows, o_bbound, o_bpart, o_tabf, o_src, o_ctr, ws_bytes;
@@ -146,12 +147,17 @@ int plan_config(const emb_cache_config* c, Plan* p) {
   p->total_keys = keys;
   // an FP16 table stores the elements alone; integer codes carry (s, b); under row-wise
   // Adagrad the row's FP32 accumulator follows, the record padded to the alignment of
-  // its first part (at most 16 bytes), as Rec<> in the kernels lays it out
+  // its first part (at most 16 bytes), as Rec<> in the kernels lays it out -- unless
+  // the record would then span one more 64-byte line than without it (an FP16 table of
+  // d >= 32: its records fill whole lines), when the accumulators get an array of their own
   p->acc_offset = c->dim * c->precision / 8 + (c->precision == EMB_FP16 ? 0 : c->sb_dtype == EMB_SB_FP16 ? 4 : 8);
   p->rec_bytes = p->acc_offset;
+  p->acc_in_rec = false;
   if (c->optimizer == EMB_OPT_ROWWISE_ADAGRAD) {
     const int a = std::min(p->acc_offset & -p->acc_offset, 16);
-    p->rec_bytes = (p->acc_offset + 4 + a - 1) / a * a;
+    const int with = (p->acc_offset + 4 + a - 1) / a * a;
+    p->acc_in_rec = (with + 63) / 64 <= (p->acc_offset + 63) / 64;
+    if (p->acc_in_rec) p->rec_bytes = with;
   }
 
   size_t o = 0;
@@ -166,6 +172,7 @@ int plan_config(const emb_cache_config* c, Plan* p) {
   p->o_ts = take(lru ? (size_t)slots * 4 : 0);
   p->o_cnt = take(lfu ? (size_t)rows * 4 : 0);
   p->o_accs = take(c->optimizer == EMB_OPT_ROWWISE_ADAGRAD ? (size_t)slots * 4 : 0);
+  p->o_accr = take(c->optimizer == EMB_OPT_ROWWISE_ADAGRAD && !p->acc_in_rec ? (size_t)rows * 4 : 0);
   p->o_desc = take(sizeof(TableDesc) * T);
   p->o_keyb = take(sizeof(int64_t) * (T + 1));
   p->o_stats = take(sizeof(unsigned long long) * T * embc::kNStat);
@@ -387,6 +394,8 @@ int create_impl(const emb_cache_config* cfg, void* state, size_t state_bytes, vo
   d.ts = cfg->policy == EMB_LRU ? reinterpret_cast<int32_t*>(sb + p.o_ts) : nullptr;
   d.cnt = cfg->policy == EMB_LFU ? reinterpret_cast<int32_t*>(sb + p.o_cnt) : nullptr;
   d.acc_slot = cfg->optimizer == EMB_OPT_ROWWISE_ADAGRAD ? reinterpret_cast<float*>(sb + p.o_accs) : nullptr;
+  d.acc_rows = cfg->optimizer == EMB_OPT_ROWWISE_ADAGRAD && !p.acc_in_rec ? reinterpret_cast<float*>(sb + p.o_accr)
+                                                                          : nullptr;
   d.desc = reinterpret_cast<const TableDesc*>(sb + p.o_desc);
   d.key_base = reinterpret_cast<const int64_t*>(sb + p.o_keyb);
   d.stats = reinterpret_cast<unsigned long long*>(sb + p.o_stats);
@@ -573,8 +582,11 @@ int emb_cache_export_rows(emb_cache_t h, int32_t table, int64_t row0, int64_t n,
   const int d = h->cfg.dim, RB = h->plan.rec_bytes, bits = h->cfg.precision;
   const int64_t g0 = td.row_base + row0;
   const bool ada = h->cfg.optimizer == EMB_OPT_ROWWISE_ADAGRAD;
+  const bool acc_rec = ada && h->plan.acc_in_rec;
   hipError_t e = hipSuccess;
-  if (codes_out || scale || bias || (adagrad && ada)) {
+  if (adagrad && ada && !acc_rec)
+    e = hipMemcpyAsync(adagrad, h->dev.acc_rows + g0, 4 * (size_t)n, hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess && (codes_out || scale || bias || (adagrad && acc_rec))) {
     std::vector<uint8_t> buf((size_t)n * RB);
     e = hipMemcpyAsync(buf.data(), h->dev.rec + g0 * RB, buf.size(), hipMemcpyDefault, s);  // device or pinned host table
     if (e == hipSuccess) e = hipStreamSynchronize(s);
@@ -583,7 +595,7 @@ int emb_cache_export_rows(emb_cache_t h, int32_t table, int64_t row0, int64_t n,
     uint8_t* codes = static_cast<uint8_t*>(codes_out);
     for (int64_t i = 0; i < n; ++i) {
       const uint8_t* r = buf.data() + i * RB;
-      if (adagrad && ada) std::memcpy(&adagrad[i], r + h->plan.acc_offset, 4);
+      if (adagrad && acc_rec) std::memcpy(&adagrad[i], r + h->plan.acc_offset, 4);
       if (bits == EMB_FP16) {  // binary16 bit patterns as stored, no (s, b)
         if (codes) std::memcpy(codes + i * d * 2, r, 2 * (size_t)d);
         if (scale) scale[i] = 0.0f;
@@ -640,8 +652,11 @@ int emb_cache_import_rows(emb_cache_t h, int32_t table, int64_t row0, int64_t n,
   const bool put_codes = bits == EMB_FP16 ? codes != nullptr : (codes || scale || bias);
   if (bits != EMB_FP16 && put_codes && (!codes || !scale || !bias)) return EMB_EINVAL;  // codes and (s, b) go together
   const bool put_acc = adagrad && ada;
+  const bool acc_rec = ada && h->plan.acc_in_rec;
   hipError_t e = hipSuccess;
-  if (put_codes || put_acc) {
+  if (put_acc && !acc_rec)
+    e = hipMemcpyAsync(h->dev.acc_rows + g0, adagrad, 4 * (size_t)n, hipMemcpyHostToDevice, s);
+  if (e == hipSuccess && (put_codes || (put_acc && acc_rec))) {
     // the records as they are (what is not given stays), then the given parts
     std::vector<uint8_t> buf((size_t)n * RB);
     e = hipMemcpyAsync(buf.data(), h->dev.rec + g0 * RB, buf.size(), hipMemcpyDefault, s);
@@ -671,7 +686,7 @@ int emb_cache_import_rows(emb_cache_t h, int32_t table, int64_t row0, int64_t n,
           std::memcpy(r + cb + 4, &bias[i], 4);
         }
       }
-      if (put_acc) std::memcpy(r + h->plan.acc_offset, &adagrad[i], 4);
+      if (put_acc && acc_rec) std::memcpy(r + h->plan.acc_offset, &adagrad[i], 4);
     }
     e = hipMemcpyAsync(h->dev.rec + g0 * RB, buf.data(), buf.size(), hipMemcpyDefault, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);  // buf is released on return
