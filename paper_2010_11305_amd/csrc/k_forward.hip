@@ -2,6 +2,7 @@
 // pooled[b][t] = sum over the bag of fetch(T_t, C_t, i) (Sec. 3 fetch operator).
 #include <map>
 #include <mutex>
+#include <type_traits>
 
 #include "emb_cache.h"
 #include "embc_device.h"
@@ -111,20 +112,20 @@ hipError_t launch_init_uniform(const Dev& d, float lo, float hi, uint64_t init_s
 // valid lookup gives +0.
 constexpr int kFwdUnroll = 2;
 
-#ifndef EMBC_PROBE_PU
-#define EMBC_PROBE_PU 4
-#endif
-constexpr int kProbeUnroll = EMBC_PROBE_PU;  // lookups in flight per lane group of the probe
+// Lookups in flight per lane group of the probe (PU).  On a large step 6 (96 tags per
+// lane, 2 waves per SIMD) is faster than 4 at 4 waves (355 -> 332 us on the industrial
+// workload; 8: 334 us, 12: 531 us); a step of few lookups wants the waves instead.
+constexpr int kProbeUnroll = 6, kProbeUnrollSmall = 4;
+constexpr int64_t kProbeSmallBelow = 1 << 21;  // lookups per call
 
 // QL = assoc/W lanes share one lookup (one lane up to 16 ways, W = min(assoc, 16)), each
 // comparing W of the set's tags loaded 16 bytes at a time; every lane group keeps
-// kProbeUnroll lookups in flight (all index loads, then all tag loads).  One lane per
-// lookup pays the set index, the addressing and the store of a lookup once.
-template <int W>
+// PU lookups in flight (all index loads, then all tag loads).  One lane per lookup pays
+// the set index, the addressing and the store of a lookup once.
+template <int W, int PU>
 __global__ __launch_bounds__(256) void k_fwd_probe(Dev dv, const int32_t* __restrict__ idx, int64_t L,
                                                    const int32_t* __restrict__ off, int32_t B,
                                                    int32_t* __restrict__ src) {
-  constexpr int PU = kProbeUnroll;
   const XcdSplit xs(dv.T);
   const int64_t tid = xs.unit * blockDim.x + threadIdx.x, stride = xs.units * blockDim.x;
   if (blockIdx.x == 0) {
@@ -343,14 +344,20 @@ hipError_t launch_forward(const Dev& d, const Work& w, const int32_t* idx, int64
     const auto probe = [&](auto kernel) {
       kernel<<<resident_grid(reinterpret_cast<const void*>(kernel)), 256, 0, s>>>(d, idx, L, off, B, w.fwd_src);
     };
-    switch (d.assoc < 16 ? d.assoc : 16) {
-      case 1: probe(k_fwd_probe<1>); break;
-      case 2: probe(k_fwd_probe<2>); break;
-      case 4: probe(k_fwd_probe<4>); break;
-      case 8: probe(k_fwd_probe<8>); break;
-      case 16: probe(k_fwd_probe<16>); break;
-      default: return hipErrorInvalidValue;
-    }
+    const auto probe_w = [&](auto pu) {
+      constexpr int PU = decltype(pu)::value;
+      switch (d.assoc < 16 ? d.assoc : 16) {
+        case 1: probe(k_fwd_probe<1, PU>); return hipSuccess;
+        case 2: probe(k_fwd_probe<2, PU>); return hipSuccess;
+        case 4: probe(k_fwd_probe<4, PU>); return hipSuccess;
+        case 8: probe(k_fwd_probe<8, PU>); return hipSuccess;
+        case 16: probe(k_fwd_probe<16, PU>); return hipSuccess;
+        default: return hipErrorInvalidValue;
+      }
+    };
+    const hipError_t e = L < kProbeSmallBelow ? probe_w(std::integral_constant<int, kProbeUnrollSmall>{})
+                                              : probe_w(std::integral_constant<int, kProbeUnroll>{});
+    if (e != hipSuccess) return e;
   }
   return dispatch_row(d.dim, d.bits, d.sb16, [&]<int D, int BITS, bool SB16>() -> hipError_t {
     // whole multiples of 8 workgroups (one per XCD), at most the resident count
