@@ -119,6 +119,28 @@ hipError_t scan_exclusive(const T* in, T* out, int64_t n, const unsigned long lo
   return hipGetLastError();
 }
 
+// kScanItems consecutive values of a and b from element base (0 past n); whole runs are
+// read 16 bytes at a time (the arrays are 16-byte aligned and base is a multiple of 8).
+__device__ __forceinline__ void load_pair_items(const uint32_t* a, const uint32_t* b, int64_t n, int64_t base,
+                                                uint32_t (&va)[kScanItems], uint32_t (&vb)[kScanItems]) {
+  static_assert(kScanItems % 4 == 0, "runs of 16 bytes");
+  if (base + kScanItems <= n) {
+#pragma unroll
+    for (int i = 0; i < kScanItems; i += 4) {
+      const uint4 x = *reinterpret_cast<const uint4*>(a + base + i);
+      const uint4 y = *reinterpret_cast<const uint4*>(b + base + i);
+      va[i] = x.x; va[i + 1] = x.y; va[i + 2] = x.z; va[i + 3] = x.w;
+      vb[i] = y.x; vb[i + 1] = y.y; vb[i + 2] = y.z; vb[i + 3] = y.w;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < kScanItems; ++i) {
+      va[i] = base + i < n ? a[base + i] : 0u;
+      vb[i] = base + i < n ? b[base + i] : 0u;
+    }
+  }
+}
+
 // Exclusive scans of two u32 arrays at once (a + b * 2^32 as one u64 value per element:
 // the prefix sums of a stay below 2^32), written to out_a and out_b (which may be a and
 // b); *total = the two totals packed the same way.
@@ -130,10 +152,11 @@ __global__ __launch_bounds__(kScanThreads) void k_scan2_reduce(const uint32_t* _
   if (dev_n) n = min(n, (int64_t)*dev_n);
   if ((int64_t)blockIdx.x * kScanTile >= n) return;
   const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
+  uint32_t va[kScanItems], vb[kScanItems];
+  load_pair_items(a, b, n, base, va, vb);
   unsigned long long s = 0;
 #pragma unroll
-  for (int i = 0; i < kScanItems; ++i)
-    if (base + i < n) s += (unsigned long long)a[base + i] | ((unsigned long long)b[base + i] << 32);
+  for (int i = 0; i < kScanItems; ++i) s += (unsigned long long)va[i] | ((unsigned long long)vb[i] << 32);
   unsigned long long tot;
   block_exclusive_scan<unsigned long long>(s, lds4, tot);
   if (threadIdx.x == 0) part[blockIdx.x] = tot;
@@ -147,22 +170,34 @@ __global__ __launch_bounds__(kScanThreads) void k_scan2_down(const uint32_t* a, 
   if (dev_n) n = min(n, (int64_t)*dev_n);
   if ((int64_t)blockIdx.x * kScanTile >= n) return;
   const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
-  unsigned long long v[kScanItems];
+  uint32_t va[kScanItems], vb[kScanItems];
+  load_pair_items(a, b, n, base, va, vb);
   unsigned long long s = 0;
 #pragma unroll
-  for (int i = 0; i < kScanItems; ++i) {
-    v[i] = base + i < n ? ((unsigned long long)a[base + i] | ((unsigned long long)b[base + i] << 32)) : 0ull;
-    s += v[i];
-  }
+  for (int i = 0; i < kScanItems; ++i) s += (unsigned long long)va[i] | ((unsigned long long)vb[i] << 32);
   unsigned long long tot;
   unsigned long long run = block_exclusive_scan<unsigned long long>(s, lds4, tot) + part[blockIdx.x];
+  // the exclusive prefixes replace the values in place (va, vb)
 #pragma unroll
   for (int i = 0; i < kScanItems; ++i) {
-    if (base + i < n) {
-      out_a[base + i] = (uint32_t)run;
-      out_b[base + i] = (uint32_t)(run >> 32);
+    const unsigned long long v = (unsigned long long)va[i] | ((unsigned long long)vb[i] << 32);
+    va[i] = (uint32_t)run;
+    vb[i] = (uint32_t)(run >> 32);
+    run += v;
+  }
+  if (base + kScanItems <= n) {
+#pragma unroll
+    for (int i = 0; i < kScanItems; i += 4) {
+      *reinterpret_cast<uint4*>(out_a + base + i) = make_uint4(va[i], va[i + 1], va[i + 2], va[i + 3]);
+      *reinterpret_cast<uint4*>(out_b + base + i) = make_uint4(vb[i], vb[i + 1], vb[i + 2], vb[i + 3]);
     }
-    run += v[i];
+  } else {
+#pragma unroll
+    for (int i = 0; i < kScanItems; ++i)
+      if (base + i < n) {
+        out_a[base + i] = va[i];
+        out_b[base + i] = vb[i];
+      }
   }
 }
 
@@ -698,49 +733,54 @@ __global__ __launch_bounds__(256) void k_expand(Dev dv, const int32_t* __restric
     // one high multiply; the descriptor of the wave's first table is loaded once
     const int t_run = (int)div_by((uint32_t)bag0, byB);
     const TableDesc td_run = dv.desc[t_run];
-    for (int64_t pc = P0; pc < P1; pc += 64) {
-      const int64_t p = pc + lane;
-      const bool in = p < P1;
-      const int32_t r = in ? idx[p] : 0;  // in flight during the search
-      // largest lane j with start_j <= p
-      int j = 0;
+    const auto handle = [&](int64_t p, int32_t r, int j) {
+      const uint32_t bag = (uint32_t)(bag0 + j);
+      const int t = (int)div_by(bag, byB);
+      const int b = (int)(bag - (uint32_t)t * (uint32_t)B);
+      const TableDesc td = t == t_run ? td_run : dv.desc[t];
+      uint32_t key = kKeyInvalid;
+      if (r >= 0 && (int64_t)r < td.N) {
+        if (td.n_sets > 0) {
+          const uint32_t q = div_by((uint32_t)r, td.by_sets);
+          const uint32_t set = (uint32_t)r - q * (uint32_t)td.n_sets;
+          key = (uint32_t)(td.key_base + (int64_t)set * td.Q + q);
+        } else {
+          key = (uint32_t)(td.key_base + r);
+        }
+        if (t == t_run) ++n_ok; else atomicAdd(&dv.stats[(int64_t)t * kNStat + kStBwdLookups], 1ull);
+      } else {
+        if (t == t_run) ++n_bad; else atomicAdd(&dv.stats[(int64_t)t * kNStat + kStInvalidBwd], 1ull);
+        atomicOr(dv.err, kErrIndex);
+      }
+      keys[p] = key;
+      vals[p] = (uint32_t)b;
+      if constexpr (SEG) {
+        n_skip += key == kKeyInvalid;
+        if (t == t_wg) {
+          for (int q = 0; q < eh.passes; ++q) atomicAdd(&h[q * 256 + seg_digit(key, kb_wg, 8 * q)], 1u);
+        } else {
+          const uint32_t kb = (uint32_t)eh.key_base[t];
+          uint32_t* ht = eh.hist + (int64_t)t * kMaxPasses * 256;
+          for (int q = 0; q < eh.passes; ++q) atomicAdd(&ht[q * 256 + seg_digit(key, kb, 8 * q)], 1u);
+        }
+      }
+    };
+    // two runs of 64 positions at a time: their index loads and bag searches interleave
+    for (int64_t pc = P0; pc < P1; pc += 128) {
+      const int64_t pA = pc + lane, pB = pc + 64 + lane;
+      const bool inA = pA < P1, inB = pB < P1;
+      const int32_t rA = inA ? idx[pA] : 0;
+      const int32_t rB = inB ? idx[pB] : 0;
+      int jA = 0, jB = 0;
 #pragma unroll
       for (int step = 32; step >= 1; step >>= 1) {
-        const int64_t s2 = __shfl(st, j + step);
-        if (j + step < 64 && s2 <= p) j += step;
+        const int64_t sA = __shfl(st, jA + step);
+        const int64_t sB = __shfl(st, jB + step);
+        if (jA + step < 64 && sA <= pA) jA += step;
+        if (jB + step < 64 && sB <= pB) jB += step;
       }
-      if (in) {
-        const uint32_t bag = (uint32_t)(bag0 + j);
-        const int t = (int)div_by(bag, byB);
-        const int b = (int)(bag - (uint32_t)t * (uint32_t)B);
-        const TableDesc td = t == t_run ? td_run : dv.desc[t];
-        uint32_t key = kKeyInvalid;
-        if (r >= 0 && (int64_t)r < td.N) {
-          if (td.n_sets > 0) {
-            const uint32_t q = div_by((uint32_t)r, td.by_sets);
-            const uint32_t set = (uint32_t)r - q * (uint32_t)td.n_sets;
-            key = (uint32_t)(td.key_base + (int64_t)set * td.Q + q);
-          } else {
-            key = (uint32_t)(td.key_base + r);
-          }
-          if (t == t_run) ++n_ok; else atomicAdd(&dv.stats[(int64_t)t * kNStat + kStBwdLookups], 1ull);
-        } else {
-          if (t == t_run) ++n_bad; else atomicAdd(&dv.stats[(int64_t)t * kNStat + kStInvalidBwd], 1ull);
-          atomicOr(dv.err, kErrIndex);
-        }
-        keys[p] = key;
-        vals[p] = (uint32_t)b;
-        if constexpr (SEG) {
-          n_skip += key == kKeyInvalid;
-          if (t == t_wg) {
-            for (int q = 0; q < eh.passes; ++q) atomicAdd(&h[q * 256 + seg_digit(key, kb_wg, 8 * q)], 1u);
-          } else {
-            const uint32_t kb = (uint32_t)eh.key_base[t];
-            uint32_t* ht = eh.hist + (int64_t)t * kMaxPasses * 256;
-            for (int q = 0; q < eh.passes; ++q) atomicAdd(&ht[q * 256 + seg_digit(key, kb, 8 * q)], 1u);
-          }
-        }
-      }
+      if (inA) handle(pA, rA, jA);
+      if (inB) handle(pB, rB, jB);
     }
     // lookups of the wave's first table: one atomic per wave
 #pragma unroll

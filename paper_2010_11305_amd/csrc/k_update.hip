@@ -566,26 +566,40 @@ __device__ __forceinline__ void table_rows(const Work& w, int t, int64_t& lo, in
 // Also the statistics that follow from those ranges: the unique rows of each table, and,
 // for a table without a cache, its bypasses (every row).  (Unique hits are counted by
 // k_policy, inserts and the other bypasses too.)
-__device__ __forceinline__ int64_t first_row_of_table(const Work& w, int64_t nU, int t) {
-  int64_t a = 0, b = nU;
+// The first unique row with table >= t (rows are sorted table-major), searched by a whole
+// wave: each round, lane l tests the l-th of 64 points spread over the remaining range,
+// which shrinks 64-fold (4 dependent loads for 5M unique rows instead of 23 for a binary
+// search).  Wave-uniform; every lane returns the result.
+__device__ __forceinline__ int64_t first_row_of_table_wave(const Work& w, int64_t nU, int t) {
+  const int lane = threadIdx.x & 63;
+  int64_t a = 0, b = nU;  // the row lies in [a, b] (b: there is none)
   while (a < b) {
-    const int64_t m = (a + b) >> 1;
-    if (w.utab[m] < t) a = m + 1; else b = m;
+    const int64_t step = (b - a + 63) / 64;
+    const int64_t m = a + (int64_t)lane * step;
+    const uint64_t ge = __ballot(m >= b || w.utab[m] >= t);
+    const int f = ge ? (int)__builtin_ctzll(ge) : 64;  // first probe at or past the row
+    if (f == 0) break;  // the row is a
+    const int64_t prev = a + (int64_t)(f - 1) * step;
+    if (f < 64) b = min<int64_t>(b, a + (int64_t)f * step);
+    a = prev + 1;
   }
   return a;
 }
 
-__global__ void k_tab_first(Dev dv, Work w, int T) {
+// One wave per table boundary t = 0 .. T.
+__global__ __launch_bounds__(256) void k_tab_first(Dev dv, Work w, int T) {
   const int64_t nU = (int64_t)w.ctr[kCUnique];
-  for (int t = blockIdx.x * blockDim.x + threadIdx.x; t <= T; t += gridDim.x * blockDim.x) {
-    const int64_t lo = first_row_of_table(w, nU, t);
-    w.tab_first[t] = (int32_t)lo;
-    if (t < T) {
-      const int64_t n = first_row_of_table(w, nU, t + 1) - lo;
-      unsigned long long* st = dv.stats + (int64_t)t * kNStat;
-      st[kStUnique] = (unsigned long long)n;
-      if (dv.desc[t].n_sets == 0) st[kStBypasses] = (unsigned long long)n;
-    }
+  const int t = (int)(((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6);
+  if (t > T) return;  // whole waves
+  const int64_t lo = first_row_of_table_wave(w, nU, t);
+  const int64_t hi = t < T ? first_row_of_table_wave(w, nU, t + 1) : nU;
+  if ((threadIdx.x & 63) != 0) return;
+  w.tab_first[t] = (int32_t)lo;
+  if (t < T) {
+    const int64_t n = hi - lo;
+    unsigned long long* st = dv.stats + (int64_t)t * kNStat;
+    st[kStUnique] = (unsigned long long)n;
+    if (dv.desc[t].n_sets == 0) st[kStBypasses] = (unsigned long long)n;
   }
 }
 
@@ -1098,7 +1112,7 @@ hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int6
   if (e != hipSuccess) return e;
   const auto grid = [](auto kernel) { return resident_grid(reinterpret_cast<const void*>(kernel)); };
   k_probe<<<grid(k_probe), 256, 0, s>>>(d, w, step);
-  k_tab_first<<<(d.T + 256) / 256, 256, 0, s>>>(d, w, d.T);
+  k_tab_first<<<(unsigned)((64 * (int64_t)(d.T + 1) + 255) / 256), 256, 0, s>>>(d, w, d.T);
   e = scan_exclusive_pair(w.nch, w.ubig, w.chunk_base, w.ubig, L, w.ctr + kCUnique, w.part, w.ctr + kCScanTotal, s);
   if (e != hipSuccess) return e;
   k_scan_totals<<<1, 1, 0, s>>>(w);
