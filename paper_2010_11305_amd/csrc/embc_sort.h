@@ -80,8 +80,8 @@ hipError_t launch_expand(const Dev& dv, const int32_t* idx, int64_t L, const int
 // the first unique row of each touched set (tile_cnt / tile_pre: uniq_tile_words(n) words each).
 // thread_pre: 256 words per tile, each thread's offset inside its tile.
 hipError_t launch_unique(const Dev& dv, const uint32_t* sk, int64_t n, unsigned long long* tile_cnt,
-                         unsigned long long* tile_pre, unsigned long long* thread_pre, unsigned long long* part,
-                         uint32_t* uk, uint32_t* seg, uint32_t* set_first, int32_t* utab, unsigned long long* ctr,
+                         unsigned long long* tile_pre, unsigned long long* thread_pre, uint32_t* uk, uint32_t* seg,
+                         uint32_t* set_first, int32_t* utab, unsigned long long* ctr,
                          hipStream_t s);
 
 }  // namespace embc

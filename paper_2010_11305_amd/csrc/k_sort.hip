@@ -63,23 +63,47 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_reduce(const T* __restric
   if (threadIdx.x == 0) part[blockIdx.x] = tot;
 }
 
+// Exclusive scan of in[0, nb) into out (which may be in) by one block of kScanThreads,
+// kTopItems consecutive values per thread and round; *total_out = the sum.
+constexpr int kTopItems = 16;
+template <typename T>
+__device__ __forceinline__ void scan_one_block(const T* in, T* out, int64_t nb, T* total_out) {
+  __shared__ T lds4[4];
+  T carry = 0;
+  for (int64_t b0 = 0; b0 < nb; b0 += (int64_t)kScanThreads * kTopItems) {
+    const int64_t base = b0 + (int64_t)threadIdx.x * kTopItems;
+    T v[kTopItems];
+    T s = 0;
+#pragma unroll
+    for (int q = 0; q < kTopItems; ++q) {
+      v[q] = base + q < nb ? in[base + q] : (T)0;
+      s += v[q];
+    }
+    T tot;
+    T run = carry + block_exclusive_scan<T>(s, lds4, tot);
+#pragma unroll
+    for (int q = 0; q < kTopItems; ++q) {
+      if (base + q < nb) out[base + q] = run;
+      run += v[q];
+    }
+    carry += tot;
+  }
+  if (threadIdx.x == 0 && total_out) *total_out = carry;
+}
+
 // The tiles past the device-side count (dev_n) hold no values: only the first
 // ceil(min(n, dev_n) / kScanTile) partials are scanned.
 template <typename T>
 __global__ __launch_bounds__(kScanThreads) void k_scan_top(T* part, int64_t nb, int64_t n,
                                                            const unsigned long long* dev_n, T* total_out) {
-  __shared__ T lds4[4];
   if (dev_n) nb = min(nb, (min(n, (int64_t)*dev_n) + kScanTile - 1) / kScanTile);
-  T carry = 0;
-  for (int64_t b0 = 0; b0 < nb; b0 += kScanThreads) {
-    const int64_t i = b0 + threadIdx.x;
-    const T v = i < nb ? part[i] : (T)0;
-    T tot;
-    const T ex = block_exclusive_scan<T>(v, lds4, tot);
-    if (i < nb) part[i] = carry + ex;
-    carry += tot;
-  }
-  if (threadIdx.x == 0 && total_out) *total_out = carry;
+  scan_one_block<T>(part, part, nb, total_out);
+}
+
+// A short array (tens of thousands of values) in one launch.
+template <typename T>
+__global__ __launch_bounds__(kScanThreads) void k_scan_one(const T* in, T* out, int64_t n, T* total_out) {
+  scan_one_block<T>(in, out, n, total_out);
 }
 
 template <typename T>
@@ -351,11 +375,18 @@ __global__ __launch_bounds__(256) void k_sort_scan(const uint32_t* __restrict__ 
 
 // Segment starts P_t (t = 0..T; P_0 = 0 and P_T = n, so positions outside every bag,
 // which hold skipped keys, join the first or the last segment) and the first tile of
-// each segment (tbase[T] = number of tiles).  With malformed offsets every key is
-// skipped and the whole stream is one segment.  Also clears the per-table histograms.
+// each segment (tbase[T] = number of tiles), by block 0, which also zeroes the digit
+// counts and tickets (as k_sort_begin does).  With malformed offsets every key is skipped
+// and the whole stream is one segment.  The grid clears the per-table histograms.
 __global__ __launch_bounds__(256) void k_seg_setup(const int32_t* __restrict__ off, int32_t B, int T, int64_t n,
-                                                   const unsigned long long* __restrict__ ctr, SegSort sg) {
+                                                   const unsigned long long* __restrict__ ctr, SegSort sg,
+                                                   uint32_t* __restrict__ ghist, uint32_t* __restrict__ tickets) {
   __shared__ uint32_t lds4[4];
+  const int64_t hw = (int64_t)T * kMaxPasses * 256;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < hw; i += (int64_t)gridDim.x * 256) sg.hist[i] = 0;
+  if (blockIdx.x != 0) return;
+  for (int i = threadIdx.x; i < kMaxPasses * 256; i += blockDim.x) ghist[i] = 0;
+  if (threadIdx.x < kMaxPasses) tickets[threadIdx.x] = 0;
   const bool bad = ctr[kCBadOffsets] != 0;
   const auto start = [&](int t) -> int64_t {
     if (t <= 0) return 0;
@@ -379,8 +410,6 @@ __global__ __launch_bounds__(256) void k_seg_setup(const int32_t* __restrict__ o
     }
     run += tot;
   }
-  const int64_t hw = (int64_t)T * kMaxPasses * 256;
-  for (int64_t i = threadIdx.x; i < hw; i += 256) sg.hist[i] = 0;
 }
 
 // base[t][p][d] = P_t + number of table t's keys whose pass-p digit is below d (one
@@ -597,8 +626,9 @@ hipError_t seg_begin(int64_t n, int passes, const int32_t* off, int32_t B, int T
                      const unsigned long long* ctr, const SortScratch& ss, const SegSort& sg, ExpandHist* eh,
                      hipStream_t s) {
   if (n <= 0 || passes < 1 || passes >= kMaxPasses || n > (int64_t)kStCount || T < 1) return hipErrorInvalidValue;
-  k_sort_begin<<<1, 256, 0, s>>>(ss.ghist, ss.tickets);
-  k_seg_setup<<<1, 256, 0, s>>>(off, B, T, n, ctr, sg);
+  const int64_t hw = (int64_t)T * kMaxPasses * 256;
+  k_seg_setup<<<(unsigned)std::min<int64_t>(64, (hw + 1023) / 1024), 256, 0, s>>>(off, B, T, n, ctr, sg, ss.ghist,
+                                                                                 ss.tickets);
   eh->hist = sg.hist;
   eh->key_base = key_base;
   eh->n_skipped = ss.ghist;
@@ -976,13 +1006,12 @@ __global__ __launch_bounds__(256) void k_uniq_write(Dev dv, const uint32_t* __re
 }
 
 hipError_t launch_unique(const Dev& dv, const uint32_t* sk, int64_t n, unsigned long long* tile_cnt,
-                         unsigned long long* tile_pre, unsigned long long* thread_pre, unsigned long long* part,
-                         uint32_t* uk, uint32_t* seg, uint32_t* set_first, int32_t* utab, unsigned long long* ctr,
+                         unsigned long long* tile_pre, unsigned long long* thread_pre, uint32_t* uk, uint32_t* seg,
+                         uint32_t* set_first, int32_t* utab, unsigned long long* ctr,
                          hipStream_t s) {
   const int64_t tiles = (n + kUqTile - 1) / kUqTile;
   if (tiles > 0) k_uniq_count<<<(unsigned)tiles, 256, 0, s>>>(dv, sk, n, tile_cnt, thread_pre, ctr);
-  hipError_t e = scan_exclusive<unsigned long long>(tile_cnt, tile_pre, tiles, nullptr, part, ctr + kCScanTotal, s);
-  if (e != hipSuccess) return e;
+  k_scan_one<unsigned long long><<<1, kScanThreads, 0, s>>>(tile_cnt, tile_pre, tiles, ctr + kCScanTotal);
   k_uniq_write<<<(unsigned)(tiles > 0 ? tiles : 1), 256, 0, s>>>(dv, sk, n, tile_pre, thread_pre, uk, seg,
                                                                  set_first, utab, ctr);
   return hipGetLastError();

@@ -1107,7 +1107,7 @@ hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int6
   if (e != hipSuccess) return e;
   const uint32_t* sk = in_B ? w.keysB : w.keysA;
   const uint32_t* sv = in_B ? w.valsB : w.valsA;
-  e = launch_unique(d, sk, L, w.tile_cnt, w.tile_pre, w.thread_pre, w.part, w.uniq_key, w.seg, w.set_first, w.utab,
+  e = launch_unique(d, sk, L, w.tile_cnt, w.tile_pre, w.thread_pre, w.uniq_key, w.seg, w.set_first, w.utab,
                     w.ctr, s);
   if (e != hipSuccess) return e;
   const auto grid = [](auto kernel) { return resident_grid(reinterpret_cast<const void*>(kernel)); };
