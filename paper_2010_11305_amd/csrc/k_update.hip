@@ -26,16 +26,6 @@ constexpr int32_t kActDone = 4;  // row fully handled by k_policy
 constexpr int kUnroll = 2;  // independent row loads in flight per row group
 constexpr int64_t kSpreadBelow = 1 << 21;  // lookups per step below which SPREAD kernels run
 
-// After the paired scan of the chunk counts and big-row flags: the chunk total, and the
-// big-row total, also as ubig[nU].
-__global__ void k_scan_totals(Work w) {
-  const unsigned long long tot = w.ctr[kCScanTotal];
-  w.ctr[kCChunks] = tot & 0xFFFFFFFFull;
-  const unsigned long long nb = tot >> 32;
-  w.ctr[kCBig] = nb;
-  w.ubig[w.ctr[kCUnique]] = (uint32_t)nb;
-}
-
 __global__ void k_bwd_begin(Dev dv, unsigned long long* ctr, int64_t L) {
   for (int i = threadIdx.x; i < dv.T; i += blockDim.x) {
     for (int f = kStBwdLookups; f <= kStHitEvictions; ++f) dv.stats[(int64_t)i * kNStat + f] = 0;
@@ -605,8 +595,16 @@ __global__ __launch_bounds__(256) void k_tab_first(Dev dv, Work w, int T) {
 
 // chunk_span[c] = occurrences [x, y) of the sorted stream that chunk c sums, and
 // big_rows[h] = the unique row of big row h (ubig holds the big rows' prefix count).
+// Also, after the paired scan of the chunk counts and big-row flags, the chunk total and
+// the big-row total, the latter also as ubig[nU] (read by the kernels after this one).
 __global__ __launch_bounds__(256) void k_chunk_spans(Work w) {
   const int64_t nU = (int64_t)w.ctr[kCUnique];
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    const unsigned long long tot = w.ctr[kCScanTotal];
+    w.ctr[kCChunks] = tot & 0xFFFFFFFFull;
+    w.ctr[kCBig] = tot >> 32;
+    w.ubig[nU] = (uint32_t)(tot >> 32);
+  }
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < nU; u += stride) {
     const uint32_t n = w.nch[u];
@@ -1115,7 +1113,6 @@ hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int6
   k_tab_first<<<(unsigned)((64 * (int64_t)(d.T + 1) + 255) / 256), 256, 0, s>>>(d, w, d.T);
   e = scan_exclusive_pair(w.nch, w.ubig, w.chunk_base, w.ubig, L, w.ctr + kCUnique, w.part, w.ctr + kCScanTotal, s);
   if (e != hipSuccess) return e;
-  k_scan_totals<<<1, 1, 0, s>>>(w);
   k_chunk_spans<<<grid(k_chunk_spans), 256, 0, s>>>(w);
   // bag blocks of NB = kBlockFloats/d bags (a power of two) for the big rows
   const int nb_shift = __builtin_ctz((unsigned)(kBlockFloats / d.dim));
