@@ -142,6 +142,26 @@ def test_step_parity(torch, case):
         assert s["inserts"] + s["unique_hits"] > 0
 
 
+@pytest.mark.parametrize("case", ["multi_table", "seg_tables_lfu_sr_adagrad", "big_rows_d64_lfu_sr"])
+def test_tables_without_lookups(torch, case):
+    """Steps in which some tables (first, last, in the middle, all but one) have only
+    empty bags: their unique-row ranges are empty, their sort segments hold no key, and
+    the other tables still match the oracle bit for bit, statistics included."""
+    cfg = custom_cfg(**STEP_CASES[case])
+    T = len(cfg["rows"])
+    subsets = [[t for t in range(T) if t not in (1, T - 2)] or [0], [0], [T - 1], list(range(1, T - 1)) or [0],
+               [t for t in range(T) if t % 2 == 1] or [0], list(range(T))]
+    log(f"tables without lookups {case}: T={T} subsets={subsets}")
+    o, g = make_pair(cfg)
+    for k, sub in enumerate(subsets):
+        st = workload.make_step(cfg, k, tables=sub)
+        step_both(o, g, cfg, st, torch)
+        compare_state(o, g, cfg)
+        for t in range(T):
+            if t not in sub:
+                assert g.stats(t)["unique"] == 0
+
+
 HOST_TABLE_CASES = ["tiny", "tiny_int4_fp16_lfu_adagrad", "fp16_sr_lfu_adagrad", "d128_int4_fp16_lru16",
                     "tiny_nocache", "d64_int2_fp16sb_sr_adagrad"]
 
