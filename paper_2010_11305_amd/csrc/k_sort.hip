@@ -647,7 +647,7 @@ hipError_t sort_pairs_segmented(uint32_t* kA, uint32_t* vA, uint32_t* kB, uint32
   if (passes < 1 || passes >= kMaxPasses || n > (int64_t)kStCount || T < 1) return hipErrorInvalidValue;
   const int64_t nb_max = (n + kRadixTile - 1) / kRadixTile + T;  // every segment adds at most one partial tile
   const int64_t sw = 256 * nb_max;
-  uint32_t* n_skipped = ss.ghist;  // zeroed by k_sort_begin
+  uint32_t* n_skipped = ss.ghist;  // zeroed by k_seg_setup
   uint32_t* skip_base = ss.gbase;
   k_seg_scan<<<(unsigned)T, 256, 0, s>>>(sg, passes, n, n_skipped, skip_base);
   for (int pass = 0; pass < passes; ++pass) {
