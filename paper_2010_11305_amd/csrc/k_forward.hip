@@ -241,10 +241,8 @@ __global__ __launch_bounds__(256) void k_fwd_probe(Dev dv, const int32_t* __rest
 // (split columns) rather than [8g, 8g+8): each of the two 16-byte loads of a cache row
 // then reads D/2 contiguous floats across the group (whole 128-byte lines), where with
 // 8 consecutive columns per lane both loads touch every line of the row at half use.
-// Measured: faster at d = 256 (stress workload forward 0.446 -> 0.419 ms), slower at
-// d = 128 (industrial gather 1519 -> 1610 us), so only the widest rows take it.
 template <int D>
-constexpr bool kSplitCols = D >= 256;
+constexpr bool kSplitCols = D >= 128;
 
 template <int D>
 __device__ __forceinline__ void load_frow_split(const float* row, int g, float (&x)[8]) {
@@ -261,26 +259,34 @@ __device__ __forceinline__ void store_frow_split_nt(float* row, int g, const flo
   __builtin_nontemporal_store(f4v{x[4], x[5], x[6], x[7]}, p + D / 8 + g);
 }
 
-// The codes of lane g's split columns, packed as load_code_words packs 8 consecutive ones
-// (element i of the word is column 4g+i for i < 4, D/2+4g+i-4 after): two loads of BITS/2
-// bytes, the second D*BITS/16 bytes further.
+// The codes of lane g's split columns, from the words of load_code_words (8 consecutive
+// columns per lane) moved between the group's lanes, packed as those are (element i is
+// column 4g+i for i < 4, D/2+4g+i-4 after): lane g's split columns are half g%2 of lanes g/2 and
+// LPR/2 + g/2.  Every lane of the group must take part.
 template <int D, int BITS>
-__device__ __forceinline__ CodeWords<BITS> load_code_words_split(const uint8_t* rec, int g) {
+__device__ __forceinline__ CodeWords<BITS> split_code_words(const CodeWords<BITS>& c8, int g) {
+  constexpr int LPR = Geo<D>::LPR;
+  const int s0 = g >> 1, s1 = LPR / 2 + (g >> 1), h = g & 1;
   CodeWords<BITS> c;
-  if constexpr (BITS == 2) {
-    const uint8_t* p = rec;
-    c.w[0] = (uint32_t)p[g] | ((uint32_t)p[D / 8 + g] << 8);
-  } else if constexpr (BITS == 4) {
-    const uint16_t* p = reinterpret_cast<const uint16_t*>(rec);
-    c.w[0] = (uint32_t)p[g] | ((uint32_t)p[D / 8 + g] << 16);
+  if constexpr (BITS == 2 || BITS == 4) {
+    constexpr int HB = 4 * BITS;  // bits of 4 columns
+    const uint32_t m = (1u << HB) - 1u;
+    const uint32_t a = (__shfl(c8.w[0], s0, LPR) >> (HB * h)) & m;
+    const uint32_t b = (__shfl(c8.w[0], s1, LPR) >> (HB * h)) & m;
+    c.w[0] = a | (b << HB);
   } else if constexpr (BITS == 8) {
-    const uint32_t* p = reinterpret_cast<const uint32_t*>(rec);
-    c.w[0] = p[g];
-    c.w[1] = p[D / 8 + g];
+    const uint32_t a0 = __shfl(c8.w[0], s0, LPR), a1 = __shfl(c8.w[1], s0, LPR);
+    const uint32_t b0 = __shfl(c8.w[0], s1, LPR), b1 = __shfl(c8.w[1], s1, LPR);
+    c.w[0] = h ? a1 : a0;
+    c.w[1] = h ? b1 : b0;
   } else {
-    const uint2* p = reinterpret_cast<const uint2*>(rec);
-    const uint2 lo = p[g], hi = p[D / 8 + g];
-    c.w[0] = lo.x; c.w[1] = lo.y; c.w[2] = hi.x; c.w[3] = hi.y;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const uint32_t a0 = __shfl(c8.w[i], s0, LPR), a1 = __shfl(c8.w[2 + i], s0, LPR);
+      const uint32_t b0 = __shfl(c8.w[i], s1, LPR), b1 = __shfl(c8.w[2 + i], s1, LPR);
+      c.w[i] = h ? a1 : a0;
+      c.w[2 + i] = h ? b1 : b0;
+    }
   }
   return c;
 }
@@ -348,8 +354,7 @@ __global__ __launch_bounds__(256) void k_fwd_gather(Dev dv, const int32_t* __res
             } else if (kind[q] == 2) {
               const uint8_t* rec = static_cast<const uint8_t*>(
                   __builtin_assume_aligned(rec0 + (int64_t)(-2 - cq) * RB, Rec<D, BITS, SB16>::ALIGN));
-              if constexpr (kSplitCols<D>) cw[q] = load_code_words_split<D, BITS>(rec, g);
-              else cw[q] = load_code_words<BITS>(rec, g);
+              cw[q] = load_code_words<BITS>(rec, g);  // moved to the split columns after the loads
               sbw[q] = load_sb_words<D, BITS, SB16>(rec);
             }
           }
@@ -359,7 +364,8 @@ __global__ __launch_bounds__(256) void k_fwd_gather(Dev dv, const int32_t* __res
             if (kind[q] == 2) {
               float sq, bq;
               decode_sb<SB16>(sbw[q], sq, bq);
-              dequant8<BITS>(cw[q], sq, bq, raw[q]);
+              if constexpr (kSplitCols<D>) dequant8<BITS>(split_code_words<D, BITS>(cw[q], g), sq, bq, raw[q]);
+              else dequant8<BITS>(cw[q], sq, bq, raw[q]);
             }
 #pragma unroll
             for (int i = 0; i < 8; ++i) acc[i] = acc[i] + raw[q][i];
