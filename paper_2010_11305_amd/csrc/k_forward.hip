@@ -103,7 +103,7 @@ hipError_t launch_init_uniform(const Dev& d, float lo, float hi, uint64_t init_s
 }
 
 // ---- forward --------------------------------------------------------------------------
-// Two passes.  k_fwd_probe: one lane per lookup up to 16 ways, 2 or 4 lanes for 32 or 64
+// Two passes.  k_fwd_probe: one lane per lookup up to 8 ways, 2 lanes for 16 or 32, 4 for 64
 // (tables split over the XCDs), checks the row, probes its set, and write a code: the cache slot (hit), -2-row (miss) or
 // -1 (skipped).  k_fwd_gather: one group of LPR
 // lanes per bag (64/LPR bags per wave), tables split over the XCDs; lane j reads the
@@ -118,10 +118,11 @@ constexpr int kFwdUnroll = 2;
 constexpr int kProbeUnroll = 6, kProbeUnrollSmall = 4;
 constexpr int64_t kProbeSmallBelow = 1 << 21;  // lookups per call
 
-// QL = assoc/W lanes share one lookup (one lane up to 16 ways, W = min(assoc, 16)), each
-// comparing W of the set's tags loaded 16 bytes at a time; every lane group keeps
-// PU lookups in flight (all index loads, then all tag loads).  One lane per lookup pays
-// the set index, the addressing and the store of a lookup once.
+// QL = assoc/W lanes share one lookup (W = assoc up to 8 ways, 8 at 16 ways, 16 beyond),
+// each comparing W of the set's tags loaded 16 bytes at a time; every lane group keeps
+// PU lookups in flight (all index loads, then all tag loads).  At 16 ways two lanes of 8
+// tags are faster than one of 16 (industrial probe 331 -> 303 us: a wave's tag loads
+// then touch 32 sets' lines each instead of 64), four of 4 slower (439 us).
 template <int W, int PU>
 __global__ __launch_bounds__(256) void k_fwd_probe(Dev dv, const int32_t* __restrict__ idx, int64_t L,
                                                    const int32_t* __restrict__ off, int32_t B,
@@ -403,7 +404,8 @@ hipError_t launch_forward(const Dev& d, const Work& w, const int32_t* idx, int64
     };
     const auto probe_w = [&](auto pu) {
       constexpr int PU = decltype(pu)::value;
-      switch (d.assoc < 16 ? d.assoc : 16) {
+      // tags per lane: the whole set up to 8 ways, 8 of 16 (two lanes per lookup), 16 beyond
+      switch (d.assoc <= 8 ? d.assoc : d.assoc == 16 ? 8 : 16) {
         case 1: probe(k_fwd_probe<1, PU>); return hipSuccess;
         case 2: probe(k_fwd_probe<2, PU>); return hipSuccess;
         case 4: probe(k_fwd_probe<4, PU>); return hipSuccess;
