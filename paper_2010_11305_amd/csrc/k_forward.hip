@@ -122,7 +122,8 @@ constexpr int64_t kProbeSmallBelow = 1 << 21;  // lookups per call
 // each comparing W of the set's tags loaded 16 bytes at a time; every lane group keeps
 // PU lookups in flight (all index loads, then all tag loads).  At 16 ways two lanes of 8
 // tags are faster than one of 16 (industrial probe 331 -> 303 us: a wave's tag loads
-// then touch 32 sets' lines each instead of 64), four of 4 slower (439 us).
+// then touch 32 sets' lines each instead of 64), four of 4 slower (439 us); at 32 ways four
+// lanes of 8 are slower than two of 16 (stress workload 86 -> 127 us).
 template <int W, int PU>
 __global__ __launch_bounds__(256) void k_fwd_probe(Dev dv, const int32_t* __restrict__ idx, int64_t L,
                                                    const int32_t* __restrict__ off, int32_t B,
