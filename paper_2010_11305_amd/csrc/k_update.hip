@@ -197,6 +197,35 @@ constexpr int kChunkUnroll = 4;  // gradient rows in flight per row group in a c
 // time, and a row listed more than once in one bag (adjacent occurrences with the
 // same bag) adds the row already in registers instead of loading it again (same
 // operands, same sums).
+// Chunk sums and the fold of block sums at d >= 128 hold split columns per lane ([4g, 4g+4)
+// and [d/2+4g, d/2+4g+4)): each 16-byte load of a row then reads whole lines across the row
+// group.  The sums are per column, so the lane's columns change nothing but the loads.
+template <int D>
+constexpr bool kChunkSplit = D >= 128;
+
+template <int D>
+__device__ __forceinline__ void load_grow(const float* row, int g, float (&x)[8]) {
+  if constexpr (kChunkSplit<D>) {
+    const float4* p = reinterpret_cast<const float4*>(row);
+    const float4 a = p[g], b = p[D / 8 + g];
+    x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+    x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+  } else {
+    load_frow8(row, g, x);
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void store_grow(float* row, int g, const float (&x)[8]) {
+  if constexpr (kChunkSplit<D>) {
+    float4* p = reinterpret_cast<float4*>(row);
+    p[g] = make_float4(x[0], x[1], x[2], x[3]);
+    p[D / 8 + g] = make_float4(x[4], x[5], x[6], x[7]);
+  } else {
+    store_frow8(row, g, x);
+  }
+}
+
 template <int D>
 __device__ __forceinline__ void chunk_sum(const uint32_t* __restrict__ sval, int64_t i0, int64_t i1, GradRows<D> gr,
                                           int g, float (&acc)[8]) {
@@ -257,7 +286,7 @@ __device__ __forceinline__ void chunk_sum(const uint32_t* __restrict__ sval, int
       for (int q = 0; q < U; ++q) {
         v[q] = __shfl(myv, j + q, LPR);
         fresh[q] = j + q < n && v[q] != (q == 0 ? pv : v[q - 1]);
-        if (fresh[q]) load_frow8(gr.row(v[q]), g, x[q]);
+        if (fresh[q]) load_grow<D>(gr.row(v[q]), g, x[q]);
       }
 #pragma unroll
       for (int q = 0; q < U; ++q) {
@@ -321,7 +350,7 @@ __device__ __forceinline__ void fold_blocks(const Work& w, int64_t h, int nblk, 
     for (int q = 0; q < U; ++q) {
       const int k = min(k0 + q, nblk - 1);
       nx[q] = bb[(k + 1) * kStages];
-      load_frow8(bp + (int64_t)k * D, g, x[q]);
+      load_grow<D>(bp + (int64_t)k * D, g, x[q]);
     }
 #pragma unroll
     for (int q = 0; q < U; ++q) {
@@ -350,7 +379,7 @@ __global__ __launch_bounds__(256) void k_block_fold(Work w, int nblk) {
   for (int64_t h = (int64_t)blockIdx.x * GPB + threadIdx.x / LPR; h < nbig; h += (int64_t)gridDim.x * GPB) {
     float acc[8];
     fold_blocks<D>(w, h, nblk, g, acc);
-    store_frow8(w.bpart + h * (int64_t)w.max_nblk * D, g, acc);
+    store_grow<D>(w.bpart + h * (int64_t)w.max_nblk * D, g, acc);
   }
 }
 
@@ -652,7 +681,7 @@ __global__ __launch_bounds__(256) void k_partials(Dev dv, Work w, const uint32_t
       next = w.chunk_span[min<int64_t>(c + gstride, chi - 1)];
       float acc[8];
       chunk_sum<D>(sval, sp.x, sp.y, gr, g, acc);
-      store_frow8(w.partial + c * D, g, acc);
+      store_grow<D>(w.partial + c * D, g, acc);
     }
   }
 }
