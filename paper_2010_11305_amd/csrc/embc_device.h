@@ -1,17 +1,25 @@
 // Device-side building blocks of libembcache (gfx950, wave64).
 //
 // Lane layout of one embedding row of width D: a row is handled by a group of
-// LPR = D/8 consecutive lanes (2..32), and lane g of the group holds the 8
-// contiguous columns [8g, 8g+8).  So an FP32 row is two 16-byte loads per lane,
-// the INT4 codes of a lane are one dword (INT8: two, INT2: a half-word, FP16
-// elements: four dwords), the 8 stochastic-rounding
-// uniforms of a lane are the 8 words of two Philox blocks, and a wave works on
-// 64/LPR rows at once.  The halving-tree sum pairs columns (j, j + h): lanes
-// g and g ^ (h/8) while h >= 8, then inside a lane.
+// LPR = D/8 consecutive lanes (2..32), and lane g of the group holds 8 of its
+// columns as elements 0..7: below d = 128 the contiguous columns [8g, 8g+8); from
+// d = 128 on the split columns [4g, 4g+4) and [D/2+4g, D/2+4g+4) (kSplit), so that
+// each 16-byte load or store of an FP32 row covers D/2 contiguous floats across the
+// group (whole 128-byte lines), where 8 contiguous columns per lane touch every line
+// of the row at half use in both.  An FP32 row is two 16-byte loads per lane, the
+// 8 stochastic-rounding uniforms of a lane are the 8 words of two Philox blocks, and
+// a wave works on 64/LPR rows at once.  The low-precision codes are stored with 8
+// contiguous columns per lane-sized word (INT4: one dword, INT8: two, INT2: a
+// half-word, FP16 elements: four dwords) and moved between the lanes of a group when
+// the row is split.  The halving-tree sum pairs columns (j, j + h): contiguous
+// lanes g and g ^ (h/8) while h >= 8, then inside a lane; split, inside a lane for
+// h = D/2, then lanes g and g ^ (h/4) while h >= 4, then inside a lane.
 #pragma once
 
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
+
+#include <type_traits>
 #include <stdint.h>
 
 #include "embc_internal.h"
@@ -24,6 +32,9 @@ struct Geo {
   static constexpr int LPR = D / CPL;  // lanes per row
   static constexpr int GPW = 64 / LPR; // rows per wave
 };
+
+template <int D>
+constexpr bool kSplit = D >= 128;
 
 // A row record of the low-precision table: the codes (BITS 8, 4, 2) followed by the
 // row's (scale, bias), FP16 pair or FP32 pair; or, for BITS 16, the row's binary16
@@ -104,13 +115,15 @@ __device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1
 
 __device__ __forceinline__ float u24(uint32_t w) { return (float)(w >> 8) * 5.9604644775390625e-08f; }  // 2^-24
 
-// The 8 uniforms of columns [8g, 8g+8) of (table, row) at `step`: column j uses
-// word j%4 of the block with counter (j/4, row, table, step) and key (seed lo, seed hi).
-__device__ __forceinline__ void uniforms8(uint64_t seed, uint32_t step, uint32_t table, uint32_t row, int g,
-                                          float (&u)[8]) {
+// The 8 uniforms of lane g's columns of (table, row) at `step`: column j uses word j%4
+// of the block with counter (j/4, row, table, step) and key (seed lo, seed hi).
+template <int D>
+__device__ __forceinline__ void uniforms_row(uint64_t seed, uint32_t step, uint32_t table, uint32_t row, int g,
+                                             float (&u)[8]) {
   const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
-  const uint4 a = philox4x32_10(make_uint4(2u * g, row, table, step), k0, k1);
-  const uint4 b = philox4x32_10(make_uint4(2u * g + 1u, row, table, step), k0, k1);
+  const uint32_t c0 = kSplit<D> ? (uint32_t)g : 2u * g, c1 = kSplit<D> ? (uint32_t)(D / 8 + g) : 2u * g + 1u;
+  const uint4 a = philox4x32_10(make_uint4(c0, row, table, step), k0, k1);
+  const uint4 b = philox4x32_10(make_uint4(c1, row, table, step), k0, k1);
   u[0] = u24(a.x); u[1] = u24(a.y); u[2] = u24(a.z); u[3] = u24(a.w);
   u[4] = u24(b.x); u[5] = u24(b.y); u[6] = u24(b.z); u[7] = u24(b.w);
 }
@@ -190,6 +203,111 @@ __device__ __forceinline__ CodeWords<BITS> load_code_words(const uint8_t* rec, i
   return c;
 }
 
+// Stores lane g's code words of 8 contiguous columns (the layout of load_code_words;
+// w1 only for INT8), nontemporal: a record is written once per step.
+template <int BITS>
+__device__ __forceinline__ void store_code_words(uint8_t* rec, int g, uint32_t w0, uint32_t w1) {
+  if constexpr (BITS == 2) {
+    __builtin_nontemporal_store((uint16_t)w0, reinterpret_cast<uint16_t*>(rec) + g);
+  } else {
+    uint32_t* p = reinterpret_cast<uint32_t*>(rec) + g * (BITS == 8 ? 2 : 1);
+    __builtin_nontemporal_store(w0, p);
+    if constexpr (BITS == 8) __builtin_nontemporal_store(w1, p + 1);
+  }
+}
+
+// The codes of lane g's split columns, from the words of load_code_words (8 contiguous
+// columns per lane) moved between the group's lanes and packed as those are (element i
+// is column 4g+i for i < 4, D/2+4g+i-4 after): lane g's columns are half g%2 of lanes
+// g/2 and LPR/2 + g/2.  Every lane of the group must take part.
+template <int D, int BITS>
+__device__ __forceinline__ CodeWords<BITS> split_code_words(const CodeWords<BITS>& c8, int g) {
+  constexpr int LPR = Geo<D>::LPR;
+  const int s0 = g >> 1, s1 = LPR / 2 + (g >> 1), h = g & 1;
+  CodeWords<BITS> c;
+  if constexpr (BITS == 2 || BITS == 4) {
+    constexpr int HB = 4 * BITS;  // bits of 4 columns
+    const uint32_t m = (1u << HB) - 1u;
+    const uint32_t a = (__shfl(c8.w[0], s0, LPR) >> (HB * h)) & m;
+    const uint32_t b = (__shfl(c8.w[0], s1, LPR) >> (HB * h)) & m;
+    c.w[0] = a | (b << HB);
+  } else if constexpr (BITS == 8) {
+    const uint32_t a0 = __shfl(c8.w[0], s0, LPR), a1 = __shfl(c8.w[1], s0, LPR);
+    const uint32_t b0 = __shfl(c8.w[0], s1, LPR), b1 = __shfl(c8.w[1], s1, LPR);
+    c.w[0] = h ? a1 : a0;
+    c.w[1] = h ? b1 : b0;
+  } else {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const uint32_t a0 = __shfl(c8.w[i], s0, LPR), a1 = __shfl(c8.w[2 + i], s0, LPR);
+      const uint32_t b0 = __shfl(c8.w[i], s1, LPR), b1 = __shfl(c8.w[2 + i], s1, LPR);
+      c.w[i] = h ? a1 : a0;
+      c.w[2 + i] = h ? b1 : b0;
+    }
+  }
+  return c;
+}
+
+// The codes of lane g's split columns loaded in place, packed as split_code_words packs
+// them: INT2/INT4 the 4 columns [4g, 4g+4) are byte/half-word g and [D/2+4g, D/2+4g+4)
+// byte/half-word D/8+g (a | b << 4*BITS); INT8 dwords g and D/8+g; FP16 dwords 2g, 2g+1
+// and D/4+2g, D/4+2g+1.
+template <int D, int BITS, bool NT = false>
+__device__ __forceinline__ CodeWords<BITS> load_split_code_words(const uint8_t* rec, int g) {
+  const auto ld = [](const auto* p) {
+    if constexpr (NT) return (uint32_t)__builtin_nontemporal_load(p);
+    else return (uint32_t)p[0];
+  };
+  CodeWords<BITS> c;
+  if constexpr (BITS == 2 || BITS == 4) {
+    using W = std::conditional_t<BITS == 2, uint8_t, uint16_t>;
+    const W* p = reinterpret_cast<const W*>(rec);
+    c.w[0] = ld(p + g) | (ld(p + D / 8 + g) << (4 * BITS));
+  } else if constexpr (BITS == 8) {
+    const uint32_t* p = reinterpret_cast<const uint32_t*>(rec);
+    c.w[0] = ld(p + g);
+    c.w[1] = ld(p + D / 8 + g);
+  } else {
+    const uint32_t* p = reinterpret_cast<const uint32_t*>(rec);
+    c.w[0] = ld(p + 2 * g);
+    c.w[1] = ld(p + 2 * g + 1);
+    c.w[2] = ld(p + D / 4 + 2 * g);
+    c.w[3] = ld(p + D / 4 + 2 * g + 1);
+  }
+  return c;
+}
+
+// Stores lane g's split codes (packed as load_split_code_words returns them) in place,
+// nontemporal.
+template <int D, int BITS>
+__device__ __forceinline__ void store_split_code_words(uint8_t* rec, int g, const CodeWords<BITS>& c) {
+  if constexpr (BITS == 2 || BITS == 4) {
+    using W = std::conditional_t<BITS == 2, uint8_t, uint16_t>;
+    constexpr int HB = 4 * BITS;
+    W* p = reinterpret_cast<W*>(rec);
+    __builtin_nontemporal_store((W)(c.w[0] & ((1u << HB) - 1u)), p + g);
+    __builtin_nontemporal_store((W)(c.w[0] >> HB), p + D / 8 + g);
+  } else if constexpr (BITS == 8) {
+    uint32_t* p = reinterpret_cast<uint32_t*>(rec);
+    __builtin_nontemporal_store(c.w[0], p + g);
+    __builtin_nontemporal_store(c.w[1], p + D / 8 + g);
+  } else {
+    uint32_t* p = reinterpret_cast<uint32_t*>(rec);
+    __builtin_nontemporal_store(c.w[0], p + 2 * g);
+    __builtin_nontemporal_store(c.w[1], p + 2 * g + 1);
+    __builtin_nontemporal_store(c.w[2], p + D / 4 + 2 * g);
+    __builtin_nontemporal_store(c.w[3], p + D / 4 + 2 * g + 1);
+  }
+}
+
+// The codes of lane g's columns in the row layout of width D (element i in the slot
+// of column 8g+i of load_code_words).  Every lane of the group must take part.
+template <int D, int BITS>
+__device__ __forceinline__ CodeWords<BITS> row_code_words(const CodeWords<BITS>& c8, int g) {
+  if constexpr (kSplit<D>) return split_code_words<D, BITS>(c8, g);
+  else return c8;
+}
+
 template <int BITS>
 __device__ __forceinline__ uint32_t code_of(const CodeWords<BITS>& c, int i) {
   if constexpr (BITS == 8) return (c.w[i >> 2] >> (8 * (i & 3))) & 0xFFu;
@@ -209,15 +327,6 @@ __device__ __forceinline__ void dequant8(const CodeWords<BITS>& c, float s, floa
 #pragma unroll
     for (int i = 0; i < 8; ++i) x[i] = __builtin_fmaf((float)code_of<BITS>(c, i), s, b);
   }
-}
-
-// fetch() of a non-resident row: q*s + b with one rounding (Alg. 1 dequantization).
-template <int D, int BITS, bool SB16>
-__device__ __forceinline__ void dequant_row(const uint8_t* rec, int g, float (&x)[8]) {
-  float s, b;
-  const CodeWords<BITS> c = load_code_words<BITS>(rec, g);
-  load_sb<D, BITS, SB16>(rec, s, b);
-  dequant8<BITS>(c, s, b, x);
 }
 
 __device__ __forceinline__ void load_frow8(const float* row, int g, float (&x)[8]) {
@@ -249,6 +358,42 @@ __device__ __forceinline__ void store_frow8(float* row, int g, const float (&x)[
   float4* p = reinterpret_cast<float4*>(row) + 2 * g;
   p[0] = make_float4(x[0], x[1], x[2], x[3]);
   p[1] = make_float4(x[4], x[5], x[6], x[7]);
+}
+
+// Lane g's 8 elements of an FP32 row in the row layout of width D: the 16-byte words
+// (g, g + D/8) when split, (2g, 2g + 1) otherwise.
+template <int D>
+__device__ __forceinline__ void load_row(const float* row, int g, float (&x)[8]) {
+  const float4* p = reinterpret_cast<const float4*>(row);
+  const int i0 = kSplit<D> ? g : 2 * g, i1 = kSplit<D> ? D / 8 + g : 2 * g + 1;
+  const float4 a = p[i0], b = p[i1];
+  x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+  x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+}
+
+template <int D>
+__device__ __forceinline__ void load_row_nt(const float* row, int g, float (&x)[8]) {
+  const f4v* p = reinterpret_cast<const f4v*>(row);
+  const int i0 = kSplit<D> ? g : 2 * g, i1 = kSplit<D> ? D / 8 + g : 2 * g + 1;
+  const f4v a = __builtin_nontemporal_load(p + i0), b = __builtin_nontemporal_load(p + i1);
+  x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+  x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+}
+
+template <int D>
+__device__ __forceinline__ void store_row(float* row, int g, const float (&x)[8]) {
+  float4* p = reinterpret_cast<float4*>(row);
+  const int i0 = kSplit<D> ? g : 2 * g, i1 = kSplit<D> ? D / 8 + g : 2 * g + 1;
+  p[i0] = make_float4(x[0], x[1], x[2], x[3]);
+  p[i1] = make_float4(x[4], x[5], x[6], x[7]);
+}
+
+template <int D>
+__device__ __forceinline__ void store_row_nt(float* row, int g, const float (&x)[8]) {
+  f4v* p = reinterpret_cast<f4v*>(row);
+  const int i0 = kSplit<D> ? g : 2 * g, i1 = kSplit<D> ? D / 8 + g : 2 * g + 1;
+  __builtin_nontemporal_store(f4v{x[0], x[1], x[2], x[3]}, p + i0);
+  __builtin_nontemporal_store(f4v{x[4], x[5], x[6], x[7]}, p + i1);
 }
 
 // The binary16 value next to h in increasing (up) or decreasing order, h finite:
@@ -284,19 +429,28 @@ __device__ __forceinline__ uint32_t f16_bits_round(float x, bool sr, float u) {
 // (FP32, correctly rounded; then rounded to FP16 when SB16); codes
 // q = round((x - b)/s) clamped to [0, 2^BITS - 1], all zero when s == 0; a -0
 // extreme is taken as +0.  FP16 table: each element by f16_bits_round.  A record is
-// written once per step (nontemporal stores).
+// written once per step (nontemporal stores).  x holds lane g's columns in the row
+// layout of width D, and a split row's codes are stored in place.  Every lane of the
+// group must take part (the row's minimum and maximum).
 template <int D, int BITS, bool SB16>
 __device__ __forceinline__ void quantize_store(const float (&x)[8], int g, uint8_t* rec, bool sr, uint64_t seed,
                                                uint32_t step, uint32_t table, uint32_t row) {
   if constexpr (BITS == 16) {
     float u[8];
-    if (sr) uniforms8(seed, step, table, row, g, u);
-    uint32_t* p = reinterpret_cast<uint32_t*>(rec) + 4 * g;
+    if (sr) uniforms_row<D>(seed, step, table, row, g, u);
+    uint32_t h2[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const uint32_t lo = f16_bits_round(x[2 * i], sr, sr ? u[2 * i] : 0.0f);
       const uint32_t hi = f16_bits_round(x[2 * i + 1], sr, sr ? u[2 * i + 1] : 0.0f);
-      __builtin_nontemporal_store(lo | (hi << 16), p + i);
+      h2[i] = lo | (hi << 16);
+    }
+    if constexpr (kSplit<D>) {
+      store_split_code_words<D, 16>(rec, g, CodeWords<16>{{h2[0], h2[1], h2[2], h2[3]}});
+    } else {
+      uint32_t* p = reinterpret_cast<uint32_t*>(rec);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) __builtin_nontemporal_store(h2[i], p + 4 * g + i);
     }
     return;
   }
@@ -320,7 +474,7 @@ __device__ __forceinline__ void quantize_store(const float (&x)[8], int g, uint8
     b = f16_round(b);
   }
   float u[8];
-  if (sr && s != 0.0f) uniforms8(seed, step, table, row, g, u);
+  if (sr && s != 0.0f) uniforms_row<D>(seed, step, table, row, g, u);
   uint32_t w0 = 0, w1 = 0;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
@@ -344,12 +498,13 @@ __device__ __forceinline__ void quantize_store(const float (&x)[8], int g, uint8
       w0 |= q << (BITS * i);
     }
   }
-  if constexpr (BITS == 2) {
-    __builtin_nontemporal_store((uint16_t)w0, reinterpret_cast<uint16_t*>(rec) + g);
+  if constexpr (kSplit<D>) {
+    CodeWords<BITS> c;
+    c.w[0] = w0;
+    if constexpr (BITS == 8) c.w[1] = w1;
+    store_split_code_words<D, BITS>(rec, g, c);
   } else {
-    uint32_t* p = reinterpret_cast<uint32_t*>(rec) + g * (BITS == 8 ? 2 : 1);
-    __builtin_nontemporal_store(w0, p);
-    if constexpr (BITS == 8) __builtin_nontemporal_store(w1, p + 1);
+    store_code_words<BITS>(rec, g, w0, w1);
   }
   if (g == 0) {
     uint32_t* ps = reinterpret_cast<uint32_t*>(rec + CB);

@@ -58,7 +58,7 @@ __global__ __launch_bounds__(256) void k_init_uniform(Dev dv, float lo, float hi
     const int t = table_of_row(dv, grow);
     const uint32_t r = (uint32_t)(grow - dv.desc[t].row_base);
     float u[8], x[8];
-    uniforms8(init_seed, 0xFFFFFFFFu, (uint32_t)t, r, g, u);
+    uniforms_row<D>(init_seed, 0xFFFFFFFFu, (uint32_t)t, r, g, u);
 #pragma unroll
     for (int i = 0; i < 8; ++i) x[i] = __builtin_fmaf(u[i], width, lo);
     uint8_t* rec = rec_of<D, BITS, SB16>(dv, grow);
@@ -239,60 +239,6 @@ __global__ __launch_bounds__(256) void k_fwd_probe(Dev dv, const int32_t* __rest
   }
 }
 
-// In the gather, lane g of a row group holds columns [4g, 4g+4) and [D/2+4g, D/2+4g+4)
-// (split columns) rather than [8g, 8g+8): each of the two 16-byte loads of a cache row
-// then reads D/2 contiguous floats across the group (whole 128-byte lines), where with
-// 8 consecutive columns per lane both loads touch every line of the row at half use.
-template <int D>
-constexpr bool kSplitCols = D >= 128;
-
-template <int D>
-__device__ __forceinline__ void load_frow_split(const float* row, int g, float (&x)[8]) {
-  const float4* p = reinterpret_cast<const float4*>(row);
-  const float4 a = p[g], b = p[D / 8 + g];
-  x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
-  x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
-}
-
-template <int D>
-__device__ __forceinline__ void store_frow_split_nt(float* row, int g, const float (&x)[8]) {
-  f4v* p = reinterpret_cast<f4v*>(row);
-  __builtin_nontemporal_store(f4v{x[0], x[1], x[2], x[3]}, p + g);
-  __builtin_nontemporal_store(f4v{x[4], x[5], x[6], x[7]}, p + D / 8 + g);
-}
-
-// The codes of lane g's split columns, from the words of load_code_words (8 consecutive
-// columns per lane) moved between the group's lanes, packed as those are (element i is
-// column 4g+i for i < 4, D/2+4g+i-4 after): lane g's split columns are half g%2 of lanes g/2 and
-// LPR/2 + g/2.  Every lane of the group must take part.
-template <int D, int BITS>
-__device__ __forceinline__ CodeWords<BITS> split_code_words(const CodeWords<BITS>& c8, int g) {
-  constexpr int LPR = Geo<D>::LPR;
-  const int s0 = g >> 1, s1 = LPR / 2 + (g >> 1), h = g & 1;
-  CodeWords<BITS> c;
-  if constexpr (BITS == 2 || BITS == 4) {
-    constexpr int HB = 4 * BITS;  // bits of 4 columns
-    const uint32_t m = (1u << HB) - 1u;
-    const uint32_t a = (__shfl(c8.w[0], s0, LPR) >> (HB * h)) & m;
-    const uint32_t b = (__shfl(c8.w[0], s1, LPR) >> (HB * h)) & m;
-    c.w[0] = a | (b << HB);
-  } else if constexpr (BITS == 8) {
-    const uint32_t a0 = __shfl(c8.w[0], s0, LPR), a1 = __shfl(c8.w[1], s0, LPR);
-    const uint32_t b0 = __shfl(c8.w[0], s1, LPR), b1 = __shfl(c8.w[1], s1, LPR);
-    c.w[0] = h ? a1 : a0;
-    c.w[1] = h ? b1 : b0;
-  } else {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const uint32_t a0 = __shfl(c8.w[i], s0, LPR), a1 = __shfl(c8.w[2 + i], s0, LPR);
-      const uint32_t b0 = __shfl(c8.w[i], s1, LPR), b1 = __shfl(c8.w[2 + i], s1, LPR);
-      c.w[i] = h ? a1 : a0;
-      c.w[2 + i] = h ? b1 : b0;
-    }
-  }
-  return c;
-}
-
 template <int D, int BITS, bool SB16>
 __global__ __launch_bounds__(256) void k_fwd_gather(Dev dv, const int32_t* __restrict__ src, int64_t L,
                                                     const int32_t* __restrict__ off, int32_t B,
@@ -351,12 +297,11 @@ __global__ __launch_bounds__(256) void k_fwd_gather(Dev dv, const int32_t* __res
               else if (cq <= -2 && -2 - cq < nrows) kind[q] = 2;
             }
             if (kind[q] == 1) {
-              if constexpr (kSplitCols<D>) load_frow_split<D>(dv.crow + (int64_t)cq * D, g, raw[q]);
-              else load_frow8(dv.crow + (int64_t)cq * D, g, raw[q]);
+              load_row<D>(dv.crow + (int64_t)cq * D, g, raw[q]);
             } else if (kind[q] == 2) {
               const uint8_t* rec = static_cast<const uint8_t*>(
                   __builtin_assume_aligned(rec0 + (int64_t)(-2 - cq) * RB, Rec<D, BITS, SB16>::ALIGN));
-              cw[q] = load_code_words<BITS>(rec, g);  // moved to the split columns after the loads
+              cw[q] = load_code_words<BITS>(rec, g);  // moved to the row layout after the loads
               sbw[q] = load_sb_words<D, BITS, SB16>(rec);
             }
           }
@@ -366,8 +311,7 @@ __global__ __launch_bounds__(256) void k_fwd_gather(Dev dv, const int32_t* __res
             if (kind[q] == 2) {
               float sq, bq;
               decode_sb<SB16>(sbw[q], sq, bq);
-              if constexpr (kSplitCols<D>) dequant8<BITS>(split_code_words<D, BITS>(cw[q], g), sq, bq, raw[q]);
-              else dequant8<BITS>(cw[q], sq, bq, raw[q]);
+              dequant8<BITS>(row_code_words<D, BITS>(cw[q], g), sq, bq, raw[q]);
             }
 #pragma unroll
             for (int i = 0; i < 8; ++i) acc[i] = acc[i] + raw[q][i];
@@ -379,8 +323,7 @@ __global__ __launch_bounds__(256) void k_fwd_gather(Dev dv, const int32_t* __res
 #pragma unroll
         for (int i = 0; i < 8; ++i) acc[i] = 0.0f;
       }
-      if constexpr (kSplitCols<D>) store_frow_split_nt<D>(out + ((int64_t)b * dv.T + t) * D, g, acc);
-      else store_frow8_nt(out + ((int64_t)b * dv.T + t) * D, g, acc);
+      store_row_nt<D>(out + ((int64_t)b * dv.T + t) * D, g, acc);
     }
   }
 }

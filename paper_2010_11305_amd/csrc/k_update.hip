@@ -142,7 +142,7 @@ __device__ __forceinline__ void sum_occ(const uint32_t* __restrict__ sval, int64
 #pragma unroll
         for (int q = 0; q < US; ++q) {
           const int j = j0 + q;
-          if (j < n) load_frow8(gr.row(__shfl(myv[j / LPR], j % LPR, LPR)), g, x[q]);
+          if (j < n) load_row<D>(gr.row(__shfl(myv[j / LPR], j % LPR, LPR)), g, x[q]);
         }
 #pragma unroll
         for (int q = 0; q < US; ++q) {
@@ -167,14 +167,14 @@ __device__ __forceinline__ void sum_occ(const uint32_t* __restrict__ sval, int64
     const uint32_t myv = (have0 && ic == i0) ? myv0 : (g < n ? sval[ic + g] : 0u);
     int j = 0;
     if (first) {
-      load_frow8(gr.row(__shfl(myv, 0, LPR)), g, acc);
+      load_row<D>(gr.row(__shfl(myv, 0, LPR)), g, acc);
       first = false;
       j = 1;
     }
     for (; j + U <= n; j += U) {
       float x[U][CPL];
 #pragma unroll
-      for (int q = 0; q < U; ++q) load_frow8(gr.row(__shfl(myv, j + q, LPR)), g, x[q]);
+      for (int q = 0; q < U; ++q) load_row<D>(gr.row(__shfl(myv, j + q, LPR)), g, x[q]);
 #pragma unroll
       for (int q = 0; q < U; ++q)
 #pragma unroll
@@ -182,7 +182,7 @@ __device__ __forceinline__ void sum_occ(const uint32_t* __restrict__ sval, int64
     }
     for (; j < n; ++j) {
       float x[CPL];
-      load_frow8(gr.row(__shfl(myv, j, LPR)), g, x);
+      load_row<D>(gr.row(__shfl(myv, j, LPR)), g, x);
 #pragma unroll
       for (int k = 0; k < CPL; ++k) acc[k] = acc[k] + x[k];
     }
@@ -197,35 +197,6 @@ constexpr int kChunkUnroll = 4;  // gradient rows in flight per row group in a c
 // time, and a row listed more than once in one bag (adjacent occurrences with the
 // same bag) adds the row already in registers instead of loading it again (same
 // operands, same sums).
-// Chunk sums and the fold of block sums at d >= 128 hold split columns per lane ([4g, 4g+4)
-// and [d/2+4g, d/2+4g+4)): each 16-byte load of a row then reads whole lines across the row
-// group.  The sums are per column, so the lane's columns change nothing but the loads.
-template <int D>
-constexpr bool kChunkSplit = D >= 128;
-
-template <int D>
-__device__ __forceinline__ void load_grow(const float* row, int g, float (&x)[8]) {
-  if constexpr (kChunkSplit<D>) {
-    const float4* p = reinterpret_cast<const float4*>(row);
-    const float4 a = p[g], b = p[D / 8 + g];
-    x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
-    x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
-  } else {
-    load_frow8(row, g, x);
-  }
-}
-
-template <int D>
-__device__ __forceinline__ void store_grow(float* row, int g, const float (&x)[8]) {
-  if constexpr (kChunkSplit<D>) {
-    float4* p = reinterpret_cast<float4*>(row);
-    p[g] = make_float4(x[0], x[1], x[2], x[3]);
-    p[D / 8 + g] = make_float4(x[4], x[5], x[6], x[7]);
-  } else {
-    store_frow8(row, g, x);
-  }
-}
-
 template <int D>
 __device__ __forceinline__ void chunk_sum(const uint32_t* __restrict__ sval, int64_t i0, int64_t i1, GradRows<D> gr,
                                           int g, float (&acc)[8]) {
@@ -257,7 +228,7 @@ __device__ __forceinline__ void chunk_sum(const uint32_t* __restrict__ sval, int
 #pragma unroll
         for (int q = 0; q < US; ++q) {
           const int j = j0 + q;
-          if (j < n) load_frow8(gr.row(__shfl(myv[j / LPR], j % LPR, LPR)), g, x[q]);
+          if (j < n) load_row<D>(gr.row(__shfl(myv[j / LPR], j % LPR, LPR)), g, x[q]);
         }
 #pragma unroll
         for (int q = 0; q < US; ++q) {
@@ -286,7 +257,7 @@ __device__ __forceinline__ void chunk_sum(const uint32_t* __restrict__ sval, int
       for (int q = 0; q < U; ++q) {
         v[q] = __shfl(myv, j + q, LPR);
         fresh[q] = j + q < n && v[q] != (q == 0 ? pv : v[q - 1]);
-        if (fresh[q]) load_grow<D>(gr.row(v[q]), g, x[q]);
+        if (fresh[q]) load_row<D>(gr.row(v[q]), g, x[q]);
       }
 #pragma unroll
       for (int q = 0; q < U; ++q) {
@@ -312,12 +283,12 @@ template <int D>
 __device__ __forceinline__ void fold_chunks(const float* __restrict__ partial, int64_t c0, uint32_t n, int g,
                                             float (&acc)[8]) {
   constexpr int U = kUnroll;
-  load_frow8(partial + c0 * D, g, acc);
+  load_row<D>(partial + c0 * D, g, acc);
   uint32_t j = 1;
   for (; j + U <= n; j += U) {
     float x[U][8];
 #pragma unroll
-    for (int q = 0; q < U; ++q) load_frow8(partial + (c0 + j + q) * D, g, x[q]);
+    for (int q = 0; q < U; ++q) load_row<D>(partial + (c0 + j + q) * D, g, x[q]);
 #pragma unroll
     for (int q = 0; q < U; ++q)
 #pragma unroll
@@ -325,7 +296,7 @@ __device__ __forceinline__ void fold_chunks(const float* __restrict__ partial, i
   }
   for (; j < n; ++j) {
     float x[8];
-    load_frow8(partial + (c0 + j) * D, g, x);
+    load_row<D>(partial + (c0 + j) * D, g, x);
 #pragma unroll
     for (int k = 0; k < 8; ++k) acc[k] = acc[k] + x[k];
   }
@@ -350,7 +321,7 @@ __device__ __forceinline__ void fold_blocks(const Work& w, int64_t h, int nblk, 
     for (int q = 0; q < U; ++q) {
       const int k = min(k0 + q, nblk - 1);
       nx[q] = bb[(k + 1) * kStages];
-      load_grow<D>(bp + (int64_t)k * D, g, x[q]);
+      load_row<D>(bp + (int64_t)k * D, g, x[q]);
     }
 #pragma unroll
     for (int q = 0; q < U; ++q) {
@@ -379,7 +350,7 @@ __global__ __launch_bounds__(256) void k_block_fold(Work w, int nblk) {
   for (int64_t h = (int64_t)blockIdx.x * GPB + threadIdx.x / LPR; h < nbig; h += (int64_t)gridDim.x * GPB) {
     float acc[8];
     fold_blocks<D>(w, h, nblk, g, acc);
-    store_grow<D>(w.bpart + h * (int64_t)w.max_nblk * D, g, acc);
+    store_row<D>(w.bpart + h * (int64_t)w.max_nblk * D, g, acc);
   }
 }
 
@@ -388,7 +359,7 @@ template <int D>
 __device__ __forceinline__ void merged_grad(const Work& w, const uint32_t* __restrict__ sval, GradRows<D> gr,
                                             int64_t u, int g, float (&acc)[8]) {
   const uint32_t s0 = w.seg[u], s1 = w.seg[u + 1];
-  if (s1 - s0 > kBlockAbove) load_frow8(w.bpart + (int64_t)w.ubig[u] * w.max_nblk * D, g, acc);
+  if (s1 - s0 > kBlockAbove) load_row<D>(w.bpart + (int64_t)w.ubig[u] * w.max_nblk * D, g, acc);
   else if (w.nch[u] > 0) fold_chunks<D>(w.partial, w.chunk_base[u], w.nch[u], g, acc);
   else sum_occ<D>(sval, s0, s1, gr, g, acc);
 }
@@ -681,7 +652,7 @@ __global__ __launch_bounds__(256) void k_partials(Dev dv, Work w, const uint32_t
       next = w.chunk_span[min<int64_t>(c + gstride, chi - 1)];
       float acc[8];
       chunk_sum<D>(sval, sp.x, sp.y, gr, g, acc);
-      store_grow<D>(w.partial + c * D, g, acc);
+      store_row<D>(w.partial + c * D, g, acc);
     }
   }
 }
@@ -699,15 +670,30 @@ __device__ __forceinline__ void apply_optimizer(const Dev& dv, float (&x)[8], co
     for (int i = 0; i < 8; ++i) x[i] = __builtin_fmaf(-dv.lr, gr[i], x[i]);
     return;
   }
+  // the halving tree over the row's squares, in the lanes' column layout
   float a[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) a[i] = gr[i] * gr[i];
+  if constexpr (kSplit<D>) {
+    // h = D/2 pairs element i with i + 4 of the same lane; h = D/4 .. 4 pairs lanes
+    // g and g ^ (h/4); h = 2, 1 are inside the lane
 #pragma unroll
-  for (int i = 0; i < 8; ++i) a[i] = butterfly<LPR>(a[i], [](float p, float q) { return p + q; });
+    for (int i = 0; i < 4; ++i) a[i] = a[i] + a[i + 4];
 #pragma unroll
-  for (int h = 4; h >= 1; h >>= 1)
+    for (int i = 0; i < 4; ++i) a[i] = butterfly<LPR>(a[i], [](float p, float q) { return p + q; });
 #pragma unroll
-    for (int i = 0; i < h; ++i) a[i] = a[i] + a[i + h];
+    for (int h = 2; h >= 1; h >>= 1)
+#pragma unroll
+      for (int i = 0; i < h; ++i) a[i] = a[i] + a[i + h];
+  } else {
+    // h = D/2 .. 8 pairs lanes g and g ^ (h/8); h = 4, 2, 1 are inside the lane
+#pragma unroll
+    for (int i = 0; i < 8; ++i) a[i] = butterfly<LPR>(a[i], [](float p, float q) { return p + q; });
+#pragma unroll
+    for (int h = 4; h >= 1; h >>= 1)
+#pragma unroll
+      for (int i = 0; i < h; ++i) a[i] = a[i] + a[i + h];
+  }
   const float Gn = G_old + a[0] * (1.0f / (float)D);
   if (g == 0) *acc = Gn;
   const float rate = dv.lr / (__builtin_sqrtf(Gn) + dv.eps);
@@ -975,7 +961,7 @@ __global__ __launch_bounds__(256) void k_evict(Dev dv, Work w, const uint32_t* _
         const int64_t vgrow = td.row_base + e_vrow;
         uint8_t* vrec = rec_of<D, BITS, SB16>(dv, vgrow);
         float xv[8];
-        load_frow8_nt(dv.crow + (int64_t)e_dst * D, g, xv);
+        load_row_nt<D>(dv.crow + (int64_t)e_dst * D, g, xv);
         // the displaced row's accumulator leaves the slot for its record (before the
         // insert that takes the slot writes its own there)
         float* acc = dv.optimizer ? acc_of<D, BITS, SB16>(dv, vgrow, vrec) : nullptr;
@@ -1067,18 +1053,19 @@ __global__ __launch_bounds__(256) void k_update(Dev dv, Work w, const uint32_t* 
       float x[8], gr[8];
       // both loads unconditional (a row with more lookups re-reads bag 0's gradient
       // row; the position index is clamped into the row's occurrences, or 0)
-      load_frow8(gtab.row(n == 1 ? m.z : 0u), g, gr);
+      load_row<D>(gtab.row(n == 1 ? m.z : 0u), g, gr);
       const uint32_t myv0 = sval[n == 1 ? 0u : m.z + min<uint32_t>((uint32_t)g, n - 1)];
       CodeWords<BITS> cw;
       SbWords<SB16> sbw;
       if (hit) {
-        load_frow8_nt(dv.crow + (int64_t)(int32_t)m.y * D, g, x);
+        load_row_nt<D>(dv.crow + (int64_t)(int32_t)m.y * D, g, x);
       } else {
-        cw = load_code_words<BITS, true>(rec, g);
+        if constexpr (kSplit<D>) cw = load_split_code_words<D, BITS, true>(rec, g);
+        else cw = load_code_words<BITS, true>(rec, g);
         sbw = load_sb_words<D, BITS, SB16>(rec);
       }
       const float G_old = load_G(dv, acc);
-      if (big) load_frow8(w.bpart + (int64_t)w.ubig[u] * w.max_nblk * D, g, gr);
+      if (big) load_row<D>(w.bpart + (int64_t)w.ubig[u] * w.max_nblk * D, g, gr);
       else if (n > (uint32_t)kSumChunk)
         fold_chunks<D>(w.partial, w.chunk_base[u], (n + kSumChunk - 1) / kSumChunk, g, gr);
       else if (n > 1) sum_occ<D>(sval, m.z, m.z + n, gtab, g, gr, myv0, true);
@@ -1090,7 +1077,7 @@ __global__ __launch_bounds__(256) void k_update(Dev dv, Work w, const uint32_t* 
       apply_optimizer<D>(dv, x, gr, acc_out, g, G_old);
       if (hit || kind == kKindInsert) {
         const int64_t cs = (int32_t)m.y;
-        store_frow8_nt(dv.crow + cs * D, g, x);
+        store_row_nt<D>(dv.crow + cs * D, g, x);
         if (!hit && g == 0) {
           dv.tag[cs] = (int32_t)(grow - td.row_base);
           if (dv.policy == 0) dv.ts[cs] = (int32_t)step;
