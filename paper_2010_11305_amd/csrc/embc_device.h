@@ -203,6 +203,61 @@ __device__ __forceinline__ CodeWords<BITS> load_code_words(const uint8_t* rec, i
   return c;
 }
 
+// The raw words of a record that lane g needs: its code words (as load_code_words
+// returns them) and the record's (scale, bias) words, unpacked by rec_words_unpack once
+// they are needed (so that further loads can be issued first).  INT8: one load per lane
+// that reads the dwords from the first of its own code words on, one or two (the
+// (scale, bias) words) more than it needs, so that the last lane of the group reads the
+// (scale, bias) that follow the codes and the other lanes take them from it; every
+// dword read lies inside the record's codes and (scale, bias), and each read is dword
+// aligned (one vector load of 3 or 4 dwords).  That is done for INT8 rows of d >= 128
+// (the gather of 256-column rows: 0.46 -> 0.44 ms); INT4 and INT2 load the codes and
+// the (scale, bias) apart (the widened load was slower there: 128-column INT4 rows
+// 1.84 -> 1.90 ms), and so do narrower INT8 rows.  FP16: the code words.
+template <int N>
+struct alignas(4) DWords {
+  uint32_t w[N];
+};
+
+template <int D, int BITS, bool SB16>
+struct RecRaw {
+  static constexpr bool kOneLoad = BITS == 8 && kSplit<D>;
+  static constexpr int SBW = SB16 ? 1 : 2;  // (scale, bias) dwords
+  DWords<kOneLoad ? 2 + SBW : 1> v;         // INT8: code words, then (scale, bias) words
+  CodeWords<BITS> c;                        // the others
+  SbWords<SB16> sb;
+};
+
+template <int D, int BITS, bool SB16>
+__device__ __forceinline__ RecRaw<D, BITS, SB16> load_rec_raw(const uint8_t* rec, int g) {
+  using R = RecRaw<D, BITS, SB16>;
+  R r;
+  if constexpr (R::kOneLoad) {
+    r.v = *reinterpret_cast<const DWords<2 + R::SBW>*>(rec + 8 * g);
+  } else {
+    r.c = load_code_words<BITS>(rec, g);
+    if constexpr (BITS != 16) r.sb = load_sb_words<D, BITS, SB16>(rec);
+  }
+  return r;
+}
+
+// Every lane of the group must take part.
+template <int D, int BITS, bool SB16>
+__device__ __forceinline__ void rec_words_unpack(const RecRaw<D, BITS, SB16>& r, CodeWords<BITS>& c,
+                                                 SbWords<SB16>& sb) {
+  using R = RecRaw<D, BITS, SB16>;
+  if constexpr (R::kOneLoad) {
+    constexpr int LPR = Geo<D>::LPR;
+    c.w[0] = r.v.w[0];
+    c.w[1] = r.v.w[1];
+#pragma unroll
+    for (int i = 0; i < R::SBW; ++i) sb.w[i] = __shfl(r.v.w[2 + i], LPR - 1, LPR);
+  } else {
+    c = r.c;
+    sb = r.sb;
+  }
+}
+
 // Stores lane g's code words of 8 contiguous columns (the layout of load_code_words;
 // w1 only for INT8), nontemporal: a record is written once per step.
 template <int BITS>

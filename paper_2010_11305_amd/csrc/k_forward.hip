@@ -285,8 +285,7 @@ __global__ __launch_bounds__(256) void k_fwd_gather(Dev dv, const int32_t* __res
         code_next = pc + LPR + g < p1 ? src[pc + LPR + g] : -1;
         for (int j = 0; j < n; j += FU) {
           float raw[FU][8];
-          CodeWords<BITS> cw[FU];
-          SbWords<SB16> sbw[FU];
+          RecRaw<D, BITS, SB16> rr[FU];
           int kind[FU];  // 0 skip, 1 cache row, 2 low-precision row
 #pragma unroll
           for (int q = 0; q < FU; ++q) {
@@ -301,17 +300,19 @@ __global__ __launch_bounds__(256) void k_fwd_gather(Dev dv, const int32_t* __res
             } else if (kind[q] == 2) {
               const uint8_t* rec = static_cast<const uint8_t*>(
                   __builtin_assume_aligned(rec0 + (int64_t)(-2 - cq) * RB, Rec<D, BITS, SB16>::ALIGN));
-              cw[q] = load_code_words<BITS>(rec, g);  // moved to the row layout after the loads
-              sbw[q] = load_sb_words<D, BITS, SB16>(rec);
+              rr[q] = load_rec_raw<D, BITS, SB16>(rec, g);  // unpacked after the loads
             }
           }
 #pragma unroll
           for (int q = 0; q < FU; ++q) {
             if (kind[q] == 0) continue;
             if (kind[q] == 2) {
+              CodeWords<BITS> cw;
+              SbWords<SB16> sbw;
+              rec_words_unpack<D, BITS, SB16>(rr[q], cw, sbw);
               float sq, bq;
-              decode_sb<SB16>(sbw[q], sq, bq);
-              dequant8<BITS>(row_code_words<D, BITS>(cw[q], g), sq, bq, raw[q]);
+              decode_sb<SB16>(sbw, sq, bq);
+              dequant8<BITS>(row_code_words<D, BITS>(cw, g), sq, bq, raw[q]);
             }
 #pragma unroll
             for (int i = 0; i < 8; ++i) acc[i] = acc[i] + raw[q][i];
