@@ -28,7 +28,7 @@ namespace embc {
 
 template <int D>
 struct Geo {
-  static constexpr int CPL = 8;        // contiguous columns per lane
+  static constexpr int CPL = 8;        // columns per lane (their layout: kSplit)
   static constexpr int LPR = D / CPL;  // lanes per row
   static constexpr int GPW = 64 / LPR; // rows per wave
 };

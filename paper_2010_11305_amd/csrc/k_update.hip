@@ -659,8 +659,9 @@ __global__ __launch_bounds__(256) void k_partials(Dev dv, Work w, const uint32_t
 
 // ---- optimizer (FP32) -----------------------------------------------------------------------
 // SGD: x = fma(-lr, g, x).  Row-wise Adagrad: S = halving-tree sum of g_j^2
-// (a[j] += a[j + h] for h = D/2, ..., 1: across lanes g ^ (h/8) while h >= 8, then
-// inside the lane), G += S * (1/D), r = lr / (sqrt(G) + eps), x = fma(-r, g, x).
+// (a[j] += a[j + h] for h = D/2, ..., 1, the pairs of columns taken across or inside
+// the lanes as the row layout places them), G += S * (1/D), r = lr / (sqrt(G) + eps),
+// x = fma(-r, g, x).
 template <int D>
 __device__ __forceinline__ void apply_optimizer(const Dev& dv, float (&x)[8], const float (&gr)[8], float* acc,
                                                 int g, float G_old) {
