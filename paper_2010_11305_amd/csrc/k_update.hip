@@ -1149,7 +1149,9 @@ hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int6
   if (nblk > 0) k_block_bounds<<<grid(k_block_bounds), 256, 0, s>>>(w, sv, stage_shift, nblk);
   return dispatch_row(d.dim, d.bits, d.sb16, [&]<int D, int BITS, bool SB16>() -> hipError_t {
     // replacement decisions and the write-back of residents displaced without an update
-    // on the side stream, the merged gradients on `s`; joined before the updates
+    // on the side stream, the merged gradients on `s`; joined before the updates (the
+    // packing of the row update's inputs on the side stream, after the decisions: the
+    // block sums beside the eviction 1111 -> 1434 us)
     const bool cached = d.total_slots > 0;
     if (cached) {
       hipError_t e2 = hipEventRecord(side.fork, s);
@@ -1172,7 +1174,10 @@ hipError_t launch_backward(const Dev& d, const Work& w, const int32_t* idx, int6
     if (cached) {
       const hipError_t e2 = hipStreamWaitEvent(s, side.join, 0);
       if (e2 != hipSuccess) return e2;
-      k_evict<D, BITS, SB16, true><<<grid(k_evict<D, BITS, SB16, true>), 256, 0, s>>>(d, w, sv, grad, step);
+      // a resident hit this step is displaced only under LFU or in a direct-mapped LRU
+      // cache (under LRU a hit takes the step's stamp, which no candidate exceeds)
+      if (d.policy != 0 || d.assoc == 1)
+        k_evict<D, BITS, SB16, true><<<grid(k_evict<D, BITS, SB16, true>), 256, 0, s>>>(d, w, sv, grad, step);
     }
     k_pack_meta<<<grid(k_pack_meta), 256, 0, s>>>(w, sv);
     if (update_events) {
