@@ -171,10 +171,6 @@ __device__ __forceinline__ void decode_sb(const SbWords<SB16>& r, float& s, floa
   }
 }
 
-template <int D, int BITS, bool SB16>
-__device__ __forceinline__ void load_sb(const uint8_t* rec, float& s, float& b) {
-  decode_sb<SB16>(load_sb_words<D, BITS, SB16>(rec), s, b);
-}
 
 // Raw code words of lane g: INT2 one half-word (column 8g+i in bits 2i..2i+1), INT4
 // one dword (column 8g+i in nibble i), INT8 two dwords (column 8g+i in byte i), FP16
@@ -384,36 +380,10 @@ __device__ __forceinline__ void dequant8(const CodeWords<BITS>& c, float s, floa
   }
 }
 
-__device__ __forceinline__ void load_frow8(const float* row, int g, float (&x)[8]) {
-  const float4* p = reinterpret_cast<const float4*>(row) + 2 * g;
-  const float4 a = p[0], b = p[1];
-  x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
-  x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
-}
-
 // Nontemporal forms for data touched once per kernel (a row fetched and written back,
 // a pooled output): the hint keeps such lines from displacing, in L2, the lines that
 // other lanes still read (gradient rows, hot cache rows).
 typedef float f4v __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ void load_frow8_nt(const float* row, int g, float (&x)[8]) {
-  const f4v* p = reinterpret_cast<const f4v*>(row) + 2 * g;
-  const f4v a = __builtin_nontemporal_load(p), b = __builtin_nontemporal_load(p + 1);
-  x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
-  x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
-}
-
-__device__ __forceinline__ void store_frow8_nt(float* row, int g, const float (&x)[8]) {
-  f4v* p = reinterpret_cast<f4v*>(row) + 2 * g;
-  __builtin_nontemporal_store(f4v{x[0], x[1], x[2], x[3]}, p);
-  __builtin_nontemporal_store(f4v{x[4], x[5], x[6], x[7]}, p + 1);
-}
-
-__device__ __forceinline__ void store_frow8(float* row, int g, const float (&x)[8]) {
-  float4* p = reinterpret_cast<float4*>(row) + 2 * g;
-  p[0] = make_float4(x[0], x[1], x[2], x[3]);
-  p[1] = make_float4(x[4], x[5], x[6], x[7]);
-}
 
 // Lane g's 8 elements of an FP32 row in the row layout of width D: the 16-byte words
 // (g, g + D/8) when split, (2g, 2g + 1) otherwise.
