@@ -142,6 +142,39 @@ def test_step_parity(torch, case):
         assert s["inserts"] + s["unique_hits"] > 0
 
 
+# Rows of 128 and 256 columns are handled with split columns per lane (columns [4g, 4g+4)
+# and [d/2+4g, d/2+4g+4)), their codes loaded and stored in place in the row update and
+# the eviction, and INT8 codes read with their (scale, bias) in one load in the gather:
+# every code width and (scale, bias) format at both widths, with stochastic rounding and
+# row-wise Adagrad, under LRU (inserts and bypasses), direct-mapped LRU and LFU (residents
+# updated and then displaced).
+WIDE_POLICIES = {"lru": {"policy": "lru", "assoc": 4}, "direct": {"policy": "lru", "assoc": 1},
+                 "lfu": {"policy": "lfu", "assoc": 4, "lfu_decay_interval": 2}}
+WIDE_CASES = [(d, b, sb, pol) for d in (128, 256) for (b, sb) in ((8, False), (8, True), (4, False), (4, True),
+                                                                    (2, False), (2, True), (16, False))
+              for pol in WIDE_POLICIES]
+
+
+@pytest.mark.parametrize("dim,bits,sb16,policy", WIDE_CASES)
+def test_wide_row_layouts(torch, dim, bits, sb16, policy):
+    cfg = custom_cfg(rows=[600, 37], dim=dim, bits=bits, sb_fp16=sb16, cache_fraction=0.05, rounding="stochastic",
+                     optimizer="adagrad", lr=0.05, batch=96, pooling=("uniform", 1, 5), zipf=1.2,
+                     **WIDE_POLICIES[policy])
+    log(f"wide rows dim={dim} bits={bits} sb16={sb16} policy={policy}")
+    o, g = make_pair(cfg)
+    tot = {"inserts": 0, "bypasses": 0, "hit_evictions": 0}
+    for k in range(6):
+        st = workload.make_step(cfg, k)
+        step_both(o, g, cfg, st, torch)
+        compare_state(o, g, cfg)
+        s = o.stats(0)
+        for n in tot:
+            tot[n] += s[n]
+    assert tot["inserts"] > 0 and tot["bypasses"] > 0
+    if policy != "lru":
+        assert tot["hit_evictions"] > 0
+
+
 @pytest.mark.parametrize("case", ["multi_table", "seg_tables_lfu_sr_adagrad", "big_rows_d64_lfu_sr"])
 def test_tables_without_lookups(torch, case):
     """Steps in which some tables (first, last, in the middle, all but one) have only
