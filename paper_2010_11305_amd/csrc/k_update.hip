@@ -1014,8 +1014,8 @@ __global__ __launch_bounds__(256) void k_pack_meta(Work w, const uint32_t* __res
 // 97-102 VGPRs (4 waves) the 128-column INT2 and FP16 tables took 1950 and 1916 us
 // (1767, 1765 held); INT4 and the 256-column INT8 table are unchanged by it.
 template <int D, int BITS, bool SB16, bool SPREAD>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kSplit<D> ? 5 : 1))) void k_update(Dev dv, Work w, const uint32_t* __restrict__ sval,
-                                                const float* __restrict__ grad, uint32_t step) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kSplit<D> ? 5 : 1)))
+void k_update(Dev dv, Work w, const uint32_t* __restrict__ sval, const float* __restrict__ grad, uint32_t step) {
   constexpr int LPR = Geo<D>::LPR;
   constexpr int GPB = 256 / LPR;
   const int g = threadIdx.x & (LPR - 1);
